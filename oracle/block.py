@@ -1,0 +1,110 @@
+"""One DiT block over a pack of nodes -- oracle, test infrastructure only.
+
+The paper fixes only the network's role (F_theta in Eq. 1, reading the
+context of each node through the visibility mask of Eq. 6).  The block form
+is the Wan-shaped reading used for the workload (parity unpinned against a
+real model; no trained weights exist here):
+
+    h  = RMSNorm(x)                          eps = 1e-6, unit gain
+    q, k, v = h Wq^T, h Wk^T, h Wv^T          heads of d channels
+    q, k = RoPE(q), RoPE(k)                   at each token's (t, h, w) position
+    o  = attention of each node over its selected states (Eq. 6)
+    x' = x + o Wo^T
+    y  = x' + GELU_tanh(RMSNorm(x') Wup^T) Wdown^T
+
+Weights are in [out, in] layout (y = x W^T); Wqkv stacks Wq, Wk, Wv along
+its output axis.  Every product here is an fp64 numpy matmul.  The K and V a
+node produces become the cached representation of its state (Sec. 3.2,
+"Effective context and visibility"): later nodes read them.
+"""
+from __future__ import annotations
+
+import math
+from typing import Callable, Dict, Optional, Sequence, Tuple
+
+import numpy as np
+
+from .attention import node_attention
+from .rope import chunk_positions, rope
+
+RMS_EPS = 1e-6
+
+
+def rmsnorm(x: np.ndarray, eps: float = RMS_EPS) -> np.ndarray:
+    x = np.asarray(x, dtype=np.float64)
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps)
+
+
+def gelu_tanh(x: np.ndarray) -> np.ndarray:
+    x = np.asarray(x, dtype=np.float64)
+    return 0.5 * x * (1.0 + np.tanh(math.sqrt(2.0 / math.pi) * (x + 0.044715 * x ** 3)))
+
+
+class BlockShape:
+    def __init__(self, hidden=1536, heads=12, head_dim=128, mlp=8960,
+                 frames_per_chunk=3, grid_h=30, grid_w=52, rope_dims=(44, 42, 42),
+                 theta=10000.0):
+        self.hidden, self.heads, self.head_dim, self.mlp = hidden, heads, head_dim, mlp
+        self.frames_per_chunk, self.grid_h, self.grid_w = frames_per_chunk, grid_h, grid_w
+        self.rope_dims, self.theta = tuple(rope_dims), theta
+
+    @property
+    def tokens_per_chunk(self):
+        return self.frames_per_chunk * self.grid_h * self.grid_w
+
+
+def project_kv(x: np.ndarray, chunk: int, w_qkv: np.ndarray, shp: BlockShape):
+    """Rotated K and plain V of one node's tokens: x [Nq, hidden] -> [Nq, H, d] x 2."""
+    D = shp.hidden
+    h = rmsnorm(x)
+    w = np.asarray(w_qkv, dtype=np.float64)
+    k = (h @ w[D:2 * D].T).reshape(-1, shp.heads, shp.head_dim)
+    v = (h @ w[2 * D:3 * D].T).reshape(-1, shp.heads, shp.head_dim)
+    pos = chunk_positions(chunk, shp.frames_per_chunk, shp.grid_h, shp.grid_w)
+    return rope(k, pos, shp.rope_dims, shp.theta), v
+
+
+def project_q(x: np.ndarray, chunk: int, w_qkv: np.ndarray, shp: BlockShape, rows=None):
+    D = shp.hidden
+    x = np.asarray(x, dtype=np.float64)
+    pos = chunk_positions(chunk, shp.frames_per_chunk, shp.grid_h, shp.grid_w)
+    if rows is not None:
+        x, pos = x[rows], pos[rows]
+    h = rmsnorm(x)
+    q = (h @ np.asarray(w_qkv, dtype=np.float64)[0:D].T).reshape(-1, shp.heads, shp.head_dim)
+    return rope(q, pos, shp.rope_dims, shp.theta)
+
+
+def block_forward(sel, x_of: Callable[[int], np.ndarray], weights: Dict[str, np.ndarray],
+                  resident_kv: Callable[[Tuple[int, int]], Tuple[np.ndarray, np.ndarray]],
+                  shp: BlockShape, rows: Optional[Sequence[int]] = None):
+    """Run one block for every node of ``sel``.
+
+    x_of(i) gives node i's input [Nq, hidden].  resident_kv(state) gives the
+    cached (rotated K, V) of a state that no pack node produces.  ``rows``
+    restricts the outputs to those token rows of every node (the K/V of all
+    rows are still computed, since every row reads all of them).
+    Returns ({i: y_i}, {i: (k_i, v_i)}).
+    """
+    new_kv = {}
+    for i, (c, j) in enumerate(sel.nodes):
+        new_kv[i] = project_kv(x_of(i), c, weights["w_qkv"], shp)
+    index_of = {node: i for i, node in enumerate(sel.nodes)}
+
+    def kv_of(state):
+        if state in index_of:
+            return new_kv[index_of[state]]
+        return resident_kv(state)
+
+    scale = 1.0 / math.sqrt(shp.head_dim)
+    out = {}
+    for i, (c, j) in enumerate(sel.nodes):
+        x = np.asarray(x_of(i), dtype=np.float64)
+        if rows is not None:
+            x = x[rows]
+        q = project_q(x_of(i), c, weights["w_qkv"], shp, rows)
+        o = node_attention(q, sel.segments(i), kv_of, scale).reshape(q.shape[0], -1)
+        x1 = x + o @ np.asarray(weights["w_o"], dtype=np.float64).T
+        u = rmsnorm(x1) @ np.asarray(weights["w_up"], dtype=np.float64).T
+        out[i] = x1 + gelu_tanh(u) @ np.asarray(weights["w_down"], dtype=np.float64).T
+    return out, new_kv

@@ -1,0 +1,163 @@
+"""Pins of the oracle's RoPE, RMSNorm, GELU, block and pipeline (CPU only).
+
+RoPE and the block form are readings (the paper defines neither): their pins
+are mathematical properties that any correct implementation of the stated
+reading satisfies, plus special cases with closed forms.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from oracle.block import BlockShape, block_forward, gelu_tanh, rmsnorm
+from oracle.pipeline import pipeline_rounds, run_stack, serial_order
+from oracle.policy import policy, select
+from oracle.rope import chunk_positions, rope
+from synth import normal
+
+DIMS = (12, 10, 10)
+
+
+def _pos(n, seed):
+    rng = np.random.default_rng(seed)
+    return rng.integers(0, 60, size=(n, 3))
+
+
+def test_rope_identity_at_origin_and_norm():
+    x = normal((7, 3, 32), (1,)).astype(np.float64)
+    np.testing.assert_array_equal(rope(x, np.zeros((7, 3), dtype=int), DIMS), x)
+    y = rope(x, _pos(7, 0), DIMS)
+    np.testing.assert_allclose(np.linalg.norm(y, axis=2), np.linalg.norm(x, axis=2), rtol=1e-13)
+    # each channel pair keeps its own length (a rotation inside the pair)
+    np.testing.assert_allclose(y[..., 0::2] ** 2 + y[..., 1::2] ** 2,
+                               x[..., 0::2] ** 2 + x[..., 1::2] ** 2, rtol=1e-12, atol=1e-14)
+
+
+def test_rope_relative_positions():
+    """<R(p+s) q, R(p'+s) k> == <R(p) q, R(p') k> for any shift s of all axes."""
+    q = normal((5, 2, 32), (2,)).astype(np.float64)
+    k = normal((5, 2, 32), (3,)).astype(np.float64)
+    p1, p2 = _pos(5, 1), _pos(5, 2)
+    shift = np.array([[7, 3, 11]])
+    a = np.einsum("nhd,mhd->hnm", rope(q, p1, DIMS), rope(k, p2, DIMS))
+    b = np.einsum("nhd,mhd->hnm", rope(q, p1 + shift, DIMS), rope(k, p2 + shift, DIMS))
+    np.testing.assert_allclose(a, b, atol=1e-11)
+
+
+def test_rope_composes_and_first_pair_rotates_by_position():
+    x = normal((4, 1, 32), (4,)).astype(np.float64)
+    p1, p2 = _pos(4, 3), _pos(4, 4)
+    np.testing.assert_allclose(rope(rope(x, p1, DIMS), p2, DIMS), rope(x, p1 + p2, DIMS), atol=1e-12)
+    # the first pair of each axis has frequency 1: its angle moves by the position
+    pos = np.array([[1, 0, 0], [0, 2, 0], [0, 0, 3], [0, 0, 0]])
+    y = rope(x, pos, DIMS)
+    starts = [0, DIMS[0] // 2, (DIMS[0] + DIMS[1]) // 2]
+    for a, p in enumerate(starts):
+        ang_x = np.arctan2(x[a, 0, 2 * p + 1], x[a, 0, 2 * p])
+        ang_y = np.arctan2(y[a, 0, 2 * p + 1], y[a, 0, 2 * p])
+        delta = (ang_y - ang_x - pos[a, a]) % (2 * math.pi)
+        assert min(delta, 2 * math.pi - delta) < 1e-12
+
+
+def test_chunk_positions():
+    pos = chunk_positions(2, 3, 2, 4)
+    assert pos.shape == (24, 3)
+    assert list(pos[0]) == [6, 0, 0] and list(pos[5]) == [6, 1, 1] and list(pos[23]) == [8, 1, 3]
+
+
+def test_rmsnorm_and_gelu():
+    x = 3.0 * normal((10, 64), (5,)).astype(np.float64)
+    r = rmsnorm(x)
+    np.testing.assert_allclose(np.sqrt(np.mean(r * r, axis=1)), 1.0, rtol=1e-6)
+    # tanh GELU vs the exact erf GELU: the approximation error is below 1e-3
+    t = np.linspace(-8, 8, 4001)
+    exact = np.array([0.5 * v * (1 + math.erf(v / math.sqrt(2))) for v in t])
+    assert np.max(np.abs(gelu_tanh(t) - exact)) < 1e-3
+    assert gelu_tanh(np.array([0.0]))[0] == 0.0
+    np.testing.assert_allclose(gelu_tanh(np.array([20.0, -20.0])), [20.0, 0.0], atol=1e-12)
+
+
+def _tiny_shape():
+    return BlockShape(hidden=32, heads=2, head_dim=16, mlp=48, frames_per_chunk=2,
+                      grid_h=2, grid_w=3, rope_dims=(6, 6, 4))
+
+
+def _weights(shp, layer, seed=0, zero_out=False):
+    D, M = shp.hidden, shp.mlp
+    w = {"w_qkv": normal((3 * D, D), (seed, 10, layer), 0.2).astype(np.float64),
+         "w_o": normal((D, D), (seed, 11, layer), 0.2).astype(np.float64),
+         "w_up": normal((M, D), (seed, 12, layer), 0.2).astype(np.float64),
+         "w_down": normal((D, M), (seed, 13, layer), 0.2).astype(np.float64)}
+    if zero_out:
+        w["w_o"][:] = 0
+        w["w_down"][:] = 0
+    return w
+
+
+def test_block_identity_with_zero_output_weights():
+    shp = _tiny_shape()
+    sel = select(policy("prog", 4, 2), [(0, 4)])
+    x = normal((shp.tokens_per_chunk, shp.hidden), (1, 4)).astype(np.float64)
+    y, kv = block_forward(sel, lambda i: x, _weights(shp, 0, zero_out=True), None, shp)
+    np.testing.assert_array_equal(y[0], x)
+
+
+def test_block_single_token_attention_is_value_projection():
+    """With one token per chunk and no history, attention returns that token's V."""
+    shp = BlockShape(hidden=32, heads=2, head_dim=16, mlp=48, frames_per_chunk=1,
+                     grid_h=1, grid_w=1, rope_dims=(6, 6, 4))
+    w = _weights(shp, 0)
+    w["w_up"][:] = 0                                   # MLP branch vanishes
+    sel = select(policy("clean", 4, 0), [(3, 2)])
+    x = normal((1, shp.hidden), (2,)).astype(np.float64)
+    y, _ = block_forward(sel, lambda i: x, w, None, shp)
+    h = rmsnorm(x)
+    v = h @ w["w_qkv"][2 * shp.hidden:].T
+    np.testing.assert_allclose(y[0], x + v @ w["w_o"].T, atol=1e-12)
+
+
+def test_block_rows_subset_matches_full():
+    shp = _tiny_shape()
+    pack = [(1, 1), (2, 2)]
+    sel = select(policy("prog", 4, 2), pack)
+    xs = [normal((shp.tokens_per_chunk, shp.hidden), (3, i)).astype(np.float64) for i in range(2)]
+    res = {(0, 0): tuple(normal((shp.tokens_per_chunk, 2, 16), (3, t, 0)).astype(np.float64) for t in (2, 3))}
+    full, _ = block_forward(sel, lambda i: xs[i], _weights(shp, 0), res.__getitem__, shp)
+    rows = [0, 5, 11]
+    part, _ = block_forward(sel, lambda i: xs[i], _weights(shp, 0), res.__getitem__, shp, rows=rows)
+    for i in range(2):
+        np.testing.assert_array_equal(part[i], full[i][rows])
+
+
+def test_pipeline_counts():
+    """K + B - 1 rounds and B*K updates (Sec. 3.3); with the refresh node
+    K + B rounds and B*(K+1) forwards; first clean chunk after K rounds."""
+    B, K = 16, 4
+    r = pipeline_rounds(B, K, refresh=False)
+    assert len(r) == K + B - 1 and sum(len(p) for p in r) == B * K
+    assert sorted(n for p in r for n in p) == sorted((c, j) for c in range(B) for j in range(1, K + 1))
+    finishing = [n for n, p in enumerate(r) if any(j == 1 for _, j in p)]
+    assert finishing[0] == K - 1 and finishing == list(range(K - 1, K - 1 + B))
+    rr = pipeline_rounds(B, K, refresh=True)
+    assert len(rr) == K + B and sum(len(p) for p in rr) == B * (K + 1)
+    assert max(len(p) for p in rr) == K + 1
+    assert rr[10] == [(6, 0), (7, 1), (8, 2), (9, 3), (10, 4)]
+    s = serial_order(B, K, refresh=False)
+    assert len(s) == B * K and s[:K] == [(0, 4), (0, 3), (0, 2), (0, 1)]
+
+
+def test_serial_and_pipelined_progressive_agree_bitwise():
+    """Serial execution admits progressive history when states are retained
+    (Sec. 3.3); the pipelined schedule computes the same updates."""
+    shp = _tiny_shape()
+    B, K, L = 5, 3, 2
+    pol = policy("prog", K, 2)
+    noise = lambda c, j: normal((shp.tokens_per_chunk, shp.hidden), (9, 20, c, j))
+    weights = {l: _weights(shp, l) for l in range(L)}
+    pipe, _, _ = run_stack(pipeline_rounds(B, K, True), pol, L, weights.__getitem__, noise, shp,
+                           t_sched=(0.0, 0.5, 0.75, 1.0))
+    ser, _, _ = run_stack([[n] for n in serial_order(B, K, True)], pol, L, weights.__getitem__, noise,
+                          shp, t_sched=(0.0, 0.5, 0.75, 1.0), release=False)
+    assert set(pipe) == set(ser) and len(pipe) == B * (K + 1)
+    for node in pipe:
+        assert np.array_equal(pipe[node], ser[node]), node
