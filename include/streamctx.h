@@ -1,0 +1,225 @@
+/*
+ * streamctx -- packed causal-context DiT step on MI355X (gfx950).
+ *
+ * C ABI of the hot path of progressive-history pipelining from "Rethinking
+ * Streaming Video Diffusion Model: Context, Execution, and Training":
+ * several in-flight denoising nodes (chunk, level) run as one forward, and
+ * every node attends over the cached keys/values of the historical states its
+ * context policy selects.
+ *
+ * Conventions shared by every call
+ *  - Return codes: SC_OK (0) or a negative SC_E* code.  The message of the
+ *    last failing call on the calling thread is returned by sc_last_error().
+ *    No C++ exception crosses this boundary.
+ *  - Nodes: chunk c is 0-based (the paper's b = c + 1); level 0 is the clean
+ *    endpoint x^0 and level K the initial noise x^K (Sec. 3.1).
+ *  - Device pointers are plain HIP device addresses owned by the caller; the
+ *    library never allocates device memory.  Device work is enqueued on the
+ *    given stream (sc_stream is a hipStream_t; NULL is the null stream) and
+ *    runs asynchronously.  Host-side table work completes before the call
+ *    returns.
+ *  - Handles are not thread-safe; one handle is used by one thread at a time.
+ *  - bf16 tensors are raw bfloat16 bit patterns (uint16), fp32 tensors IEEE
+ *    binary32.
+ */
+#ifndef STREAMCTX_H
+#define STREAMCTX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SC_ABI_VERSION 1
+
+enum {
+  SC_OK = 0,
+  SC_EINVAL = -1,        /* bad argument, policy or node set            */
+  SC_EUNAVAILABLE = -2,  /* a selected state is neither cached nor produced in the pack */
+  SC_ECAPACITY = -3,     /* not enough free page slots                  */
+  SC_EEXIST = -4,        /* state's K/V for this layer already written  */
+  SC_ENOTFOUND = -5,     /* state not in the cache                      */
+  SC_ESTALE = -6,        /* plan refers to a slot released since it was built */
+  SC_EDEVICE = -7,       /* HIP runtime error                           */
+  SC_EUNSUPPORTED = -8   /* shape or dtype this build has no kernel for */
+};
+
+enum { SC_POLICY_CLEAN = 0, SC_POLICY_SAME = 1, SC_POLICY_PROG = 2, SC_POLICY_TABLE = 3 };
+enum { SC_DTYPE_BF16 = 0, SC_DTYPE_F32 = 1 };
+
+typedef void* sc_stream; /* hipStream_t */
+
+typedef struct {
+  int32_t chunk; /* 0-based chunk index c              */
+  int32_t level; /* noise level j, 0 (clean) .. K      */
+} sc_node;
+
+/* History selection policy, Sec. 3.2 Eq. 4-5.  For a node (c, j) the offsets
+ * r = min(W, c) .. 1 with r_mask[j*W + r-1] != 0 (all of them when r_mask is
+ * NULL) select the state of chunk c - r at level phi(j, r):
+ *   SC_POLICY_CLEAN  phi = 0
+ *   SC_POLICY_SAME   phi = j
+ *   SC_POLICY_PROG   phi = max(j - r, 0)
+ *   SC_POLICY_TABLE  phi = phi_table[j*W + r-1]   (entries in [0, K])
+ * The arrays are read during sc_selection_build only. */
+typedef struct {
+  int32_t kind;
+  int32_t K;                 /* number of noise levels above clean, >= 1 */
+  int32_t W;                 /* history window in chunks, >= 0           */
+  const int8_t* phi_table;   /* (K+1) x W, kind TABLE only, else NULL    */
+  const uint8_t* r_mask;     /* (K+1) x W or NULL (dense offsets)        */
+} sc_policy;
+
+typedef struct sc_selection sc_selection;
+typedef struct sc_cache sc_cache;
+typedef struct sc_plan sc_plan;
+
+int sc_abi_version(void);
+const char* sc_last_error(void);
+const char* sc_status_name(int status);
+
+/* ---- Selection table (Sec. 3.2, Eq. 4-5) -------------------------------
+ * Builds the canonical table of a pack of n distinct nodes (pack order is the
+ * caller's).  Node i's segments are its selected history states from the
+ * oldest chunk to the newest, then its own state (c, j): a query chunk sees
+ * its own tokens (Eq. 6 text: within-chunk attention is bidirectional).
+ * seg_src[s] is the index of the pack node that produces state s in this
+ * pack (in-pack history, or the node itself), else -1 (must be cached).
+ * Errors: SC_EINVAL for K < 1, W < 0, an unknown kind, a phi entry outside
+ * [0, K], a node with chunk < 0 or level outside [0, K], or a duplicate node.
+ * The returned handle owns every array; free it with sc_selection_free. */
+int sc_selection_build(const sc_policy* policy, const sc_node* nodes, int32_t n,
+                       sc_selection** out);
+int sc_selection_get(const sc_selection* sel, int32_t* n_nodes, int32_t* n_segments,
+                     const int32_t** seg_off, const int32_t** seg_chunk,
+                     const int32_t** seg_level, const int32_t** seg_src);
+/* Node-level visibility (the chunk-level form of Eq. 6's mask M): the
+ * distinct states read by the pack, sorted by (chunk, level), and a row-major
+ * n_nodes x n_states 0/1 matrix. */
+int sc_visibility_get(const sc_selection* sel, int32_t* n_states, const sc_node** states,
+                      const uint8_t** vis);
+void sc_selection_free(sc_selection* sel);
+
+/* ---- Paged history KV cache (Sec. 3.2, "Effective context") ------------
+ * The representations of selected states are cached keys/values.  One page
+ * slot holds one latent frame (tokens_per_page tokens) of one state, for
+ * every layer; a state occupies pages_per_chunk slots, the same slot ids in
+ * every layer.  The pool is caller device memory of sc_cache_pool_bytes():
+ *   pool[layer][slot] = { K[head][token][d], V[head][d][token] }
+ * (V is stored transposed: the attention kernel reads it as the A operand of
+ * O^T = V^T P^T).  Slots are handed out lowest-free-first.  Requirements:
+ * tokens_per_page a positive multiple of 8, head_dim 64 or 128 (bf16: 128).
+ * The pool must outlive the cache handle. */
+typedef struct {
+  int32_t n_layers, n_heads, head_dim, tokens_per_page, pages_per_chunk, n_slots, dtype;
+} sc_cache_desc;
+
+size_t sc_cache_pool_bytes(const sc_cache_desc* desc);
+int sc_cache_create(const sc_cache_desc* desc, void* dev_pool, sc_cache** out);
+void sc_cache_free(sc_cache* cache);
+/* 1 when the state holds slots (appended or reserved by a plan), 0 if not;
+ * with layer >= 0, 1 only when that layer has been written. */
+int sc_cache_contains(const sc_cache* cache, sc_node state, int32_t layer);
+/* Copies the state's pages_per_chunk slot ids to slots[]. SC_ENOTFOUND. */
+int sc_cache_slots(const sc_cache* cache, sc_node state, int32_t* slots);
+int sc_cache_free_slot_count(const sc_cache* cache);
+/* Frees the state's slots in every layer and bumps their generation, so a
+ * plan that still names them fails with SC_ESTALE.  SC_ENOTFOUND. */
+int sc_cache_release(sc_cache* cache, sc_node state);
+
+/* ---- 3D RoPE table ------------------------------------------------------
+ * The paper does not define the positional encoding; this follows the
+ * Wan-shaped workload: head_dim split into dim_t + dim_h + dim_w channels
+ * (44/42/42 for 128), interleaved pairs, pair i of axis a rotated by
+ * pos_a * theta^(-2 i / dim_a); token n of frame f of chunk c sits at
+ * (t, h, w) = (c * pages_per_chunk + f, n / grid_w, n % grid_w).
+ * The table holds cos/sin per (position, pair) for each axis, in fp32,
+ * computed on the device in double precision; build it once. */
+typedef struct {
+  int32_t grid_h, grid_w, dim_t, dim_h, dim_w, max_frames;
+  float theta;
+} sc_rope_desc;
+typedef struct {
+  sc_rope_desc desc;
+  const void* dev_table; /* built by sc_rope_table_build */
+} sc_rope;
+size_t sc_rope_table_bytes(const sc_rope_desc* desc);
+int sc_rope_table_build(const sc_rope_desc* desc, void* dev_table, sc_stream stream);
+
+/* Writes the K/V of one state for one layer into its page slots (allocating
+ * them, lowest free first, unless a plan reserved them).  k, v: device
+ * [pages_per_chunk * tokens_per_page, n_heads, head_dim] in the cache dtype,
+ * read asynchronously on the stream.  With rope != NULL the keys are rotated
+ * at the state's absolute positions first (grid_h * grid_w must equal
+ * tokens_per_page).  Errors: SC_EEXIST (layer already written),
+ * SC_ECAPACITY, SC_EINVAL, SC_EDEVICE. */
+int sc_cache_append(sc_cache* cache, int32_t layer, sc_node state, const void* k,
+                    const void* v, const sc_rope* rope, sc_stream stream);
+
+/* ---- Plan: availability and page lists (Eq. 6, Eq. 8) ------------------
+ * Resolves every segment of the selection to page slots and checks
+ * availability: a state read by a node must be in the cache or produced by
+ * the pack (Sec. 3.3, "Restrictions on context selection"; for Eq. 7 packs
+ * this is Eq. 8).  Pack states not yet cached get slots reserved now, in pack
+ * order.  Node i's pages are its segments' frames, in segment order.
+ * Errors: SC_EUNAVAILABLE, SC_ECAPACITY (the cache is unchanged on error).
+ * The plan stays valid for every layer until one of its slots is released. */
+int sc_plan_build(const sc_selection* sel, sc_cache* cache, sc_plan** out);
+int sc_plan_get(const sc_plan* plan, int32_t* n_nodes, int32_t* n_pages,
+                const int32_t** page_off, const int32_t** page_slot,
+                const int32_t** page_tokens, const int32_t** page_frame);
+void sc_plan_free(sc_plan* plan);
+
+/* ---- Packed block-causal attention (Eq. 6 over the plan) ---------------
+ * For every pack node i and head h:
+ *   O_i = softmax(Q_i K_i^T * scale) V_i
+ * where K_i, V_i are the keys/values of node i's pages at this layer -- the
+ * tokens Eq. 6's mask leaves visible; no dense mask is formed.
+ * q, o: device [n_nodes * Nq, n_heads, head_dim] in the cache dtype, node i
+ * at rows [i*Nq, (i+1)*Nq) with Nq = pages_per_chunk * tokens_per_page.
+ * Every page must have been written at this layer by calls enqueued earlier
+ * on the same stream.  Errors: SC_ESTALE, SC_EUNAVAILABLE (a page's state not
+ * written at this layer), SC_EUNSUPPORTED, SC_EDEVICE. */
+int sc_attention(const sc_plan* plan, const sc_cache* cache, int32_t layer, const void* q,
+                 void* o, float scale, sc_stream stream);
+
+/* ---- One DiT block over the pack ----------------------------------------
+ * The network F_theta of Eq. 1 for the packed nodes, one block (bf16 only):
+ *   h = RMSNorm(x); [q k v] = h Wqkv^T; q, k = RoPE(q), RoPE(k)
+ *   (k, v of each pack node are appended to its reserved slots, this layer)
+ *   o = sc_attention(q); x' = x + o Wo^T
+ *   x = x' + GELU_tanh(RMSNorm(x') Wup^T) Wdown^T
+ * RMSNorm: eps 1e-6, unit gain.  Weights: device bf16 in [out, in] layout
+ * (Wqkv is [3*hidden, hidden] = Wq;Wk;Wv).  x: device bf16
+ * [n_nodes * Nq, hidden], updated in place.  ws: device workspace of at least
+ * sc_block_workspace_bytes() bytes.  The block form is the Wan-shaped
+ * reading of the workload (the paper does not define the network). */
+typedef struct {
+  int32_t hidden, n_heads, head_dim, mlp;
+  const void* w_qkv;  /* [3*hidden, hidden] */
+  const void* w_o;    /* [hidden, hidden]   */
+  const void* w_up;   /* [mlp, hidden]      */
+  const void* w_down; /* [hidden, mlp]      */
+} sc_block_weights;
+size_t sc_block_workspace_bytes(const sc_block_weights* w, int32_t n_tokens);
+int sc_block_forward(const sc_block_weights* w, sc_cache* cache, int32_t layer,
+                     const sc_plan* plan, void* x, const sc_rope* rope, void* ws,
+                     size_t ws_bytes, sc_stream stream);
+
+/* ---- Sampler step (Eq. 1) ----------------------------------------------
+ * For each node i with level j >= 1:
+ *   out_i = (1 - t[j-1]) * y_i + t[j-1] * noise_i
+ * (the network output is read as a clean-state prediction and re-noised to
+ * the next input time; a reading, the paper leaves S_j open).  Nodes at
+ * level 0 are left untouched.  y, noise, out: device bf16
+ * [n_nodes, elems_per_node]; out may alias y.  t: host, K+1 input times. */
+int sc_sampler_step(const sc_node* nodes, int32_t n_nodes, const float* t, int32_t K,
+                    void* out, const void* y, const void* noise, int64_t elems_per_node,
+                    sc_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* STREAMCTX_H */

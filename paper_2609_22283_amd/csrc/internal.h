@@ -1,0 +1,84 @@
+// Internal declarations shared by the host core and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdint>
+#include <map>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "../../include/streamctx.h"
+
+namespace sc {
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int hip_fail(hipError_t e, const char* what);
+
+#define SC_HIP(call)                                   \
+  do {                                                 \
+    hipError_t e_ = (call);                            \
+    if (e_ != hipSuccess) return ::sc::hip_fail(e_, #call); \
+  } while (0)
+
+using StateKey = std::pair<int32_t, int32_t>;  // (chunk, level)
+
+struct StateEntry {
+  std::vector<int32_t> slots;    // pages_per_chunk slot ids, frames ascending
+  std::vector<uint8_t> written;  // per layer
+};
+
+inline size_t dtype_size(int32_t dtype) { return dtype == SC_DTYPE_F32 ? 4 : 2; }
+
+}  // namespace sc
+
+struct sc_selection {
+  std::vector<sc_node> nodes;
+  std::vector<int32_t> seg_off, seg_chunk, seg_level, seg_src;
+  std::vector<sc_node> states;
+  std::vector<uint8_t> vis;
+};
+
+struct sc_cache {
+  sc_cache_desc d;
+  char* pool;
+  size_t slot_bytes;    // bytes of one slot in one layer (K and V)
+  size_t kv_half;       // offset of V within a slot
+  std::vector<uint8_t> used;
+  std::vector<uint32_t> gen;
+  std::vector<sc::StateKey> owner;  // slot -> state (valid when used)
+  std::map<sc::StateKey, sc::StateEntry> states;
+};
+
+struct sc_plan {
+  std::vector<sc_node> nodes;
+  std::vector<int32_t> page_off, page_slot, page_tokens, page_frame;
+  std::vector<uint32_t> page_gen;
+  std::vector<sc::StateKey> page_state;
+  const sc_cache* cache;
+  int32_t nq;  // query tokens per node
+};
+
+namespace sc {
+
+// Validates a plan against the cache for reading `layer` (generations and
+// written flags).  Returns SC_OK or an error code with the message set.
+int plan_check(const sc_plan* plan, const sc_cache* cache, int32_t layer);
+
+// Kernel launchers (device code lives in the .hip files).
+int launch_attention(const sc_plan* plan, const sc_cache* cache, int32_t layer,
+                     const void* q, void* o, float scale, hipStream_t stream);
+int launch_append(const sc_cache* cache, int32_t layer, const int32_t* slots, int32_t chunk,
+                  const void* k, const void* v, const sc_rope* rope, hipStream_t stream);
+int launch_rope_table(const sc_rope_desc* d, void* table, hipStream_t stream);
+
+// Offsets of the three axis tables inside a RoPE table, in float2 units.
+struct RopeLayout {
+  int32_t pairs_t, pairs_h, pairs_w;
+  int64_t off_t, off_h, off_w, total;  // float2 entries
+};
+RopeLayout rope_layout(const sc_rope_desc* d);
+
+}  // namespace sc

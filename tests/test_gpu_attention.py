@@ -1,0 +1,165 @@
+"""GPU parity of the packed paged attention against the CPU oracle.
+
+Covers the tiny fp32 case (every node of 4 chunks x 5 levels under all three
+policies, several pack shapes), small bf16 packs whose pages (40 tokens) leave
+ragged tails inside 64-key tiles, the Wan-shaped clean / same-level /
+progressive packs on sampled rows, the segment probe, negative controls
+(mistakes planted in the oracle must fail the gates), NaN poisoning of
+unused slots, packed == sequential, and run-to-run determinism.
+"""
+import numpy as np
+import pytest
+
+import paper_2609_22283_amd as sc
+from oracle.attention import node_attention
+from oracle.pipeline import pipeline_rounds
+from oracle.policy import policy as oracle_policy
+from oracle.policy import select
+from synth.configs import SMALL, TINY, WAN, cfg2_clean, cfg3_same, cfg4_prog
+
+from gpu_cases import (AttnCase, BF16_MAX_ABS, F32_MAX_ABS, bf16_gates, from_device, sample_rows,
+                       to_device)
+
+pytestmark = pytest.mark.gpu
+
+ALL_TINY = [(c, j) for c in range(4) for j in range(TINY.K + 1)]
+
+
+def _tiny_packs(kind):
+    packs = [[n] for n in ALL_TINY]
+    if kind == "prog":
+        packs += [p for p in pipeline_rounds(4, TINY.K, refresh=True) if len(p) > 1]
+    if kind == "same":
+        packs += [[(c, j) for c in range(4)] for j in range(TINY.K + 1)]
+    packs.append(list(ALL_TINY))           # everything resident, one pack of 20
+    return packs
+
+
+@pytest.mark.parametrize("kind", ["clean", "same", "prog"])
+def test_tiny_fp32_every_node(kind):
+    for pack in _tiny_packs(kind):
+        case = AttnCase(TINY, sc.SC_DTYPE_F32, kind, pack, resident=ALL_TINY, seed=1)
+        out = case.run()
+        for i, node in enumerate(pack):
+            want = case.oracle(i)
+            err = np.abs(out[i] - want).max()
+            assert err <= F32_MAX_ABS, (kind, pack, node, err)
+
+
+SMALL_PACKS = [
+    ("prog", [(6, 1), (7, 2), (8, 3), (9, 4)], [(c, 0) for c in range(6)]),
+    ("prog", [(6, 0), (7, 1), (8, 2), (9, 3), (10, 4)], [(c, 0) for c in range(6)]),
+    ("same", [(6 + i, 2) for i in range(4)], [(c, 2) for c in range(6)]),
+    ("clean", [(6, 3)], [(c, 0) for c in range(6)]),
+    ("clean", [(2, 4)], [(c, 0) for c in range(2)]),
+    ("prog", [(0, 4)], []),
+]
+
+
+@pytest.mark.parametrize("kind,pack,resident", SMALL_PACKS)
+def test_small_bf16_packs(kind, pack, resident):
+    case = AttnCase(SMALL, sc.SC_DTYPE_BF16, kind, pack, resident, seed=2)
+    out = case.run()
+    for i in range(len(pack)):
+        bf16_gates(out[i], case.oracle(i), f"{kind} node {pack[i]}")
+
+
+def test_small_packed_equals_sequential_bitwise():
+    kind, pack, resident = SMALL_PACKS[0]
+    packed = AttnCase(SMALL, sc.SC_DTYPE_BF16, kind, pack, resident, seed=3).run()
+    # the same nodes one per call, ascending chunk (in-pack history comes
+    # from the cache, appended by the earlier calls)
+    for i, node in enumerate(pack):
+        res = resident + pack[:i]
+        alone = AttnCase(SMALL, sc.SC_DTYPE_BF16, kind, [node], res, seed=3).run()[0]
+        assert np.array_equal(alone, packed[i]), node
+
+
+def test_small_deterministic_and_pack_order_free():
+    kind, pack, resident = SMALL_PACKS[1]
+    a = AttnCase(SMALL, sc.SC_DTYPE_BF16, kind, pack, resident, seed=4)
+    o1 = a.run()
+    o2 = a.run()
+    rev = AttnCase(SMALL, sc.SC_DTYPE_BF16, kind, pack[::-1], resident, seed=4).run()
+    for i in range(len(pack)):
+        assert np.array_equal(o1[i], o2[i])
+        assert np.array_equal(o1[i], rev[len(pack) - 1 - i])
+
+
+def _probe_case(geo, kind, pack, resident):
+    """V = one-hot(state id) in the first channels (exact in bf16)."""
+    states = sorted(set(resident) | set(pack))
+    sid = {s: k for k, s in enumerate(states)}
+
+    def value_fn(st):
+        v = np.zeros((geo.tokens_per_chunk, geo.heads, geo.head_dim), dtype=np.float32)
+        v[:, :, sid[tuple(st)]] = 1.0
+        return v
+    return AttnCase(geo, sc.SC_DTYPE_BF16, kind, pack, resident, seed=5, value_fn=value_fn), states
+
+
+@pytest.mark.parametrize("kind,pack,resident", SMALL_PACKS[:3])
+def test_segment_probe_small(kind, pack, resident):
+    case, states = _probe_case(SMALL, kind, pack, resident)
+    out = case.run()
+    for i in range(len(pack)):
+        want = case.oracle(i)
+        chosen = set(select(oracle_policy(kind, SMALL.K, SMALL.W), pack).segments(i))
+        for k, st in enumerate(states):
+            np.testing.assert_allclose(out[i][:, :, k], want[:, :, k], atol=2e-3)
+            if st not in chosen:
+                assert np.all(out[i][:, :, k] == 0.0), (pack[i], st)
+
+
+def _corruptions(segs, geo):
+    """Plausible planning mistakes, planted in the oracle's segment list."""
+    c, j = segs[-1]
+    out = {"drop_oldest": segs[1:], "level_off_by_one": [(sc_, min(l + 1, geo.K)) for sc_, l in segs[:-1]] + [segs[-1]]}
+    out["future_chunk"] = segs + [(c + 1, j)]
+    return out
+
+
+def test_negative_controls_fail_gates():
+    kind, pack, resident = SMALL_PACKS[0]
+    extra = [(10, 4)] + [(c, min(l + 1, SMALL.K)) for c in range(10) for l in range(SMALL.K)]
+    case = AttnCase(SMALL, sc.SC_DTYPE_BF16, kind, pack, resident + extra, seed=6,
+                    n_slots=(len(resident) + len(extra) + len(pack) + 2) * SMALL.frames_per_chunk)
+    out = case.run()
+    sel = select(oracle_policy(kind, SMALL.K, SMALL.W), pack)
+    node = 3
+    segs = sel.segments(node)
+    bf16_gates(out[node], case.oracle(node), "correct plan")
+    for name, bad in _corruptions(segs, SMALL).items():
+        bad = [s for s in bad if s in case.kv]
+        want = case.oracle(node, segments=bad)
+        with pytest.raises(AssertionError):
+            bf16_gates(out[node], want, name)
+
+
+WAN_CASES = [cfg2_clean(4), cfg3_same(2), cfg4_prog(False), cfg4_prog(True)]
+
+
+@pytest.mark.parametrize("wl", WAN_CASES, ids=[w.name for w in WAN_CASES])
+def test_wan_sampled_rows(wl):
+    case = AttnCase(WAN, sc.SC_DTYPE_BF16, wl.policy, wl.pack, wl.resident, seed=7)
+    out = case.run()
+    rows = sample_rows(WAN.tokens_per_chunk, 40, seed=len(wl.pack))
+    for i in range(len(wl.pack)):
+        got = out[i]
+        assert np.all(np.isfinite(got)), "NaN from a poisoned slot or a bad tile"
+        bf16_gates(got[rows], case.oracle(i, rows=rows), f"{wl.name} node {wl.pack[i]}")
+
+
+def test_wan_segment_probe_prog():
+    wl = cfg4_prog(True)
+    case, states = _probe_case(WAN, wl.policy, wl.pack, wl.resident)
+    out = case.run()
+    rows = sample_rows(WAN.tokens_per_chunk, 16, seed=9)
+    for i in range(len(wl.pack)):
+        want = case.oracle(i, rows=rows)
+        got = out[i][rows]
+        chosen = set(select(oracle_policy(wl.policy, WAN.K, WAN.W), wl.pack).segments(i))
+        for k, st in enumerate(states):
+            np.testing.assert_allclose(got[:, :, k], want[:, :, k], atol=2e-3)
+            if st not in chosen:
+                assert np.all(out[i][:, :, k] == 0.0), (wl.pack[i], st)

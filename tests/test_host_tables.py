@@ -1,0 +1,174 @@
+"""C ABI host core vs the oracle, on the CPU (no kernel launches).
+
+Selection tables, visibility and plan tables (page slots under the
+lowest-free-first allocator) must match the oracle bit for bit; error codes
+must match the oracle's failures.  Also checks that the library exports every
+function include/streamctx.h declares.
+"""
+import os
+import random
+import re
+
+import pytest
+
+import paper_2609_22283_amd as sc
+from oracle.plan import CacheModel, PlanError, build_plan
+from oracle.policy import Policy, SelectionError, policy, select
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_header_symbols_exported():
+    with open(os.path.join(ROOT, "include", "streamctx.h")) as f:
+        text = f.read()
+    declared = set(re.findall(r"\b(sc_[a-z_0-9]+)\s*\(", text))
+    assert declared == set(sc.EXPORTED_SYMBOLS)
+    for name in declared:
+        assert hasattr(sc.lib, name), name
+    assert sc.sc_abi_version() == 1
+
+
+def _random_pack(rnd, K, max_chunk=9, max_n=6):
+    cand = [(c, j) for c in range(max_chunk) for j in range(K + 1)]
+    return rnd.sample(cand, rnd.randint(1, max_n))
+
+
+def _oracle_policy(kind, K, W, phi, mask):
+    return Policy({"clean": 0, "same": 1, "prog": 2, "table": 3}[kind], K, W, phi, mask)
+
+
+def test_selection_tables_bit_exact():
+    rnd = random.Random(1)
+    for trial in range(400):
+        K, W = rnd.randint(1, 6), rnd.randint(0, 7)
+        kind = rnd.choice(["clean", "same", "prog", "table"])
+        phi = [[rnd.randint(0, K) for _ in range(W)] for _ in range(K + 1)] if kind == "table" else None
+        mask = None
+        if rnd.random() < 0.3:
+            mask = [[rnd.randint(0, 1) for _ in range(W)] for _ in range(K + 1)]
+        pack = _random_pack(rnd, K)
+        want = select(_oracle_policy(kind, K, W, phi, mask), pack)
+        got = sc.sc_selection_build(kind, K, W, pack, phi_table=phi, r_mask=mask)
+        off, ch, lv, src = got.tables()
+        assert off == want.seg_off and ch == want.seg_chunk
+        assert lv == want.seg_level and src == want.seg_src
+        states, vis = got.visibility()
+        assert states == want.states and vis == want.vis
+
+
+@pytest.mark.parametrize("bad", [
+    dict(kind="prog", K=0, W=2, pack=[(0, 0)]),
+    dict(kind="prog", K=4, W=-1, pack=[(0, 0)]),
+    dict(kind="prog", K=4, W=2, pack=[(0, 5)]),
+    dict(kind="prog", K=4, W=2, pack=[(-1, 1)]),
+    dict(kind="prog", K=4, W=2, pack=[(1, 1), (1, 1)]),
+    dict(kind="table", K=2, W=2, pack=[(1, 1)], phi=[[0, 3], [0, 0], [0, 0]]),
+    dict(kind=7, K=2, W=2, pack=[(1, 1)]),
+])
+def test_selection_errors(bad):
+    with pytest.raises(sc.ScError) as e:
+        sc.sc_selection_build(bad["kind"], bad["K"], bad["W"], bad["pack"], phi_table=bad.get("phi"))
+    assert e.value.code == sc.SC_EINVAL
+    if isinstance(bad["kind"], str):
+        with pytest.raises(SelectionError):
+            select(_oracle_policy(bad["kind"], bad["K"], bad["W"], bad.get("phi"), None), bad["pack"])
+
+
+def _host_cache(n_slots, ppc, tpp=16):
+    # a fake device address: no kernel is launched by plan building
+    return sc.sc_cache_create(0x100000, 1, 2, 128, tpp, ppc, n_slots)
+
+
+def test_plan_tables_and_allocator_bit_exact():
+    """Random sequences of plans and releases: page lists, slots, frames and
+    error codes equal the oracle's cache model step by step."""
+    rnd = random.Random(2)
+    for trial in range(60):
+        K, W, ppc = rnd.randint(1, 4), rnd.randint(0, 4), rnd.randint(1, 3)
+        n_slots = rnd.randint(4, 60)
+        cache = _host_cache(n_slots, ppc)
+        model = CacheModel(n_slots=n_slots, pages_per_chunk=ppc)
+        for step in range(25):
+            if model.slots and rnd.random() < 0.3:
+                st = rnd.choice(sorted(model.slots))
+                model.release(st)
+                cache.release(st)
+                continue
+            kind = rnd.choice(["clean", "same", "prog"])
+            pack = _random_pack(rnd, K, max_chunk=7, max_n=4)
+            sel_o = select(policy(kind, K, W), pack)
+            sel_c = sc.sc_selection_build(kind, K, W, pack)
+            try:
+                want = build_plan(sel_o, model, 16)
+                err = None
+            except PlanError as e:
+                err = e.code
+            if err is not None:
+                with pytest.raises(sc.ScError) as e:
+                    sc.sc_plan_build(sel_c, cache)
+                assert e.value.code == {"EUNAVAILABLE": sc.SC_EUNAVAILABLE,
+                                        "ECAPACITY": sc.SC_ECAPACITY}[err]
+                continue
+            got = sc.sc_plan_build(sel_c, cache)
+            off, slot, tok, frame = got.tables()
+            assert off == want.page_off and slot == want.page_slot
+            assert tok == want.page_tokens and frame == want.page_frame
+            for st in model.slots:
+                assert cache.slots(st) == model.slots[st]
+            assert cache.free_slot_count() == len(model.free_slots())
+
+
+def test_worked_example_through_abi():
+    """Sec. 3.3, K = 3 round two, through the C ABI."""
+    for kind, expect in [("same", ((0, 3), -1)), ("prog", ((0, 2), 0)), ("clean", None)]:
+        cache = _host_cache(16, 1)
+        sc.sc_plan_build(sc.sc_selection_build("same", 3, 0, [(0, 3)]), cache)  # (0,3) cached
+        sel = sc.sc_selection_build(kind, 3, 1, [(0, 2), (1, 3)])
+        off, ch, lv, src = sel.tables()
+        if expect is None:
+            with pytest.raises(sc.ScError) as e:
+                sc.sc_plan_build(sel, cache)
+            assert e.value.code == sc.SC_EUNAVAILABLE
+            continue
+        g = off[1]
+        assert (ch[g], lv[g]) == expect[0] and src[g] == expect[1]
+        sc.sc_plan_build(sel, cache)
+
+
+def test_cache_errors_without_device():
+    cache = _host_cache(4, 2)
+    with pytest.raises(sc.ScError) as e:
+        cache.release((3, 3))
+    assert e.value.code == sc.SC_ENOTFOUND
+    with pytest.raises(sc.ScError) as e:
+        cache.slots((3, 3))
+    assert e.value.code == sc.SC_ENOTFOUND
+    sc.sc_plan_build(sc.sc_selection_build("prog", 4, 0, [(0, 4), (1, 4)]), cache)
+    assert cache.free_slot_count() == 0
+    with pytest.raises(sc.ScError) as e:
+        sc.sc_plan_build(sc.sc_selection_build("prog", 4, 0, [(2, 4)]), cache)
+    assert e.value.code == sc.SC_ECAPACITY
+    assert cache.contains((0, 4)) and not cache.contains((0, 4), 0)
+    with pytest.raises(sc.ScError) as e:
+        sc.sc_cache_create(0x1000, 1, 2, 128, 12, 2, 4)         # tokens_per_page % 8 != 0
+    assert e.value.code == sc.SC_EINVAL
+    with pytest.raises(sc.ScError) as e:
+        sc.sc_cache_create(0x1000, 1, 2, 96, 16, 2, 4)          # head_dim 96
+    assert e.value.code == sc.SC_EUNSUPPORTED
+    assert sc.sc_cache_pool_bytes(2, 12, 128, 1560, 3, 10) == 2 * 10 * 2 * 12 * 1560 * 128 * 2
+
+
+def test_stale_plan_detected_on_cpu():
+    """A plan whose slot was released must not reach a kernel: sc_attention
+    fails with SC_ESTALE before launching anything."""
+    cache = _host_cache(8, 1)
+    sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(0, 0)]), cache)
+    plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 1, [(1, 4)]), cache)
+    cache.release((0, 0))
+    with pytest.raises(sc.ScError) as e:
+        sc.sc_attention(plan, cache, 0, 0x1000, 0x2000, 0.125)
+    assert e.value.code == sc.SC_ESTALE
+    plan2 = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(2, 4)]), cache)
+    with pytest.raises(sc.ScError) as e:                       # reserved but never written
+        sc.sc_attention(plan2, cache, 0, 0x1000, 0x2000, 0.125)
+    assert e.value.code == sc.SC_EUNAVAILABLE
