@@ -1,0 +1,297 @@
+#!/usr/bin/env python3
+"""Steady-state packed progressive-history DiT step on one MI355X.
+
+One step is one pass of the whole hot path over one pack of in-flight
+nodes: the selection table, the plan (availability + page lists), one
+Wan2.1-1.3B-shaped DiT block over the packed nodes (RMSNorm, QKV GEMM with
+RoPE and the KV-cache append, packed paged attention, out-projection,
+RMSNorm, MLP), the sampler step, and the release of the pack's noisy states.
+
+Default workload ("cfg4"): the progressive-history diagonal
+[(6,1), (7,2), (8,3), (9,4)] (levels 0 = clean .. 4 = noise) over clean
+history chunks 0..5 cached in 1560-token pages; every node attends to its
+own chunk plus 6 prior chunks (21 latent frames, 32760 keys).  Inputs are
+seeded synthetic tensors (N(0,1) activations and cached K/V, N(0, 0.02)
+weights), all resident in HBM before timing.
+
+Prints one JSON line.  ``value`` is latent frames/s per DiT block:
+3 latent frames per chunk, K + 1 = 5 node forwards per chunk.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+METRIC = "steady-state latent frames/s per DiT block + attention TFLOP/s (% bf16 MFMA peak)"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def workload(name):
+    from synth.configs import cfg2_clean, cfg3_same, cfg4_prog
+    return {"cfg4": cfg4_prog(False), "cfg4R": cfg4_prog(True), "cfg3": cfg3_same(2),
+            "cfg2": cfg2_clean(4)}[name]
+
+
+class Setup:
+    """Device-resident inputs of one packed block step."""
+
+    def __init__(self, wl, seed=0):
+        import numpy as np
+        import torch
+
+        import paper_2609_22283_amd as sc
+        from synth import (TAG_K, TAG_NOISE, TAG_V, TAG_W_DOWN, TAG_W_O, TAG_W_QKV, TAG_W_UP, TAG_X,
+                           bf16_bits, normal_parallel)
+        from synth.configs import WAN as g
+
+        self.sc, self.torch, self.g, self.wl = sc, torch, g, wl
+        ppc, tpp, n = g.frames_per_chunk, g.tokens_per_page, g.tokens_per_chunk
+        self.n = n
+
+        def dev(x):
+            return torch.from_numpy(bf16_bits(x).view(np.int16)).cuda().view(torch.bfloat16)
+
+        n_slots = (len(wl.resident) + 2 * len(wl.pack) + 2) * ppc
+        nbytes = sc.sc_cache_pool_bytes(1, g.heads, g.head_dim, tpp, ppc, n_slots)
+        self.pool = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        self.cache = sc.sc_cache_create(self.pool, 1, g.heads, g.head_dim, tpp, ppc, n_slots)
+        rt = torch.empty(sc.sc_rope_table_bytes(g.grid_h, g.grid_w, g.rope_dims, 256),
+                         dtype=torch.uint8, device="cuda")
+        self.rope = sc.sc_rope_table_build(rt, g.grid_h, g.grid_w, g.rope_dims, 256, g.theta)
+        shape = (n, g.heads, g.head_dim)
+        for st in wl.resident:
+            k = dev(normal_parallel(shape, (seed, TAG_K) + st))
+            v = dev(normal_parallel(shape, (seed, TAG_V) + st))
+            self.cache.append(0, st, k, v, rope=self.rope)
+        torch.cuda.synchronize()
+        D, M = g.hidden, g.mlp
+        self.w = [dev(normal_parallel(s, (seed, tag, 0), 0.02)) for s, tag in
+                  [((3 * D, D), TAG_W_QKV), ((D, D), TAG_W_O), ((M, D), TAG_W_UP), ((D, M), TAG_W_DOWN)]]
+        self.bw = sc.BlockWeights(D, g.heads, g.head_dim, M, *self.w)
+        T = len(wl.pack) * n
+        self.x = dev(np.concatenate([normal_parallel((n, D), (seed, TAG_X) + st) for st in wl.pack]))
+        self.noise = dev(np.concatenate([normal_parallel((n, D), (seed, TAG_NOISE) + st)
+                                         for st in wl.pack]))
+        self.ws_bytes = sc.sc_block_workspace_bytes(self.bw, T)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device="cuda")
+        self.t_sched = (0.0, 5.0 / 8.0, 5.0 / 6.0, 15.0 / 16.0, 1.0)
+        torch.cuda.synchronize()
+
+    def packed_step(self):
+        sc, g, wl = self.sc, self.g, self.wl
+        sel = sc.sc_selection_build(wl.policy, g.K, g.W, wl.pack)
+        plan = sc.sc_plan_build(sel, self.cache)
+        sc.sc_block_forward(self.bw, self.cache, 0, plan, self.x, self.rope, self.ws, self.ws_bytes)
+        sc.sc_sampler_step(wl.pack, self.t_sched, g.K, self.x, self.x, self.noise,
+                           self.n * g.hidden)
+        for st in wl.pack:
+            self.cache.release(st)
+
+    def sequential_step(self):
+        """The same nodes one forward each, ascending chunk (history produced
+        by an earlier node of the pack is read back from the cache)."""
+        sc, g, wl = self.sc, self.g, self.wl
+        D = g.hidden
+        order = sorted(range(len(wl.pack)), key=lambda i: wl.pack[i])
+        for i in order:
+            node = wl.pack[i]
+            sel = sc.sc_selection_build(wl.policy, g.K, g.W, [node])
+            plan = sc.sc_plan_build(sel, self.cache)
+            xi = self.x[i * self.n:(i + 1) * self.n]
+            sc.sc_block_forward(self.bw, self.cache, 0, plan, xi, self.rope, self.ws, self.ws_bytes)
+            sc.sc_sampler_step([node], self.t_sched, g.K, xi, xi,
+                               self.noise[i * self.n:(i + 1) * self.n], self.n * D)
+        for st in wl.pack:
+            self.cache.release(st)
+
+
+def time_steps(setup, fn, steps, warmup, timer=False):
+    torch, sc = setup.torch, setup.sc
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    if timer:
+        sc.sc_timer_enable(True)
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1) / steps
+    kernels = {}
+    if timer:
+        for kind in ("attention", "gemm_qkv", "gemm_out", "gemm_up", "gemm_down", "rmsnorm",
+                     "sampler"):
+            n, tot = sc.sc_timer_read(kind)
+            if n:
+                kernels[kind] = (n, tot / n)
+        sc.sc_timer_enable(False)
+    return ms, wall / steps * 1e3, kernels
+
+
+def segment_counts(wl, g):
+    """Segments (chunk-states) each pack node reads, from the library's table."""
+    import paper_2609_22283_amd as sc
+    off, _, _, _ = sc.sc_selection_build(wl.policy, g.K, g.W, wl.pack).tables()
+    return [off[i + 1] - off[i] for i in range(len(wl.pack))]
+
+
+def attention_flops(wl, g):
+    """4 d H sum_i Nq_i Nk_i over the pairs the selection table makes visible."""
+    nq = g.tokens_per_chunk
+    return 4.0 * g.head_dim * g.heads * sum(nq * (s * nq) for s in segment_counts(wl, g))
+
+
+def gemm_flops(n_tokens, g):
+    D, M = g.hidden, g.mlp
+    return 2.0 * n_tokens * (D * 3 * D + D * D + D * M + M * D)
+
+
+def cpu_baseline(wl, seed=0, row_stride=16):
+    """The oracle's block on this workload, timed on the host's cores.
+
+    Bounded sample: K/V projections for every token of every pack node (every
+    query row reads them), then query-side work (Q, attention, out-projection,
+    MLP) for every ``row_stride``-th row only; the query-side time is scaled
+    by the row ratio (rows are independent)."""
+    import numpy as np
+
+    from oracle.block import BlockShape, block_forward, project_kv
+    from oracle.policy import policy, select
+    from oracle.rope import chunk_positions, rope
+    from synth import (TAG_K, TAG_V, TAG_W_DOWN, TAG_W_O, TAG_W_QKV, TAG_W_UP, TAG_X, bf16_round,
+                       normal_parallel)
+    from synth.configs import WAN as g
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    n = g.tokens_per_chunk
+    shp = BlockShape(g.hidden, g.heads, g.head_dim, g.mlp, g.frames_per_chunk, g.grid_h, g.grid_w,
+                     g.rope_dims, g.theta)
+    D, M = g.hidden, g.mlp
+    w = {k: bf16_round(normal_parallel(s, (seed, tag, 0), 0.02)).astype(np.float64) for k, s, tag in
+         [("w_qkv", (3 * D, D), TAG_W_QKV), ("w_o", (D, D), TAG_W_O), ("w_up", (M, D), TAG_W_UP),
+          ("w_down", (D, M), TAG_W_DOWN)]}
+    res = {}
+    for st in wl.resident:
+        k = bf16_round(normal_parallel((n, g.heads, g.head_dim), (seed, TAG_K) + st))
+        v = bf16_round(normal_parallel((n, g.heads, g.head_dim), (seed, TAG_V) + st))
+        pos = chunk_positions(st[0], g.frames_per_chunk, g.grid_h, g.grid_w)
+        res[st] = (rope(k, pos, g.rope_dims, g.theta), v.astype(np.float64))
+    xs = [bf16_round(normal_parallel((n, D), (seed, TAG_X) + st)).astype(np.float64) for st in wl.pack]
+    sel = select(policy(wl.policy, g.K, g.W), wl.pack)
+    rows = np.arange(0, n, row_stride)
+    t0 = time.perf_counter()
+    for i, (c, j) in enumerate(wl.pack):
+        project_kv(xs[i], c, w["w_qkv"], shp)
+    t_kv = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    block_forward(sel, lambda i: xs[i], w, res.__getitem__, shp, rows=rows)
+    t_all = time.perf_counter() - t0
+    t_rows = max(t_all - t_kv, 0.0)        # block_forward repeats the K/V projections
+    est = t_kv + t_rows * (n / len(rows))
+    node_fwd_per_s = len(wl.pack) / est
+    return {"value": 3.0 * node_fwd_per_s / (g.K + 1), "unit": "latent frames/s per DiT block",
+            "cores": int(threads), "kind": "oracle",
+            "sample": (f"one block over all {len(wl.pack)} pack nodes: K/V projections of all "
+                       f"{n} tokens per node timed in full ({t_kv:.1f} s), query-side work on "
+                       f"every {row_stride}th row ({len(rows)} rows/node, {t_rows:.1f} s) scaled "
+                       f"x{n / len(rows):.2f}; estimated {est:.1f} s per step")}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="cfg4", choices=["cfg4", "cfg4R", "cfg3", "cfg2"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sequential", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(collectives and sharding are out of scope); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    wl = workload(args.workload)
+    log(f"[bench] workload {wl.name}: pack {wl.pack}, resident {len(wl.resident)} states")
+    setup = Setup(wl)
+    g = setup.g
+    ms, wall_ms, kernels = time_steps(setup, setup.packed_step, args.steps, args.warmup, timer=True)
+    log(f"[bench] packed: {ms:.3f} ms/step (host wall {wall_ms:.3f})")
+    seq_ms = None
+    if not args.no_sequential:
+        seq_ms, _, _ = time_steps(setup, setup.sequential_step, max(3, args.steps // 2), 1)
+        log(f"[bench] sequential: {seq_ms:.3f} ms/step")
+
+    n_nodes = len(wl.pack)
+    T = n_nodes * g.tokens_per_chunk
+    a_flops = attention_flops(wl, g)
+    g_flops = gemm_flops(T, g)
+    attn_n, attn_ms = kernels.get("attention", (0, float("nan")))
+    attn_tflops = a_flops / (attn_ms * 1e-3) / 1e12
+    gemm_ms = sum(kernels[k][1] for k in ("gemm_qkv", "gemm_out", "gemm_up", "gemm_down") if k in kernels)
+    node_fwd_per_s = n_nodes / (ms * 1e-3)
+    value = 3.0 * node_fwd_per_s / (g.K + 1)
+    result = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "latent frames/s per DiT block",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) activations and cached K/V, N(0,0.02) weights)",
+        "config": {"workload": f"{wl.name}: {wl.description}", "nodes": wl.pack,
+                   "policy": wl.policy, "tokens_per_node": g.tokens_per_chunk,
+                   "keys_per_node": [s * g.tokens_per_chunk for s in segment_counts(wl, g)],
+                   "hidden": g.hidden, "heads": g.heads,
+                   "head_dim": g.head_dim, "mlp": g.mlp, "page_tokens": g.tokens_per_page,
+                   "parallelism": "single GPU"},
+        "attention_tflops": round(attn_tflops, 1),
+        "attention_pct_peak": round(100.0 * attn_tflops / PEAK_BF16_TFLOPS, 2),
+        "attention_ms": round(attn_ms, 4),
+        "gemm_tflops": round(g_flops / (gemm_ms * 1e-3) / 1e12, 1) if gemm_ms else None,
+        "kernel_avg_ms": {k: round(v[1], 4) for k, v in kernels.items()},
+        "sequential_ms_per_step": round(seq_ms, 4) if seq_ms else None,
+        "packed_vs_sequential": round(seq_ms / ms, 3) if seq_ms else None,
+        "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 1), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None, "kernel": "attn_bf16_kernel",
+                     "algorithmic_per_launch": f"{a_flops:.4e} FLOP"},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the oracle on the host (bounded sample)...")
+        result["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

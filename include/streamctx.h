@@ -219,6 +219,17 @@ int sc_sampler_step(const sc_node* nodes, int32_t n_nodes, const float* t, int32
                     void* out, const void* y, const void* noise, int64_t elems_per_node,
                     sc_stream stream);
 
+/* ---- Kernel timing (measurement support) ------------------------------
+ * While enabled, every kernel the library launches is bracketed by two HIP
+ * events recorded on the launch stream.  sc_timer_read synchronises those
+ * events and returns, for one kernel kind, the number of launches and the
+ * summed elapsed milliseconds since the timer was last enabled.  Kinds:
+ * "attention", "gemm_qkv", "gemm_out", "gemm_up", "gemm_down", "rmsnorm",
+ * "append", "sampler".  Enabling clears earlier records.  Events are created
+ * lazily and reused; the cost is two event records per launch. */
+int sc_timer_enable(int on);
+int sc_timer_read(const char* kind, int32_t* launches, double* total_ms);
+
 #ifdef __cplusplus
 }
 #endif

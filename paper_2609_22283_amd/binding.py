@@ -20,7 +20,7 @@ __all__ = [
     "sc_abi_version", "sc_selection_build", "sc_cache_pool_bytes", "sc_cache_create",
     "sc_rope_table_bytes", "sc_rope_table_build", "sc_plan_build", "sc_attention",
     "sc_block_workspace_bytes", "sc_block_forward", "sc_sampler_step",
-    "Selection", "Cache", "Plan", "Rope", "BlockWeights",
+    "sc_timer_enable", "sc_timer_read", "Selection", "Cache", "Plan", "Rope", "BlockWeights",
 ]
 
 SC_OK, SC_EINVAL, SC_EUNAVAILABLE, SC_ECAPACITY = 0, -1, -2, -3
@@ -38,7 +38,18 @@ EXPORTED_SYMBOLS = [
     "sc_rope_table_bytes", "sc_rope_table_build",
     "sc_plan_build", "sc_plan_get", "sc_plan_free",
     "sc_attention", "sc_block_workspace_bytes", "sc_block_forward", "sc_sampler_step",
+    "sc_timer_enable", "sc_timer_read",
 ]
+
+# The library and PyTorch must share one HIP runtime: torch ships its own
+# libamdhip64 (same SONAME as /opt/rocm's).  Loading torch first makes the
+# dynamic linker bind the library to torch's copy, so device pointers and
+# streams created by torch are valid inside the library.  Loading the
+# library first would bring up a second HIP/HSA runtime in the process.
+try:
+    import torch as _torch  # noqa: F401
+except ImportError:  # a non-torch host process uses the system HIP runtime
+    _torch = None
 
 library_path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstreamctx.so")
 if not os.path.exists(library_path):
@@ -114,6 +125,8 @@ _SIG = {
                                    C.POINTER(sc_rope), _P, C.c_size_t, _P]),
     "sc_sampler_step": (C.c_int, [C.POINTER(sc_node), C.c_int32, C.POINTER(C.c_float), C.c_int32,
                                   _P, _P, _P, C.c_int64, _P]),
+    "sc_timer_enable": (C.c_int, [C.c_int]),
+    "sc_timer_read": (C.c_int, [C.c_char_p, _I32P, C.POINTER(C.c_double)]),
 }
 for _name, (_res, _args) in _SIG.items():
     _f = getattr(lib, _name)
@@ -352,3 +365,14 @@ def sc_sampler_step(nodes, t: Sequence[float], K: int, out, y, noise, elems_per_
     tt = (C.c_float * len(t))(*[float(v) for v in t])
     _check(lib.sc_sampler_step(arr, len(nodes), tt, K, _ptr(out), _ptr(y), _ptr(noise),
                                elems_per_node, _stream(stream)))
+
+
+def sc_timer_enable(on: bool = True) -> None:
+    _check(lib.sc_timer_enable(1 if on else 0))
+
+
+def sc_timer_read(kind: str):
+    """(launches, total milliseconds) of one kernel kind since enabling."""
+    n, ms = C.c_int32(), C.c_double()
+    _check(lib.sc_timer_read(kind.encode(), C.byref(n), C.byref(ms)))
+    return n.value, ms.value

@@ -138,6 +138,7 @@ int launch_append(const sc_cache* c, int32_t layer, const int32_t* slots, int32_
   char* layer_base = c->pool + (size_t)layer * d.n_slots * c->slot_bytes;
   dim3 grid(d.pages_per_chunk * ((d.tokens_per_page + 63) / 64), d.n_heads);
   const int use_rope = rope ? 1 : 0;
+  timer_begin(TK_APPEND, stream);
   if (d.dtype == SC_DTYPE_BF16) {
     if (d.head_dim == 128)
       hipLaunchKernelGGL((append_kernel<uint16_t, 128>), grid, dim3(256), 0, stream,
@@ -157,6 +158,7 @@ int launch_append(const sc_cache* c, int32_t layer, const int32_t* slots, int32_
                          static_cast<const float*>(k), static_cast<const float*>(v), layer_base,
                          c->slot_bytes, c->kv_half, sl, d.n_heads, d.tokens_per_page, use_rope, ra);
   }
+  timer_end(TK_APPEND, stream);
   SC_HIP(hipGetLastError());
   return SC_OK;
 }

@@ -283,6 +283,7 @@ int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const v
   g.tpp_div = magic_div((uint32_t)d.tokens_per_page);
   g.scale = scale;
   g.scale_log2 = scale * 1.4426950408889634f;
+  timer_begin(TK_ATTENTION, stream);
   if (d.dtype == SC_DTYPE_F32) {
     g.n_qtiles = (p->nq + 63) / 64;
     const uint32_t nwg = (uint32_t)n * d.n_heads * g.n_qtiles;
@@ -299,6 +300,7 @@ int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const v
     hipLaunchKernelGGL(attn_bf16_kernel, dim3(nwg), dim3(256), 0, stream,
                        static_cast<const uint16_t*>(q), static_cast<uint16_t*>(o), g, plan);
   }
+  timer_end(TK_ATTENTION, stream);
   SC_HIP(hipGetLastError());
   return SC_OK;
 }

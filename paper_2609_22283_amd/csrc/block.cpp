@@ -106,7 +106,7 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
 
   int rc;
   if ((rc = launch_rmsnorm(xb, hn, T, D, stream)) != SC_OK) return rc;
-  if ((rc = launch_gemm(EPI_QKV, static_cast<const uint16_t*>(w->w_qkv), hn, 3 * D, T, D, ep, stream)) != SC_OK)
+  if ((rc = launch_gemm(EPI_QKV, TK_GEMM_QKV, static_cast<const uint16_t*>(w->w_qkv), hn, 3 * D, T, D, ep, stream)) != SC_OK)
     return rc;
   for (int32_t i = 0; i < n; ++i)
     c->states.at(StateKey(p->nodes[i].chunk, p->nodes[i].level)).written[layer] = 1;
@@ -116,16 +116,16 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
   std::memset(&e2, 0, sizeof e2);
   e2.out = xb;
   e2.ld_out = D;
-  if ((rc = launch_gemm(EPI_RESIDUAL, static_cast<const uint16_t*>(w->w_o), ob, D, T, D, e2, stream)) != SC_OK)
+  if ((rc = launch_gemm(EPI_RESIDUAL, TK_GEMM_OUT, static_cast<const uint16_t*>(w->w_o), ob, D, T, D, e2, stream)) != SC_OK)
     return rc;
   if ((rc = launch_rmsnorm(xb, hn, T, D, stream)) != SC_OK) return rc;
   GemmEpilogue e3;
   std::memset(&e3, 0, sizeof e3);
   e3.out = ub;
   e3.ld_out = w->mlp;
-  if ((rc = launch_gemm(EPI_GELU, static_cast<const uint16_t*>(w->w_up), hn, w->mlp, T, D, e3, stream)) != SC_OK)
+  if ((rc = launch_gemm(EPI_GELU, TK_GEMM_UP, static_cast<const uint16_t*>(w->w_up), hn, w->mlp, T, D, e3, stream)) != SC_OK)
     return rc;
-  if ((rc = launch_gemm(EPI_RESIDUAL, static_cast<const uint16_t*>(w->w_down), ub, D, T, w->mlp, e2, stream)) != SC_OK)
+  if ((rc = launch_gemm(EPI_RESIDUAL, TK_GEMM_DOWN, static_cast<const uint16_t*>(w->w_down), ub, D, T, w->mlp, e2, stream)) != SC_OK)
     return rc;
   return SC_OK;
 }

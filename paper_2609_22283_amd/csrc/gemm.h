@@ -27,8 +27,8 @@ struct GemmEpilogue {
   int32_t node_slot[kGemmMaxNodePages];  // [node][frame] page slot of the node's own state
 };
 
-int launch_gemm(int epi, const uint16_t* W, const uint16_t* X, int32_t F, int32_t T, int32_t Kd,
-                const GemmEpilogue& ep, hipStream_t stream);
+int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, int32_t F, int32_t T,
+                int32_t Kd, const GemmEpilogue& ep, hipStream_t stream);
 int launch_rmsnorm(const uint16_t* x, uint16_t* y, int32_t rows, int32_t D, hipStream_t stream);
 
 }  // namespace sc

@@ -194,12 +194,13 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   }
 }
 
-int launch_gemm(int epi, const uint16_t* W, const uint16_t* X, int32_t F, int32_t T, int32_t Kd,
-                const GemmEpilogue& ep, hipStream_t stream) {
+int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, int32_t F, int32_t T,
+                int32_t Kd, const GemmEpilogue& ep, hipStream_t stream) {
   if (F % GBM || Kd % GBK || T <= 0)
     return fail(SC_EUNSUPPORTED, "gemm needs F %% %d == 0, K %% %d == 0 (F=%d K=%d T=%d)", GBM, GBK,
                 F, Kd, T);
   const uint32_t tiles = (uint32_t)(F / GBM) * (uint32_t)((T + GBN - 1) / GBN);
+  timer_begin(timer_kind, stream);
   switch (epi) {
     case EPI_QKV:
       hipLaunchKernelGGL(gemm_bf16_kernel<EPI_QKV>, dim3(tiles), dim3(G_THREADS), 0, stream, W, X, F,
@@ -217,6 +218,7 @@ int launch_gemm(int epi, const uint16_t* W, const uint16_t* X, int32_t F, int32_
       hipLaunchKernelGGL(gemm_bf16_kernel<EPI_STORE>, dim3(tiles), dim3(G_THREADS), 0, stream, W, X,
                          F, T, Kd, ep);
   }
+  timer_end(timer_kind, stream);
   SC_HIP(hipGetLastError());
   return SC_OK;
 }
@@ -258,7 +260,9 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
 
 int launch_rmsnorm(const uint16_t* x, uint16_t* y, int32_t rows, int32_t D, hipStream_t stream) {
   if (D % 8) return fail(SC_EUNSUPPORTED, "rmsnorm needs D %% 8 == 0");
+  timer_begin(TK_RMSNORM, stream);
   hipLaunchKernelGGL(rmsnorm_kernel, dim3((rows + 3) / 4), dim3(256), 0, stream, x, y, rows, D, 1e-6f);
+  timer_end(TK_RMSNORM, stream);
   SC_HIP(hipGetLastError());
   return SC_OK;
 }

@@ -74,6 +74,14 @@ int launch_append(const sc_cache* cache, int32_t layer, const int32_t* slots, in
                   const void* k, const void* v, const sc_rope* rope, hipStream_t stream);
 int launch_rope_table(const sc_rope_desc* d, void* table, hipStream_t stream);
 
+// Kernel timer: launchers bracket their kernel with timer_begin/timer_end.
+enum TimerKind {
+  TK_ATTENTION = 0, TK_GEMM_QKV, TK_GEMM_OUT, TK_GEMM_UP, TK_GEMM_DOWN, TK_RMSNORM, TK_APPEND,
+  TK_SAMPLER, TK_COUNT
+};
+void timer_begin(int kind, hipStream_t stream);
+void timer_end(int kind, hipStream_t stream);
+
 // Offsets of the three axis tables inside a RoPE table, in float2 units.
 struct RopeLayout {
   int32_t pairs_t, pairs_h, pairs_w;

@@ -68,10 +68,12 @@ extern "C" int sc_sampler_step(const sc_node* nodes, int32_t n, const float* t, 
   const int64_t total = elems_per_node / 8 * n;
   const int threads = 256;
   const int64_t blocks = std::min<int64_t>((total + threads - 1) / threads, 4096);
+  timer_begin(TK_SAMPLER, static_cast<hipStream_t>(stream));
   hipLaunchKernelGGL(sampler_kernel, dim3((unsigned)blocks), dim3(threads), 0,
                      static_cast<hipStream_t>(stream), static_cast<uint16_t*>(out),
                      static_cast<const uint16_t*>(y), static_cast<const uint16_t*>(noise),
                      elems_per_node, n, coef);
+  timer_end(TK_SAMPLER, static_cast<hipStream_t>(stream));
   SC_HIP(hipGetLastError());
   return SC_OK;
 }
