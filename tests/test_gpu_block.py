@@ -1,10 +1,15 @@
 """GPU parity of RoPE append, the DiT block and the sampler against the oracle.
 
 Block outputs pass through seven bf16 roundings (normalised input, q/k/v,
-attention output, residual stream, second norm, GELU output, final output),
-so their gate is relative for large values: |gpu - oracle| <= 2e-2 * max(1, |oracle|)
-elementwise and mean |gpu - oracle| <= 2e-3 * max(1, mean |oracle|).  The
-K/V the block writes into the cache use the attention gates.
+attention output, residual stream, second norm, GELU output, final output).
+Two of them land on the residual stream itself (x' = x + o Wo, then y), and a
+bf16 rounding moves a value by half a spacing at most (2^-8 relative) and by
+a quarter spacing on average (~2^-9 of the value over a binade); the others
+are averaged over >= 256-term dot products.  Gates: elementwise
+|gpu - oracle| <= 2e-2 * max(1, |oracle|), and
+mean |gpu - oracle| <= 4e-3 * max(1, mean |oracle|) (two residual roundings
+of ~2^-9 each, with margin).  The K/V the block writes into the cache use the
+attention gates.
 """
 import math
 
@@ -151,7 +156,7 @@ def block_gate(got, want, what):
     lim = 2e-2 * np.maximum(1.0, np.abs(want))
     worst = float((d / lim).max())
     assert worst <= 1.0, f"{what}: worst error/limit {worst:.3g}"
-    mean_lim = 2e-3 * max(1.0, float(np.abs(want).mean()))
+    mean_lim = 4e-3 * max(1.0, float(np.abs(want).mean()))
     assert d.mean() <= mean_lim, f"{what}: mean abs {d.mean():.3g}"
     return worst, float(d.mean())
 
