@@ -13,6 +13,8 @@
 // softmax in fp32.  The K rows feeding the S^T MFMA are permuted so that each
 // lane's probabilities are exactly the B operand of the PV MFMA, and V is
 // stored transposed in the cache so its A operand is one 16-byte LDS read.
+#include <type_traits>
+
 #include "device.h"
 #include "internal.h"
 
@@ -87,15 +89,107 @@ constexpr int BK = 64;        // keys per tile
 constexpr int HDB = 128;      // head dim of the bf16 kernel
 constexpr int KT_BYTES = BK * HDB * 2;   // 16 KB
 constexpr int VT_BYTES = HDB * BK * 2;   // 16 KB
+constexpr int BUF_BYTES = KT_BYTES + VT_BYTES;
+// Running maxima are only raised when a tile's maximum exceeds them by more
+// than this many powers of two; probabilities then stay below 2^8, which fp32
+// sums and bf16 products hold exactly as well as values below 1.
+constexpr float RESCALE_LOG2 = 8.0f;
 
-__device__ __forceinline__ void load16_global(u32x4& r, const char* p) {
-  r = *reinterpret_cast<const u32x4*>(p);
+struct AttnLane {
+  // per-lane LDS read offsets (bytes) inside one buffer
+  uint32_t koff[8];   // K row sigma, 16-byte column 2 si + hl   (kb adds 8192)
+  uint32_t voff[4];   // V^T row r32, column 4 kb + 2 mm + hl    (db adds 4096)
+};
+
+template <int BUF, bool MASK>
+__device__ __forceinline__ void attn_tile(const char* smem, const AttnLane& L, const bf16x8 (&qreg)[8],
+                                          f32x16 (&oacc)[4], float& m_run, float& l_run, float c2,
+                                          int32_t t0, int32_t nk, int32_t hl) {
+  const char* kl = smem + BUF * BUF_BYTES;
+  const char* vl = kl + KT_BYTES;
+  f32x16 s[2];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    s[kb] = f32x16{};
+#pragma unroll
+    for (int si = 0; si < 8; ++si) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + L.koff[si] + kb * 8192);
+      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[si], s[kb], 0, 0, 0);
+    }
+  }
+  if constexpr (MASK) {  // keys past the node's last key get no weight
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int32_t key = t0 + 32 * kb + 16 * (i >> 3) + 8 * hl + (i & 7);
+        if (key >= nk) s[kb][i] = -INFINITY;
+      }
+  }
+  float mx = fmaxf(s[0][0], s[0][1]);
+#pragma unroll
+  for (int i = 2; i < 16; ++i) mx = fmaxf(mx, s[0][i]);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[1][i]);
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float m_tile = mx * c2;
+  if (__builtin_amdgcn_ballot_w64(m_tile > m_run + RESCALE_LOG2)) {
+    // an opaque statement keeps this a (wave-uniform) branch instead of
+    // being flattened into 64 unconditional multiplies per tile
+    asm volatile("" ::: "memory");
+    const float m_new = fmaxf(m_run, m_tile);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
+  }
+  bf16x8 pb[2][2];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int mm = 0; mm < 2; ++mm)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        pb[kb][mm][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(s[kb][8 * mm + e], c2, -m_run)));
+  // row sum of the rounded probabilities (what the PV product uses)
+  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int mm = 0; mm < 2; ++mm)
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const bf16x2 pair = {pb[kb][mm][e], pb[kb][mm][e + 1]};
+        l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
+      }
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int mm = 0; mm < 2; ++mm)
+#pragma unroll
+      for (int db = 0; db < 4; ++db) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(vl + L.voff[2 * kb + mm] + db * 4096);
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kb][mm], oacc[db], 0, 0, 0);
+      }
+}
+
+// Direct global -> LDS copy of 16 bytes per lane (gfx950 LDS DMA): lane i
+// of the wave writes bytes [16 i, 16 i + 16) after the wave-uniform LDS
+// address, so the XOR swizzle is applied by choosing each lane's source.
+__device__ __forceinline__ void dma16(const char* src, char* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src),
+                                   reinterpret_cast<__attribute__((address_space(3))) void*>(
+                                       reinterpret_cast<uintptr_t>(lds_wave_base)),
+                                   16, 0, 0);
 }
 
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                            uint16_t* __restrict__ o, AttnGeom g,
                                                            AttnPlan plan) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * (KT_BYTES + VT_BYTES)];
+  __shared__ __attribute__((aligned(1024))) char smem[2 * BUF_BYTES];
   const uint32_t nwg = (uint32_t)g.n_nodes * g.n_heads * g.n_qtiles;
   const uint32_t w = xcd_remap(blockIdx.x, nwg);
   const int32_t qt = w % g.n_qtiles;
@@ -105,65 +199,98 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   const int32_t tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int32_t hl = lane >> 5, r32 = lane & 31;
   const int32_t p0 = plan.page_off[node];
-  const int32_t nk = (plan.page_off[node + 1] - p0) * g.tpp;
+  const int32_t npages = plan.page_off[node + 1] - p0;
+  const int32_t nk = npages * g.tpp;
   const int32_t ntiles = (nk + BK - 1) / BK;
+  const int32_t nfull = nk / BK;
 
-  // Q^T operand: lane holds Q[row][16 s + 8 hl .. +7] for s = 0..7.
+  // Q^T operand: lane holds Q[row][16 si + 8 hl .. +7] for si = 0..7.
   const int32_t qrow = qt * BQ + wave * 32 + r32;
   const int32_t qrow_c = qrow < g.nq ? qrow : g.nq - 1;
   const uint16_t* qp = q + (((size_t)node * g.nq + qrow_c) * g.n_heads + head) * HDB + 8 * hl;
   bf16x8 qreg[8];
 #pragma unroll
-  for (int s = 0; s < 8; ++s) qreg[s] = *reinterpret_cast<const bf16x8*>(qp + 16 * s);
+  for (int si = 0; si < 8; ++si) qreg[si] = *reinterpret_cast<const bf16x8*>(qp + 16 * si);
 
-  // Row of the S^T MFMA that holds key sigma(r): lane-local probabilities then
-  // come out as keys 8*hl .. 8*hl+7 (+16) of each 32-key block.
-  const int32_t sa = r32 >> 3, sh = (r32 >> 2) & 1, sb = r32 & 3;
-  const int32_t sigma = 16 * (sa >> 1) + 8 * sh + 4 * (sa & 1) + sb;
+  // Row sigma of the S^T MFMA holds key sigma: each lane's probabilities are
+  // then keys 8 hl .. 8 hl + 7 (+16) of every 32-key block -- exactly the B
+  // operand layout of the PV MFMA.
+  AttnLane L;
+  {
+    const int32_t sa = r32 >> 3, sh = (r32 >> 2) & 1, sb = r32 & 3;
+    const int32_t sigma = 16 * (sa >> 1) + 8 * sh + 4 * (sa & 1) + sb;
+#pragma unroll
+    for (int si = 0; si < 8; ++si)
+      L.koff[si] = sigma * 256 + (((2 * si + hl) ^ (sigma & 15)) << 4);
+#pragma unroll
+    for (int cm = 0; cm < 4; ++cm)
+      L.voff[cm] = r32 * 128 + (((2 * cm + hl) ^ ((r32 >> 1) & 7)) << 4);
+  }
 
-  // Tile loaders: 4 K chunks and 4 V^T chunks of 16 bytes per thread.
-  const char* kbase = g.layer_base + (size_t)head * g.tpp * HDB * 2;
-  const char* vbase = g.layer_base + g.kv_half + (size_t)head * HDB * g.tpp * 2;
-  u32x4 kpre[4], vpre[4];
-  auto issue_loads = [&](int32_t t0) {
+  // Tile copies.  A 64-key tile spans at most two pages (pages hold >= 64
+  // tokens), so the page of a key is chosen against one wave-uniform
+  // boundary.  Offsets are 32-bit, relative to the layer's slots (the host
+  // checks a layer fits in 4 GB); the per-page parts are wave-uniform.  Per
+  // wave: 4 copies of 4 K rows (1 KB each) and 4 copies of 8 V^T rows.  Lane
+  // (row, physical column p) fetches logical column p ^ swizzle(row).
+  const char* lbase = g.layer_base;
+  const uint32_t khead = (uint32_t)head * g.tpp * HDB * 2;
+  const uint32_t vhead = (uint32_t)g.kv_half + (uint32_t)head * HDB * g.tpp * 2;
+  const int32_t krow0 = 16 * wave + (lane >> 4), kp = lane & 15;
+  const int32_t vrow0 = 32 * wave + (lane >> 3), vp = lane & 7;
+  uint32_t kswz[4], vlane[4];
+  int32_t vkey[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int32_t c = tid + 256 * i;
-      const int32_t row = c >> 4, col = c & 15;
-      int32_t key = t0 + row;
-      key = key < nk ? key : nk - 1;
-      const int32_t pg = fast_div(key, g.tpp_div);
-      const int32_t off = key - pg * g.tpp;
-      const size_t slot = plan.page_slot[p0 + pg];
-      load16_global(kpre[i], kbase + slot * g.slot_bytes + ((size_t)off * HDB + col * 8) * 2);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int32_t c = tid + 256 * i;
-      const int32_t d = c >> 3, col = c & 7;
-      int32_t key = t0 + col * 8;
-      key = key < nk ? key : nk - 8;
-      const int32_t pg = fast_div(key, g.tpp_div);
-      const int32_t off = key - pg * g.tpp;
-      const size_t slot = plan.page_slot[p0 + pg];
-      load16_global(vpre[i], vbase + slot * g.slot_bytes + ((size_t)d * g.tpp + off) * 2);
-    }
-  };
-  auto store_lds = [&](int buf) {
-    char* kl = smem + buf * (KT_BYTES + VT_BYTES);
+  for (int j = 0; j < 4; ++j) {
+    const int32_t row = krow0 + 4 * j;
+    kswz[j] = (uint32_t)row * 256 + ((kp ^ (row & 15)) << 4);   // plus t0 * 256
+    const int32_t d = vrow0 + 8 * j;
+    vkey[j] = 8 * (vp ^ ((d >> 1) & 7));                           // key offset in tile
+    vlane[j] = (uint32_t)d * g.tpp * 2 + (uint32_t)vkey[j] * 2;    // plus t0 * 2
+  }
+  auto issue = [&](int32_t t0, int buf, auto clamp_c) {
+    constexpr bool CLAMP = decltype(clamp_c)::value;
+    const int32_t plo = (int32_t)fast_div((uint32_t)t0, g.tpp_div);
+    const int32_t bkey = (plo + 1) * g.tpp;
+    const int32_t phi = plo + 1 < npages ? plo + 1 : plo;
+    const uint32_t slo = (uint32_t)plan.page_slot[p0 + plo] * (uint32_t)g.slot_bytes;
+    const uint32_t shi = (uint32_t)plan.page_slot[p0 + phi] * (uint32_t)g.slot_bytes;
+    // offset of key k on page lo: slo + head part + (k - plo*tpp) * row bytes
+    const uint32_t k_lo = slo + khead - (uint32_t)plo * g.tpp * 256 + (uint32_t)t0 * 256;
+    const uint32_t k_hi = shi + khead - (uint32_t)bkey * 256 + (uint32_t)t0 * 256;
+    const uint32_t v_lo = slo + vhead - (uint32_t)plo * g.tpp * 2 + (uint32_t)t0 * 2;
+    const uint32_t v_hi = shi + vhead - (uint32_t)bkey * 2 + (uint32_t)t0 * 2;
+    const int32_t split = bkey - t0;  // tile-relative first key of page hi
+    char* kl = smem + buf * BUF_BYTES;
     char* vl = kl + KT_BYTES;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int32_t c = tid + 256 * i;
-      const int32_t row = c >> 4, col = c & 15;
-      *reinterpret_cast<u32x4*>(kl + row * 256 + ((col ^ (row & 15)) << 4)) = kpre[i];
+    for (int j = 0; j < 4; ++j) {
+      int32_t rk = krow0 + 4 * j;  // tile-relative key
+      uint32_t lo = kswz[j];
+      if constexpr (CLAMP) {
+        if (t0 + rk >= nk) {
+          lo -= (uint32_t)(t0 + rk - (nk - 1)) * 256;
+          rk = nk - 1 - t0;
+        }
+      }
+      dma16(lbase + ((rk < split ? k_lo : k_hi) + lo), kl + (16 * wave + 4 * j) * 256);
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int32_t c = tid + 256 * i;
-      const int32_t d = c >> 3, col = c & 7;
-      *reinterpret_cast<u32x4*>(vl + d * 128 + ((col ^ ((d >> 1) & 7)) << 4)) = vpre[i];
+    for (int j = 0; j < 4; ++j) {
+      int32_t rk = vkey[j];
+      uint32_t lo = vlane[j];
+      if constexpr (CLAMP) {
+        if (t0 + rk >= nk) {
+          lo -= (uint32_t)(t0 + rk - (nk - 8)) * 2;
+          rk = nk - 8 - t0;
+        }
+      }
+      dma16(lbase + ((rk < split ? v_lo : v_hi) + lo), vl + (32 * wave + 8 * j) * 128);
     }
+  };
+  auto landed = [&]() {  // this wave's copies are in LDS, then everyone's
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
   };
 
   f32x16 oacc[4];
@@ -172,77 +299,32 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   float m_run = -INFINITY, l_run = 0.f;
   const float c2 = g.scale_log2;
 
-  issue_loads(0);
-  store_lds(0);
-  __syncthreads();
+  if (ntiles > 1) issue(0, 0, std::false_type{});
+  else issue(0, 0, std::true_type{});
+  landed();
 
-  for (int32_t t = 0; t < ntiles; ++t) {
-    const int32_t t0 = t * BK;
-    if (t + 1 < ntiles) issue_loads(t0 + BK);
-    const char* kl = smem + (t & 1) * (KT_BYTES + VT_BYTES);
-    const char* vl = kl + KT_BYTES;
-
-    f32x16 s[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      s[kb] = f32x16{};
-      const int32_t krow = 32 * kb + sigma;
-#pragma unroll
-      for (int si = 0; si < 8; ++si) {
-        const int32_t col = 2 * si + hl;
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + krow * 256 + ((col ^ (krow & 15)) << 4));
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[si], s[kb], 0, 0, 0);
-      }
-    }
-    if (t0 + BK > nk) {  // ragged last tile: keys beyond nk get no weight
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int32_t key = t0 + 32 * kb + 16 * (i >> 3) + 8 * hl + (i & 7);
-          if (key >= nk) s[kb][i] = -INFINITY;
-        }
-    }
-    float mx = s[0][0];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx * c2);
-    const float alpha = exp2f(m_run - m_new);
-    m_run = m_new;
-    l_run *= alpha;
-#pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
-
-    bf16x8 pb[2][2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int mm = 0; mm < 2; ++mm)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float p = exp2f(fmaf(s[kb][8 * mm + e], c2, -m_new));
-          l_run += p;
-          pb[kb][mm][e] = static_cast<__bf16>(p);
-        }
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int mm = 0; mm < 2; ++mm) {
-        const int32_t col = 4 * kb + 2 * mm + hl;
-#pragma unroll
-        for (int db = 0; db < 4; ++db) {
-          const int32_t drow = 32 * db + r32;
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(vl + drow * 128 + ((col ^ ((drow >> 1) & 7)) << 4));
-          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kb][mm], oacc[db], 0, 0, 0);
-        }
-      }
-    if (t + 1 < ntiles) store_lds((t + 1) & 1);
-    __syncthreads();
+  int32_t t = 0;
+  for (; t + 1 < nfull; t += 2) {
+    if (t + 1 < nfull) issue((t + 1) * BK, 1, std::false_type{});
+    else issue((t + 1) * BK, 1, std::true_type{});
+    attn_tile<0, false>(smem, L, qreg, oacc, m_run, l_run, c2, t * BK, nk, hl);
+    landed();
+    if (t + 2 < nfull) issue((t + 2) * BK, 0, std::false_type{});
+    else if (t + 2 < ntiles) issue((t + 2) * BK, 0, std::true_type{});
+    attn_tile<1, false>(smem, L, qreg, oacc, m_run, l_run, c2, (t + 1) * BK, nk, hl);
+    landed();
+  }
+  if (t < nfull) {  // t even: buffer 0
+    if (t + 1 < ntiles) issue((t + 1) * BK, 1, std::true_type{});
+    attn_tile<0, false>(smem, L, qreg, oacc, m_run, l_run, c2, t * BK, nk, hl);
+    landed();
+    ++t;
+  }
+  if (t < ntiles) {  // ragged last tile (the only one that needs masking)
+    if (t & 1)
+      attn_tile<1, true>(smem, L, qreg, oacc, m_run, l_run, c2, t * BK, nk, hl);
+    else
+      attn_tile<0, true>(smem, L, qreg, oacc, m_run, l_run, c2, t * BK, nk, hl);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
@@ -295,6 +377,11 @@ int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const v
                          static_cast<const float*>(q), static_cast<float*>(o), g, plan);
   } else {
     if (d.head_dim != HDB) return fail(SC_EUNSUPPORTED, "bf16 attention needs head_dim 128");
+    if (d.tokens_per_page < BK)
+      return fail(SC_EUNSUPPORTED, "bf16 attention needs pages of >= %d tokens (got %d)", BK,
+                  d.tokens_per_page);
+    if ((uint64_t)d.n_slots * c->slot_bytes > 0xffffffffull)
+      return fail(SC_EUNSUPPORTED, "bf16 attention needs one layer of the pool within 4 GB");
     g.n_qtiles = (p->nq + BQ - 1) / BQ;
     const uint32_t nwg = (uint32_t)n * d.n_heads * g.n_qtiles;
     hipLaunchKernelGGL(attn_bf16_kernel, dim3(nwg), dim3(256), 0, stream,

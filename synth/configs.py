@@ -43,9 +43,10 @@ TINY = Geometry(heads=2, head_dim=64, grid_h=4, grid_w=4, frames_per_chunk=2, K=
 WAN = Geometry(heads=12, head_dim=128, grid_h=30, grid_w=52, frames_per_chunk=3, K=4, W=6,
                hidden=1536, mlp=8960)
 
-# Small bf16 shape spanning several 64-key tiles with ragged page tails
-# (40 tokens per page), used by the fast GPU parity tests.
-SMALL = Geometry(heads=2, head_dim=128, grid_h=5, grid_w=8, frames_per_chunk=3, K=4, W=6,
+# Small bf16 shape spanning several 64-key tiles, with pages (104 tokens)
+# that end inside a tile and nodes whose last tile is ragged; used by the
+# fast GPU parity tests.
+SMALL = Geometry(heads=2, head_dim=128, grid_h=8, grid_w=13, frames_per_chunk=3, K=4, W=6,
                  hidden=256, mlp=512, rope_dims=(44, 42, 42))
 
 
