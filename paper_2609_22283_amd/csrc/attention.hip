@@ -6,8 +6,8 @@
 // a multiple of 8 tokens, so any 8 consecutive keys of the concatenation that
 // start at a multiple of 8 lie in one page.
 //
-// bf16 kernel (head_dim 128), per work-group: 128 queries of one (node, head),
-// four waves of 32 queries.  Key tiles of 64 are staged through LDS (double
+// bf16 kernel (head_dim 128), per work-group: 256 queries of one (node, head),
+// eight waves of 32 queries.  Key tiles of 64 are copied into LDS (double
 // buffered, XOR-swizzled against bank conflicts); each wave computes
 // S^T = K Q^T and O^T += V^T P^T with 32x32x16 bf16 MFMAs and keeps an online
 // softmax in fp32.  The K rows feeding the S^T MFMA are permuted so that each
@@ -84,12 +84,13 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 }
 
 // ------------------------------------------------------------- bf16 kernel
-constexpr int BQ = 128;       // queries per work-group
-constexpr int BK = 64;        // keys per tile
-constexpr int HDB = 128;      // head dim of the bf16 kernel
-constexpr int KT_BYTES = BK * HDB * 2;   // 16 KB
-constexpr int VT_BYTES = HDB * BK * 2;   // 16 KB
-constexpr int BUF_BYTES = KT_BYTES + VT_BYTES;
+constexpr int NWAVES = 8;              // waves per work-group, 32 queries each
+constexpr int BQ = 32 * NWAVES;        // queries per work-group
+constexpr int BK = 64;                 // keys per tile
+constexpr int HDB = 128;               // head dim of the bf16 kernel
+constexpr int KT_BYTES = BK * HDB * 2;  // 16 KB
+constexpr int VT_BYTES = HDB * BK * 2;  // 16 KB
+constexpr int SMEM_BYTES = 2 * (KT_BYTES + VT_BYTES);
 // Running maxima are only raised when a tile's maximum exceeds them by more
 // than this many powers of two; probabilities then stay below 2^8, which fp32
 // sums and bf16 products hold exactly as well as values below 1.
@@ -101,13 +102,9 @@ struct AttnLane {
   uint32_t voff[4];   // V^T row r32, column 4 kb + 2 mm + hl    (db adds 4096)
 };
 
-template <int BUF, bool MASK>
-__device__ __forceinline__ void attn_tile(const char* smem, const AttnLane& L, const bf16x8 (&qreg)[8],
-                                          f32x16 (&oacc)[4], float& m_run, float& l_run, float c2,
-                                          int32_t t0, int32_t nk, int32_t hl) {
-  const char* kl = smem + BUF * BUF_BYTES;
-  const char* vl = kl + KT_BYTES;
-  f32x16 s[2];
+// S^T blocks of one tile: s[kb] = K_kb Q^T for the two 32-key halves.
+__device__ __forceinline__ void qk_tile(const char* kl, const AttnLane& L, const bf16x8 (&qreg)[8],
+                                        f32x16 (&s)[2]) {
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
     s[kb] = f32x16{};
@@ -117,6 +114,17 @@ __device__ __forceinline__ void attn_tile(const char* smem, const AttnLane& L, c
       s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[si], s[kb], 0, 0, 0);
     }
   }
+}
+
+// One step of the software-pipelined loop, for tile t: softmax of S(t)
+// (held in s), the next tile's S(t+1) = K(t+1) Q^T on the matrix cores while
+// the exponentials of tile t run on the vector ALUs, then O^T += V(t)^T P(t).
+// K runs one tile ahead of V: K(t+1) sits in K buffer KN, V(t) in V buffer VC.
+template <int KN, int VC, bool NEXT, bool MASK>
+__device__ __forceinline__ void attn_step(const char* smem, const AttnLane& L, const bf16x8 (&qreg)[8],
+                                          f32x16 (&oacc)[4], f32x16 (&s)[2], float& m_run,
+                                          float& l_run, float c2, int32_t t0, int32_t nk,
+                                          int32_t hl) {
   if constexpr (MASK) {  // keys past the node's last key get no weight
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -154,26 +162,25 @@ __device__ __forceinline__ void attn_tile(const char* smem, const AttnLane& L, c
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         pb[kb][mm][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(s[kb][8 * mm + e], c2, -m_run)));
-  // row sum of the rounded probabilities (what the PV product uses)
+  if constexpr (NEXT) qk_tile(smem + KN * KT_BYTES, L, qreg, s);
+  const char* vl = smem + 2 * KT_BYTES + VC * VT_BYTES;
   const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-    for (int mm = 0; mm < 2; ++mm)
-#pragma unroll
-      for (int e = 0; e < 8; e += 2) {
-        const bf16x2 pair = {pb[kb][mm][e], pb[kb][mm][e + 1]};
-        l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
-      }
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int mm = 0; mm < 2; ++mm)
+    for (int mm = 0; mm < 2; ++mm) {
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
         const bf16x8 a = *reinterpret_cast<const bf16x8*>(vl + L.voff[2 * kb + mm] + db * 4096);
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kb][mm], oacc[db], 0, 0, 0);
       }
+      // row sum of the rounded probabilities (what the PV product uses)
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const bf16x2 pair = {pb[kb][mm][e], pb[kb][mm][e + 1]};
+        l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
+      }
+    }
 }
 
 // Direct global -> LDS copy of 16 bytes per lane (gfx950 LDS DMA): lane i
@@ -186,10 +193,11 @@ __device__ __forceinline__ void dma16(const char* src, char* lds_wave_base) {
                                    16, 0, 0);
 }
 
-__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __restrict__ q,
+__global__ __launch_bounds__(64 * NWAVES, 1) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                            uint16_t* __restrict__ o, AttnGeom g,
                                                            AttnPlan plan) {
-  __shared__ __attribute__((aligned(1024))) char smem[2 * BUF_BYTES];
+  // K buffers 0, 1 then V^T buffers 0, 1 (16 KB each)
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM_BYTES];
   const uint32_t nwg = (uint32_t)g.n_nodes * g.n_heads * g.n_qtiles;
   const uint32_t w = xcd_remap(blockIdx.x, nwg);
   const int32_t qt = w % g.n_qtiles;
@@ -202,15 +210,17 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   const int32_t npages = plan.page_off[node + 1] - p0;
   const int32_t nk = npages * g.tpp;
   const int32_t ntiles = (nk + BK - 1) / BK;
-  const int32_t nfull = nk / BK;
+  const bool ragged = (nk % BK) != 0;
 
   // Q^T operand: lane holds Q[row][16 si + 8 hl .. +7] for si = 0..7.
   const int32_t qrow = qt * BQ + wave * 32 + r32;
-  const int32_t qrow_c = qrow < g.nq ? qrow : g.nq - 1;
-  const uint16_t* qp = q + (((size_t)node * g.nq + qrow_c) * g.n_heads + head) * HDB + 8 * hl;
   bf16x8 qreg[8];
+  {
+    const int32_t qrow_c = qrow < g.nq ? qrow : g.nq - 1;
+    const uint16_t* qp = q + (((size_t)node * g.nq + qrow_c) * g.n_heads + head) * HDB + 8 * hl;
 #pragma unroll
-  for (int si = 0; si < 8; ++si) qreg[si] = *reinterpret_cast<const bf16x8*>(qp + 16 * si);
+    for (int si = 0; si < 8; ++si) qreg[si] = *reinterpret_cast<const bf16x8*>(qp + 16 * si);
+  }
 
   // Row sigma of the S^T MFMA holds key sigma: each lane's probabilities are
   // then keys 8 hl .. 8 hl + 7 (+16) of every 32-key block -- exactly the B
@@ -231,61 +241,71 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   // tokens), so the page of a key is chosen against one wave-uniform
   // boundary.  Offsets are 32-bit, relative to the layer's slots (the host
   // checks a layer fits in 4 GB); the per-page parts are wave-uniform.  Per
-  // wave: 4 copies of 4 K rows (1 KB each) and 4 copies of 8 V^T rows.  Lane
+  // wave: 2 copies of 4 K rows (1 KB each) and 2 copies of 8 V^T rows.  Lane
   // (row, physical column p) fetches logical column p ^ swizzle(row).
   const char* lbase = g.layer_base;
   const uint32_t khead = (uint32_t)head * g.tpp * HDB * 2;
   const uint32_t vhead = (uint32_t)g.kv_half + (uint32_t)head * HDB * g.tpp * 2;
-  const int32_t krow0 = 16 * wave + (lane >> 4), kp = lane & 15;
-  const int32_t vrow0 = 32 * wave + (lane >> 3), vp = lane & 7;
-  uint32_t kswz[4], vlane[4];
-  int32_t vkey[4];
+  constexpr int KCP = 64 / (4 * NWAVES), VCP = 128 / (8 * NWAVES);  // copies per wave
+  const int32_t krow0 = 4 * KCP * wave + (lane >> 4), kp = lane & 15;
+  const int32_t vrow0 = 8 * VCP * wave + (lane >> 3), vp = lane & 7;
+  uint32_t kswz[KCP], vlane[VCP];
+  int32_t vkey[VCP];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < KCP; ++j) {
     const int32_t row = krow0 + 4 * j;
     kswz[j] = (uint32_t)row * 256 + ((kp ^ (row & 15)) << 4);   // plus t0 * 256
+  }
+#pragma unroll
+  for (int j = 0; j < VCP; ++j) {
     const int32_t d = vrow0 + 8 * j;
     vkey[j] = 8 * (vp ^ ((d >> 1) & 7));                           // key offset in tile
     vlane[j] = (uint32_t)d * g.tpp * 2 + (uint32_t)vkey[j] * 2;    // plus t0 * 2
   }
-  auto issue = [&](int32_t t0, int buf, auto clamp_c) {
-    constexpr bool CLAMP = decltype(clamp_c)::value;
+  struct PageSplit {
+    uint32_t lo, hi;  // layer-relative byte offset of key t0 on page lo / hi (head included)
+    int32_t split;    // tile-relative first key on page hi
+  };
+  auto pages = [&](int32_t t0, uint32_t head_off, uint32_t row_bytes) {
     const int32_t plo = (int32_t)fast_div((uint32_t)t0, g.tpp_div);
     const int32_t bkey = (plo + 1) * g.tpp;
     const int32_t phi = plo + 1 < npages ? plo + 1 : plo;
     const uint32_t slo = (uint32_t)plan.page_slot[p0 + plo] * (uint32_t)g.slot_bytes;
     const uint32_t shi = (uint32_t)plan.page_slot[p0 + phi] * (uint32_t)g.slot_bytes;
-    // offset of key k on page lo: slo + head part + (k - plo*tpp) * row bytes
-    const uint32_t k_lo = slo + khead - (uint32_t)plo * g.tpp * 256 + (uint32_t)t0 * 256;
-    const uint32_t k_hi = shi + khead - (uint32_t)bkey * 256 + (uint32_t)t0 * 256;
-    const uint32_t v_lo = slo + vhead - (uint32_t)plo * g.tpp * 2 + (uint32_t)t0 * 2;
-    const uint32_t v_hi = shi + vhead - (uint32_t)bkey * 2 + (uint32_t)t0 * 2;
-    const int32_t split = bkey - t0;  // tile-relative first key of page hi
-    char* kl = smem + buf * BUF_BYTES;
-    char* vl = kl + KT_BYTES;
+    PageSplit ps;
+    ps.lo = slo + head_off - (uint32_t)plo * g.tpp * row_bytes + (uint32_t)t0 * row_bytes;
+    ps.hi = shi + head_off - (uint32_t)bkey * row_bytes + (uint32_t)t0 * row_bytes;
+    ps.split = bkey - t0;
+    return ps;
+  };
+  auto issue_k = [&](int32_t tile, int buf) {
+    const int32_t t0 = tile * BK;
+    const PageSplit ps = pages(t0, khead, 256);
+    char* kl = smem + buf * KT_BYTES;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < KCP; ++j) {
       int32_t rk = krow0 + 4 * j;  // tile-relative key
       uint32_t lo = kswz[j];
-      if constexpr (CLAMP) {
-        if (t0 + rk >= nk) {
-          lo -= (uint32_t)(t0 + rk - (nk - 1)) * 256;
-          rk = nk - 1 - t0;
-        }
+      if (t0 + rk >= nk) {         // ragged last tile: repeat the last key
+        lo -= (uint32_t)(t0 + rk - (nk - 1)) * 256;
+        rk = nk - 1 - t0;
       }
-      dma16(lbase + ((rk < split ? k_lo : k_hi) + lo), kl + (16 * wave + 4 * j) * 256);
+      dma16(lbase + ((rk < ps.split ? ps.lo : ps.hi) + lo), kl + (4 * KCP * wave + 4 * j) * 256);
     }
+  };
+  auto issue_v = [&](int32_t tile, int buf) {
+    const int32_t t0 = tile * BK;
+    const PageSplit ps = pages(t0, vhead, 2);
+    char* vl = smem + 2 * KT_BYTES + buf * VT_BYTES;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < VCP; ++j) {
       int32_t rk = vkey[j];
       uint32_t lo = vlane[j];
-      if constexpr (CLAMP) {
-        if (t0 + rk >= nk) {
-          lo -= (uint32_t)(t0 + rk - (nk - 8)) * 2;
-          rk = nk - 8 - t0;
-        }
+      if (t0 + rk >= nk) {
+        lo -= (uint32_t)(t0 + rk - (nk - 8)) * 2;
+        rk = nk - 8 - t0;
       }
-      dma16(lbase + ((rk < split ? v_lo : v_hi) + lo), vl + (32 * wave + 8 * j) * 128);
+      dma16(lbase + ((rk < ps.split ? ps.lo : ps.hi) + lo), vl + (8 * VCP * wave + 8 * j) * 128);
     }
   };
   auto landed = [&]() {  // this wave's copies are in LDS, then everyone's
@@ -299,32 +319,40 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   float m_run = -INFINITY, l_run = 0.f;
   const float c2 = g.scale_log2;
 
-  if (ntiles > 1) issue(0, 0, std::false_type{});
-  else issue(0, 0, std::true_type{});
+  // prologue: K(0), V(0), K(1) in flight; S(0) = K(0) Q^T
+  issue_k(0, 0);
+  issue_v(0, 0);
+  if (ntiles > 1) issue_k(1, 1);
   landed();
+  f32x16 s[2];
+  qk_tile(smem, L, qreg, s);
 
+  // iteration t: copy K(t+2) over K(t) and V(t+1) over V(t-1), then step t
   int32_t t = 0;
-  for (; t + 1 < nfull; t += 2) {
-    if (t + 1 < nfull) issue((t + 1) * BK, 1, std::false_type{});
-    else issue((t + 1) * BK, 1, std::true_type{});
-    attn_tile<0, false>(smem, L, qreg, oacc, m_run, l_run, c2, t * BK, nk, hl);
+  for (; t + 2 < ntiles; t += 2) {
+    issue_k(t + 2, 0);
+    issue_v(t + 1, 1);
+    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, c2, t * BK, nk, hl);
     landed();
-    if (t + 2 < nfull) issue((t + 2) * BK, 0, std::false_type{});
-    else if (t + 2 < ntiles) issue((t + 2) * BK, 0, std::true_type{});
-    attn_tile<1, false>(smem, L, qreg, oacc, m_run, l_run, c2, (t + 1) * BK, nk, hl);
+    if (t + 3 < ntiles) issue_k(t + 3, 1);
+    issue_v(t + 2, 0);
+    attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m_run, l_run, c2, (t + 1) * BK, nk, hl);
     landed();
   }
-  if (t < nfull) {  // t even: buffer 0
-    if (t + 1 < ntiles) issue((t + 1) * BK, 1, std::true_type{});
-    attn_tile<0, false>(smem, L, qreg, oacc, m_run, l_run, c2, t * BK, nk, hl);
+  if (t + 1 < ntiles) {  // two tiles left, t even
+    issue_v(t + 1, 1);
+    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, c2, t * BK, nk, hl);
     landed();
     ++t;
-  }
-  if (t < ntiles) {  // ragged last tile (the only one that needs masking)
-    if (t & 1)
-      attn_tile<1, true>(smem, L, qreg, oacc, m_run, l_run, c2, t * BK, nk, hl);
+    if (ragged)
+      attn_step<0, 1, false, true>(smem, L, qreg, oacc, s, m_run, l_run, c2, t * BK, nk, hl);
     else
-      attn_tile<0, true>(smem, L, qreg, oacc, m_run, l_run, c2, t * BK, nk, hl);
+      attn_step<0, 1, false, false>(smem, L, qreg, oacc, s, m_run, l_run, c2, t * BK, nk, hl);
+  } else {               // one tile left, t even
+    if (ragged)
+      attn_step<1, 0, false, true>(smem, L, qreg, oacc, s, m_run, l_run, c2, t * BK, nk, hl);
+    else
+      attn_step<1, 0, false, false>(smem, L, qreg, oacc, s, m_run, l_run, c2, t * BK, nk, hl);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
@@ -384,7 +412,7 @@ int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const v
       return fail(SC_EUNSUPPORTED, "bf16 attention needs one layer of the pool within 4 GB");
     g.n_qtiles = (p->nq + BQ - 1) / BQ;
     const uint32_t nwg = (uint32_t)n * d.n_heads * g.n_qtiles;
-    hipLaunchKernelGGL(attn_bf16_kernel, dim3(nwg), dim3(256), 0, stream,
+    hipLaunchKernelGGL(attn_bf16_kernel, dim3(nwg), dim3(64 * NWAVES), 0, stream,
                        static_cast<const uint16_t*>(q), static_cast<uint16_t*>(o), g, plan);
   }
   timer_end(TK_ATTENTION, stream);
