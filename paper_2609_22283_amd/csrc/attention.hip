@@ -91,10 +91,13 @@ constexpr int HDB = 128;               // head dim of the bf16 kernel
 constexpr int KT_BYTES = BK * HDB * 2;  // 16 KB
 constexpr int VT_BYTES = HDB * BK * 2;  // 16 KB
 constexpr int SMEM_BYTES = 2 * (KT_BYTES + VT_BYTES);
-// Running maxima are only raised when a tile's maximum exceeds them by more
-// than this many powers of two; probabilities then stay below 2^8, which fp32
-// sums and bf16 products hold exactly as well as values below 1.
-constexpr float RESCALE_LOG2 = 8.0f;
+// Softmax bookkeeping.  Q is pre-scaled by scale*log2(e), so S is in log2
+// units, and each S tile starts its accumulation at -m (the running
+// maximum): p = exp2(S) directly.  m is the exact maximum of the first tile
+// and is raised only when a later tile's probabilities overflow 2^64 (their
+// sum is checked); until then p may exceed 1, which fp32 sums and bf16
+// products represent with the same relative precision.
+constexpr float GROW_LIMIT = 18446744073709551616.0f;  // 2^64
 
 struct AttnLane {
   // per-lane LDS read offsets (bytes) inside one buffer
@@ -102,12 +105,13 @@ struct AttnLane {
   uint32_t voff[4];   // V^T row r32, column 4 kb + 2 mm + hl    (db adds 4096)
 };
 
-// S^T blocks of one tile: s[kb] = K_kb Q^T for the two 32-key halves.
+// S^T blocks of one tile, s[kb] = K_kb Q^T - m for the two 32-key halves.
 __device__ __forceinline__ void qk_tile(const char* kl, const AttnLane& L, const bf16x8 (&qreg)[8],
-                                        f32x16 (&s)[2]) {
+                                        f32x16 (&s)[2], float m) {
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
-    s[kb] = f32x16{};
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s[kb][i] = -m;
 #pragma unroll
     for (int si = 0; si < 8; ++si) {
       const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + L.koff[si] + kb * 8192);
@@ -116,15 +120,48 @@ __device__ __forceinline__ void qk_tile(const char* kl, const AttnLane& L, const
   }
 }
 
-// One step of the software-pipelined loop, for tile t: softmax of S(t)
-// (held in s), the next tile's S(t+1) = K(t+1) Q^T on the matrix cores while
-// the exponentials of tile t run on the vector ALUs, then O^T += V(t)^T P(t).
-// K runs one tile ahead of V: K(t+1) sits in K buffer KN, V(t) in V buffer VC.
+__device__ __forceinline__ float tile_max(const f32x16 (&s)[2]) {
+  float mx = fmaxf(s[0][0], s[0][1]);
+#pragma unroll
+  for (int i = 2; i < 16; ++i) mx = fmaxf(mx, s[0][i]);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[1][i]);
+  return fmaxf(mx, __shfl_xor(mx, 32));
+}
+
+// p = exp2(s) rounded to bf16 (the B operands of the PV MFMA) and the sum of
+// the rounded values.
+__device__ __forceinline__ float probs(const f32x16 (&s)[2], bf16x8 (&pb)[2][2]) {
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int mm = 0; mm < 2; ++mm)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        pb[kb][mm][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(s[kb][8 * mm + e]));
+  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+  float l0 = 0.f, l1 = 0.f;
+#pragma unroll
+  for (int mm = 0; mm < 2; ++mm)
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      const bf16x2 p0 = {pb[0][mm][e], pb[0][mm][e + 1]};
+      const bf16x2 p1 = {pb[1][mm][e], pb[1][mm][e + 1]};
+      l0 = __builtin_amdgcn_fdot2_f32_bf16(p0, ones, l0, false);
+      l1 = __builtin_amdgcn_fdot2_f32_bf16(p1, ones, l1, false);
+    }
+  return l0 + l1;
+}
+
+// One step of the software-pipelined loop, for tile t: probabilities of
+// S(t) (held in s), the next tile's S(t+1) = K(t+1) Q^T - m on the matrix
+// cores while the exponentials of tile t run on the vector ALUs, then
+// O^T += V(t)^T P(t).  K runs one tile ahead of V: K(t+1) sits in K buffer
+// KN, V(t) in V buffer VC.
 template <int KN, int VC, bool NEXT, bool MASK>
 __device__ __forceinline__ void attn_step(const char* smem, const AttnLane& L, const bf16x8 (&qreg)[8],
                                           f32x16 (&oacc)[4], f32x16 (&s)[2], float& m_run,
-                                          float& l_run, float c2, int32_t t0, int32_t nk,
-                                          int32_t hl) {
+                                          float& l_run, int32_t t0, int32_t nk, int32_t hl) {
   if constexpr (MASK) {  // keys past the node's last key get no weight
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -134,53 +171,47 @@ __device__ __forceinline__ void attn_step(const char* smem, const AttnLane& L, c
         if (key >= nk) s[kb][i] = -INFINITY;
       }
   }
-  float mx = fmaxf(s[0][0], s[0][1]);
-#pragma unroll
-  for (int i = 2; i < 16; ++i) mx = fmaxf(mx, s[0][i]);
-#pragma unroll
-  for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[1][i]);
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
-  const float m_tile = mx * c2;
-  if (__builtin_amdgcn_ballot_w64(m_tile > m_run + RESCALE_LOG2)) {
-    // an opaque statement keeps this a (wave-uniform) branch instead of
-    // being flattened into 64 unconditional multiplies per tile
+  bf16x8 pb[2][2];
+  float l_tile = probs(s, pb);
+  f32x16 sn[2];
+  if constexpr (NEXT) qk_tile(smem + KN * KT_BYTES, L, qreg, sn, m_run);
+  if (__builtin_amdgcn_ballot_w64(!(l_tile < GROW_LIMIT))) {
+    // rare: raise the running maximum to this tile's and redo the tile (the
+    // next tile's logits were offset by the old maximum).  The opaque
+    // statement keeps this a wave-uniform branch.
     asm volatile("" ::: "memory");
-    const float m_new = fmaxf(m_run, m_tile);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
+    const float grow = fmaxf(tile_max(s), 0.f);
+    const float alpha = __builtin_amdgcn_exp2f(-grow);
+    m_run += grow;
     l_run *= alpha;
 #pragma unroll
     for (int db = 0; db < 4; ++db)
 #pragma unroll
       for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        s[kb][i] -= grow;
+        if constexpr (NEXT) sn[kb][i] -= grow;
+      }
+    l_tile = probs(s, pb);
   }
-  bf16x8 pb[2][2];
+  l_run += l_tile;
+  const char* vl = smem + 2 * KT_BYTES + VC * VT_BYTES;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int mm = 0; mm < 2; ++mm)
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        pb[kb][mm][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(s[kb][8 * mm + e], c2, -m_run)));
-  if constexpr (NEXT) qk_tile(smem + KN * KT_BYTES, L, qreg, s);
-  const char* vl = smem + 2 * KT_BYTES + VC * VT_BYTES;
-  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int mm = 0; mm < 2; ++mm) {
-#pragma unroll
       for (int db = 0; db < 4; ++db) {
         const bf16x8 a = *reinterpret_cast<const bf16x8*>(vl + L.voff[2 * kb + mm] + db * 4096);
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kb][mm], oacc[db], 0, 0, 0);
       }
-      // row sum of the rounded probabilities (what the PV product uses)
-#pragma unroll
-      for (int e = 0; e < 8; e += 2) {
-        const bf16x2 pair = {pb[kb][mm][e], pb[kb][mm][e + 1]};
-        l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
-      }
-    }
+  if constexpr (NEXT) {
+    s[0] = sn[0];
+    s[1] = sn[1];
+  }
 }
 
 // Direct global -> LDS copy of 16 bytes per lane (gfx950 LDS DMA): lane i
@@ -219,7 +250,12 @@ __global__ __launch_bounds__(64 * NWAVES, 1) void attn_bf16_kernel(const uint16_
     const int32_t qrow_c = qrow < g.nq ? qrow : g.nq - 1;
     const uint16_t* qp = q + (((size_t)node * g.nq + qrow_c) * g.n_heads + head) * HDB + 8 * hl;
 #pragma unroll
-    for (int si = 0; si < 8; ++si) qreg[si] = *reinterpret_cast<const bf16x8*>(qp + 16 * si);
+    for (int si = 0; si < 8; ++si) {
+      const bf16x8 raw = *reinterpret_cast<const bf16x8*>(qp + 16 * si);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)  // logits in log2 units: Q * scale * log2(e)
+        qreg[si][e] = static_cast<__bf16>(static_cast<float>(raw[e]) * g.scale_log2);
+    }
   }
 
   // Row sigma of the S^T MFMA holds key sigma: each lane's probabilities are
@@ -278,34 +314,34 @@ __global__ __launch_bounds__(64 * NWAVES, 1) void attn_bf16_kernel(const uint16_
     ps.split = bkey - t0;
     return ps;
   };
-  auto issue_k = [&](int32_t tile, int buf) {
+  // Keys past the node's end (ragged last tile) fetch the tile's first key
+  // instead: valid memory, and its probability is masked to zero anyway.
+  auto copy_k = [&](int32_t tile, int buf) {
     const int32_t t0 = tile * BK;
     const PageSplit ps = pages(t0, khead, 256);
+    const int32_t lim = nk - t0;
     char* kl = smem + buf * KT_BYTES;
 #pragma unroll
     for (int j = 0; j < KCP; ++j) {
-      int32_t rk = krow0 + 4 * j;  // tile-relative key
-      uint32_t lo = kswz[j];
-      if (t0 + rk >= nk) {         // ragged last tile: repeat the last key
-        lo -= (uint32_t)(t0 + rk - (nk - 1)) * 256;
-        rk = nk - 1 - t0;
-      }
-      dma16(lbase + ((rk < ps.split ? ps.lo : ps.hi) + lo), kl + (4 * KCP * wave + 4 * j) * 256);
+      const int32_t rk = krow0 + 4 * j;  // tile-relative key
+      const bool in = rk < lim;
+      const uint32_t lo = in ? kswz[j] : kswz[j] - (uint32_t)rk * 256;
+      const uint32_t base = (in && rk >= ps.split) ? ps.hi : ps.lo;
+      dma16(lbase + (base + lo), kl + (4 * KCP * wave + 4 * j) * 256);
     }
   };
-  auto issue_v = [&](int32_t tile, int buf) {
+  auto copy_v = [&](int32_t tile, int buf) {
     const int32_t t0 = tile * BK;
     const PageSplit ps = pages(t0, vhead, 2);
+    const int32_t lim = nk - t0;
     char* vl = smem + 2 * KT_BYTES + buf * VT_BYTES;
 #pragma unroll
     for (int j = 0; j < VCP; ++j) {
-      int32_t rk = vkey[j];
-      uint32_t lo = vlane[j];
-      if (t0 + rk >= nk) {
-        lo -= (uint32_t)(t0 + rk - (nk - 8)) * 2;
-        rk = nk - 8 - t0;
-      }
-      dma16(lbase + ((rk < ps.split ? ps.lo : ps.hi) + lo), vl + (8 * VCP * wave + 8 * j) * 128);
+      const int32_t rk = vkey[j];
+      const bool in = rk < lim;
+      const uint32_t lo = in ? vlane[j] : vlane[j] - (uint32_t)rk * 2;
+      const uint32_t base = (in && rk >= ps.split) ? ps.hi : ps.lo;
+      dma16(lbase + (base + lo), vl + (8 * VCP * wave + 8 * j) * 128);
     }
   };
   auto landed = [&]() {  // this wave's copies are in LDS, then everyone's
@@ -316,43 +352,54 @@ __global__ __launch_bounds__(64 * NWAVES, 1) void attn_bf16_kernel(const uint16_
   f32x16 oacc[4];
 #pragma unroll
   for (int db = 0; db < 4; ++db) oacc[db] = f32x16{};
-  float m_run = -INFINITY, l_run = 0.f;
-  const float c2 = g.scale_log2;
-
-  // prologue: K(0), V(0), K(1) in flight; S(0) = K(0) Q^T
-  issue_k(0, 0);
-  issue_v(0, 0);
-  if (ntiles > 1) issue_k(1, 1);
+  float m_run = 0.f, l_run = 0.f;
+  // prologue: K(0), V(0), K(1) in flight; S(0) = K(0) Q^T; m = its exact max
+  copy_k(0, 0);
+  copy_v(0, 0);
+  if (ntiles > 1) copy_k(1, 1);
   landed();
   f32x16 s[2];
-  qk_tile(smem, L, qreg, s);
+  qk_tile(smem, L, qreg, s, 0.f);
+  if (ntiles == 1 && ragged) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (32 * kb + 16 * (i >> 3) + 8 * hl + (i & 7) >= nk) s[kb][i] = -INFINITY;
+  }
+  m_run = tile_max(s);
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s[kb][i] -= m_run;
+  __syncthreads();  // every wave has read K(0) before K(2) is copied over it
 
   // iteration t: copy K(t+2) over K(t) and V(t+1) over V(t-1), then step t
   int32_t t = 0;
   for (; t + 2 < ntiles; t += 2) {
-    issue_k(t + 2, 0);
-    issue_v(t + 1, 1);
-    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, c2, t * BK, nk, hl);
+    copy_k(t + 2, 0);
+    copy_v(t + 1, 1);
+    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
     landed();
-    if (t + 3 < ntiles) issue_k(t + 3, 1);
-    issue_v(t + 2, 0);
-    attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m_run, l_run, c2, (t + 1) * BK, nk, hl);
+    if (t + 3 < ntiles) copy_k(t + 3, 1);
+    copy_v(t + 2, 0);
+    attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m_run, l_run, (t + 1) * BK, nk, hl);
     landed();
   }
   if (t + 1 < ntiles) {  // two tiles left, t even
-    issue_v(t + 1, 1);
-    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, c2, t * BK, nk, hl);
+    copy_v(t + 1, 1);
+    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
     landed();
     ++t;
     if (ragged)
-      attn_step<0, 1, false, true>(smem, L, qreg, oacc, s, m_run, l_run, c2, t * BK, nk, hl);
+      attn_step<0, 1, false, true>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
     else
-      attn_step<0, 1, false, false>(smem, L, qreg, oacc, s, m_run, l_run, c2, t * BK, nk, hl);
-  } else {               // one tile left, t even
+      attn_step<0, 1, false, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
+  } else {               // one tile left, t even (masking twice is harmless)
     if (ragged)
-      attn_step<1, 0, false, true>(smem, L, qreg, oacc, s, m_run, l_run, c2, t * BK, nk, hl);
+      attn_step<1, 0, false, true>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
     else
-      attn_step<1, 0, false, false>(smem, L, qreg, oacc, s, m_run, l_run, c2, t * BK, nk, hl);
+      attn_step<1, 0, false, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
