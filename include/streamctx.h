@@ -219,6 +219,33 @@ int sc_sampler_step(const sc_node* nodes, int32_t n_nodes, const float* t, int32
                     void* out, const void* y, const void* noise, int64_t elems_per_node,
                     sc_stream stream);
 
+/* ---- Execution schedule (Sec. 3.3) --------------------------------------
+ * Pipelined execution, Eq. 7: round n advances every active chunk by one
+ * level -- chunk n - K + j sits at level j -- for chunks 0..B-1.  Without
+ * the refresh node the levels are 1..K (K + B - 1 rounds, B*K updates); with
+ * it the clean-state refresh (c, 0) of one chunk per round joins the round
+ * as its oldest node (K + B rounds, B*(K+1) forwards; the paper refreshes
+ * each chunk's clean KV once but does not say where, this is the reading).
+ * Nodes are written oldest chunk first; out needs room for K + 1 nodes.
+ * Errors: SC_EINVAL (K < 1, B < 1, n outside the schedule). */
+int sc_pipeline_rounds(int32_t K, int32_t B, int32_t refresh);
+int sc_pipeline_round_nodes(int32_t K, int32_t B, int32_t refresh, int32_t n, sc_node* out,
+                            int32_t* n_out);
+
+/* Releases every cached state that none of the given future nodes reads
+ * under the policy (Eq. 4-5 offsets and levels), keeping only what the rest
+ * of the schedule needs ("earlier states are retained", Sec. 3.3).  Returns
+ * the number of states released, or a negative SC_E* code. */
+int sc_cache_release_unread(sc_cache* cache, const sc_policy* policy, const sc_node* future,
+                            int32_t n_future);
+
+/* The network F_theta of Eq. 1 as a stack of n_layers blocks over one pack:
+ * sc_block_forward for layer 0 .. n_layers-1 in order (layers[l] holds the
+ * weights of layer l), x updated in place, one plan for every layer. */
+int sc_stack_forward(const sc_block_weights* layers, int32_t n_layers, sc_cache* cache,
+                     const sc_plan* plan, void* x, const sc_rope* rope, void* ws, size_t ws_bytes,
+                     sc_stream stream);
+
 /* ---- Kernel timing (measurement support) ------------------------------
  * While enabled, every kernel the library launches is bracketed by two HIP
  * events recorded on the launch stream.  sc_timer_read synchronises those

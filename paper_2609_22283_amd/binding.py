@@ -21,6 +21,7 @@ __all__ = [
     "sc_rope_table_bytes", "sc_rope_table_build", "sc_plan_build", "sc_attention",
     "sc_block_workspace_bytes", "sc_block_forward", "sc_sampler_step",
     "sc_timer_enable", "sc_timer_read", "Selection", "Cache", "Plan", "Rope", "BlockWeights",
+    "sc_pipeline_rounds", "sc_pipeline_round_nodes", "sc_cache_release_unread", "sc_stack_forward",
 ]
 
 SC_OK, SC_EINVAL, SC_EUNAVAILABLE, SC_ECAPACITY = 0, -1, -2, -3
@@ -39,6 +40,7 @@ EXPORTED_SYMBOLS = [
     "sc_plan_build", "sc_plan_get", "sc_plan_free",
     "sc_attention", "sc_block_workspace_bytes", "sc_block_forward", "sc_sampler_step",
     "sc_timer_enable", "sc_timer_read",
+    "sc_pipeline_rounds", "sc_pipeline_round_nodes", "sc_cache_release_unread", "sc_stack_forward",
 ]
 
 # The library and PyTorch must share one HIP runtime: torch ships its own
@@ -127,6 +129,12 @@ _SIG = {
                                   _P, _P, _P, C.c_int64, _P]),
     "sc_timer_enable": (C.c_int, [C.c_int]),
     "sc_timer_read": (C.c_int, [C.c_char_p, _I32P, C.POINTER(C.c_double)]),
+    "sc_pipeline_rounds": (C.c_int, [C.c_int32, C.c_int32, C.c_int32]),
+    "sc_pipeline_round_nodes": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                          C.POINTER(sc_node), _I32P]),
+    "sc_cache_release_unread": (C.c_int, [_P, C.POINTER(sc_policy), C.POINTER(sc_node), C.c_int32]),
+    "sc_stack_forward": (C.c_int, [C.POINTER(sc_block_weights), C.c_int32, _P, _P, _P,
+                                   C.POINTER(sc_rope), _P, C.c_size_t, _P]),
 }
 for _name, (_res, _args) in _SIG.items():
     _f = getattr(lib, _name)
@@ -376,3 +384,34 @@ def sc_timer_read(kind: str):
     n, ms = C.c_int32(), C.c_double()
     _check(lib.sc_timer_read(kind.encode(), C.byref(n), C.byref(ms)))
     return n.value, ms.value
+
+
+# ------------------------------------------------------------------- schedule
+def sc_pipeline_rounds(K: int, B: int, refresh: bool) -> int:
+    return _check(lib.sc_pipeline_rounds(K, B, 1 if refresh else 0))
+
+
+def sc_pipeline_round_nodes(K: int, B: int, refresh: bool, n: int):
+    """Nodes of pipelined round n (Eq. 7, plus the refresh node), oldest first."""
+    buf = (sc_node * (K + 1))()
+    m = C.c_int32()
+    _check(lib.sc_pipeline_round_nodes(K, B, 1 if refresh else 0, n, buf, C.byref(m)))
+    return [(buf[i].chunk, buf[i].level) for i in range(m.value)]
+
+
+def sc_cache_release_unread(cache: "Cache", kind, K, W, future, phi_table=None, r_mask=None) -> int:
+    """Release every cached state none of the future nodes reads; returns the count."""
+    pol, keep = _policy_struct(kind, K, W, phi_table, r_mask)
+    arr = (sc_node * max(1, len(future)))(*[sc_node(int(c), int(j)) for c, j in future])
+    n = _check(lib.sc_cache_release_unread(cache.handle, C.byref(pol), arr, len(future)))
+    del keep
+    return n
+
+
+def sc_stack_forward(layers, cache: "Cache", plan: "Plan", x, rope: "Rope", ws, ws_bytes: int,
+                     stream=None) -> None:
+    """All layers of a block stack over one pack (layers: list of BlockWeights)."""
+    arr = (sc_block_weights * len(layers))(*[w.struct for w in layers])
+    _check(lib.sc_stack_forward(arr, len(layers), cache.handle, plan.handle, _ptr(x),
+                                C.byref(rope.struct) if rope is not None else None, _ptr(ws),
+                                ws_bytes, _stream(stream)))

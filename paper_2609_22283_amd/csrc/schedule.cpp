@@ -1,0 +1,74 @@
+// Execution schedule (Sec. 3.3, Eq. 7): round packs, retention, stack forward.
+#include <set>
+
+#include "internal.h"
+
+using namespace sc;
+
+extern "C" int sc_pipeline_rounds(int32_t K, int32_t B, int32_t refresh) {
+  if (K < 1 || B < 1) return fail(SC_EINVAL, "need K >= 1 and B >= 1");
+  return refresh ? K + B : K + B - 1;
+}
+
+extern "C" int sc_pipeline_round_nodes(int32_t K, int32_t B, int32_t refresh, int32_t n, sc_node* out,
+                                       int32_t* n_out) {
+  if (!out || !n_out) return fail(SC_EINVAL, "null argument");
+  const int rounds = sc_pipeline_rounds(K, B, refresh);
+  if (rounds < 0) return rounds;
+  if (n < 0 || n >= rounds) return fail(SC_EINVAL, "round %d outside [0, %d)", n, rounds);
+  int32_t m = 0;
+  // chunk n - K + j at level j; ascending j is ascending chunk (oldest first)
+  for (int32_t j = refresh ? 0 : 1; j <= K; ++j) {
+    const int32_t c = n - K + j;
+    if (c >= 0 && c < B) out[m++] = sc_node{c, j};
+  }
+  *n_out = m;
+  return SC_OK;
+}
+
+static int read_level(const sc_policy* p, int32_t j, int32_t r) {
+  switch (p->kind) {
+    case SC_POLICY_CLEAN: return 0;
+    case SC_POLICY_SAME: return j;
+    case SC_POLICY_PROG: return j - r > 0 ? j - r : 0;
+    default: return p->phi_table[j * p->W + (r - 1)];
+  }
+}
+
+extern "C" int sc_cache_release_unread(sc_cache* c, const sc_policy* p, const sc_node* future,
+                                       int32_t n_future) {
+  if (!c || !p || (n_future > 0 && !future)) return fail(SC_EINVAL, "null argument");
+  if (p->K < 1 || p->W < 0 || p->kind < SC_POLICY_CLEAN || p->kind > SC_POLICY_TABLE ||
+      (p->kind == SC_POLICY_TABLE && p->W > 0 && !p->phi_table))
+    return fail(SC_EINVAL, "bad policy");
+  std::set<StateKey> needed;
+  for (int32_t i = 0; i < n_future; ++i) {
+    const int32_t cc = future[i].chunk, j = future[i].level;
+    if (cc < 0 || j < 0 || j > p->K) return fail(SC_EINVAL, "bad future node (%d,%d)", cc, j);
+    for (int32_t r = 1; r <= p->W && r <= cc; ++r) {
+      if (p->r_mask && !p->r_mask[j * p->W + (r - 1)]) continue;
+      needed.insert(StateKey(cc - r, read_level(p, j, r)));
+    }
+  }
+  std::vector<StateKey> drop;
+  for (const auto& kv : c->states)
+    if (!needed.count(kv.first)) drop.push_back(kv.first);
+  for (const auto& k : drop) {
+    int rc = sc_cache_release(c, sc_node{k.first, k.second});
+    if (rc != SC_OK) return rc;
+  }
+  return (int)drop.size();
+}
+
+extern "C" int sc_stack_forward(const sc_block_weights* layers, int32_t n_layers, sc_cache* cache,
+                                const sc_plan* plan, void* x, const sc_rope* rope, void* ws,
+                                size_t ws_bytes, sc_stream stream) {
+  if (!layers || n_layers < 1) return fail(SC_EINVAL, "need at least one layer");
+  if (!cache || n_layers > cache->d.n_layers)
+    return fail(SC_EINVAL, "%d layers but the cache holds %d", n_layers, cache ? cache->d.n_layers : 0);
+  for (int32_t l = 0; l < n_layers; ++l) {
+    int rc = sc_block_forward(&layers[l], cache, l, plan, x, rope, ws, ws_bytes, stream);
+    if (rc != SC_OK) return rc;
+  }
+  return SC_OK;
+}

@@ -1,0 +1,95 @@
+"""Round driver of the streaming schedule (Sec. 3.3), on top of the C ABI.
+
+Each chunk's current latent state lives in ``xs[c]`` ([tokens, hidden]
+bf16), initialised with the chunk's starting noise x^K.  A forward gathers the
+states of its nodes into a staging buffer (node order), runs the block stack
+(``sc_stack_forward``), and the sampler writes x^{j-1} back into ``xs[c]``
+(``sc_sampler_step``); the refresh node (c, 0) only leaves its K/V in the cache.
+After every round the states no later node reads are released
+(``sc_cache_release_unread``).  Modes:
+
+  packed      Eq. 7 rounds (plus the refresh node), one forward per round
+  sequential  the same rounds, one forward per node, oldest chunk first
+  serial      Eq. 2 order, one forward per node, chunk by chunk
+
+Every computation runs in the library; this module sequences calls and moves
+device buffers.
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Sequence, Tuple
+
+from . import binding as sc
+
+
+class StackPipeline:
+    def __init__(self, *, layers: Sequence["sc.BlockWeights"], cache: "sc.Cache", rope: "sc.Rope",
+                 xs, noise, policy: str, K: int, W: int, B: int, t_sched: Sequence[float],
+                 refresh: bool = True, stream=None):
+        import torch
+        self.torch = torch
+        self.layers, self.cache, self.rope = list(layers), cache, rope
+        self.xs, self.noise = xs, noise            # [B, n, hidden], [B, K + 2, n, hidden]
+        self.policy, self.K, self.W, self.B = policy, K, W, B
+        self.t_sched, self.refresh, self.stream = tuple(t_sched), refresh, stream
+        self.n_tok, self.hidden = xs.shape[1], xs.shape[2]
+        max_pack = K + 1
+        self.stage = torch.empty((max_pack * self.n_tok, self.hidden), dtype=xs.dtype, device=xs.device)
+        self.ws_bytes = sc.sc_block_workspace_bytes(self.layers[0], max_pack * self.n_tok)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=xs.device)
+
+    # ----------------------------------------------------------- schedules
+    def rounds(self) -> List[List[Tuple[int, int]]]:
+        n = sc.sc_pipeline_rounds(self.K, self.B, self.refresh)
+        return [sc.sc_pipeline_round_nodes(self.K, self.B, self.refresh, r) for r in range(n)]
+
+    def serial_nodes(self) -> List[Tuple[int, int]]:
+        lo = 0 if self.refresh else 1
+        return [(c, j) for c in range(self.B) for j in range(self.K, lo - 1, -1)]
+
+    # ------------------------------------------------------------ forwards
+    def forward(self, nodes: Sequence[Tuple[int, int]]) -> None:
+        """One packed forward of ``nodes`` through every layer, then the sampler."""
+        n = self.n_tok
+        sel = sc.sc_selection_build(self.policy, self.K, self.W, nodes)
+        plan = sc.sc_plan_build(sel, self.cache)
+        for i, (c, _) in enumerate(nodes):
+            self.stage[i * n:(i + 1) * n].copy_(self.xs[c])
+        x = self.stage[:len(nodes) * n]
+        sc.sc_stack_forward(self.layers, self.cache, plan, x, self.rope, self.ws, self.ws_bytes,
+                            self.stream)
+        for i, (c, j) in enumerate(nodes):
+            if j >= 1:
+                sc.sc_sampler_step([(c, j)], self.t_sched, self.K, self.xs[c],
+                                   self.stage[i * n:(i + 1) * n], self.noise[c, j],
+                                   n * self.hidden, self.stream)
+
+    def run(self, mode: str = "packed", time_rounds: bool = False) -> List[float]:
+        """Run the whole schedule; returns per-round (or per-node for serial)
+        milliseconds when ``time_rounds``."""
+        torch = self.torch
+        times = []
+        if mode == "serial":
+            units = [[node] for node in self.serial_nodes()]
+            groups = [[u] for u in units]
+        else:
+            units = self.rounds()
+            groups = [[u] if mode == "packed" else [[node] for node in u] for u in units]
+        flat = [node for u in units for node in u]
+        done = 0
+        for g, group in enumerate(groups):
+            if time_rounds:
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+            for nodes in group:
+                self.forward(nodes)
+                done += len(nodes)
+            sc.sc_cache_release_unread(self.cache, self.policy, self.K, self.W, flat[done:])
+            if time_rounds:
+                e1.record()
+                times.append((e0, e1))
+        if time_rounds:
+            torch.cuda.synchronize()
+            return [a.elapsed_time(b) for a, b in times]
+        return []

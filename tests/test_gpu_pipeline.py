@@ -1,0 +1,110 @@
+"""GPU round driver: the pipelined schedule end to end.
+
+* Small shapes, 2-layer stack, 6 chunks, K = 4, progressive history with the
+  refresh node: every chunk's clean output x^0 against the oracle's
+  ``run_stack`` (same seeded noise and weights).  Gate: the block gate with
+  its limits scaled by the number of blocks a chunk's output passes through
+  in one forward (errors of earlier forwards are damped by the sampler, which
+  keeps at most 3/8 of the prediction at each re-noising).
+* Packed == sequential == serial, bitwise (Sec. 3.3: pipelining changes the
+  number of sequential rounds, not the updates; serial execution admits
+  progressive history when states are retained).  Per-row work does not
+  depend on how nodes are grouped, so the target is exact equality.
+"""
+import numpy as np
+import pytest
+
+import paper_2609_22283_amd as sc
+from oracle.block import BlockShape
+from oracle.pipeline import pipeline_rounds, run_stack
+from oracle.policy import policy
+from paper_2609_22283_amd.pipeline import StackPipeline
+from synth import TAG_NOISE, TAG_W_DOWN, TAG_W_O, TAG_W_QKV, TAG_W_UP, normal, normal_parallel
+from synth.configs import SMALL, WAN
+
+from gpu_cases import from_device, to_device, torch_mod
+
+pytestmark = pytest.mark.gpu
+
+T_SCHED = (0.0, 5.0 / 8.0, 5.0 / 6.0, 15.0 / 16.0, 1.0)
+
+
+def _setup(geo, L, B, W, kind, seed, n_slots):
+    torch = torch_mod()
+    n, D, M = geo.tokens_per_chunk, geo.hidden, geo.mlp
+    big = n * D > 1 << 20
+    gen = normal_parallel if big else normal
+    weights_dev, weights_np, keep = [], [], []
+    for l in range(L):
+        w = {"w_qkv": gen((3 * D, D), (seed, TAG_W_QKV, l), 0.02),
+             "w_o": gen((D, D), (seed, TAG_W_O, l), 0.02),
+             "w_up": gen((M, D), (seed, TAG_W_UP, l), 0.02),
+             "w_down": gen((D, M), (seed, TAG_W_DOWN, l), 0.02)}
+        dev, exact = {}, {}
+        for k, v in w.items():
+            dev[k], exact[k] = to_device(v, sc.SC_DTYPE_BF16)
+        keep.append(dev)
+        weights_np.append(exact)
+        weights_dev.append(sc.BlockWeights(D, geo.heads, geo.head_dim, M, dev["w_qkv"], dev["w_o"],
+                                           dev["w_up"], dev["w_down"]))
+    K = geo.K
+    noise_np = np.stack([np.stack([gen((n, D), (seed, TAG_NOISE, c, j)) for j in range(K + 2)])
+                         for c in range(B)])
+    noise_dev, noise_exact = to_device(noise_np, sc.SC_DTYPE_BF16)
+    noise_dev = noise_dev.view(B, K + 2, n, D)
+    rt = torch.empty(sc.sc_rope_table_bytes(geo.grid_h, geo.grid_w, geo.rope_dims, 3 * B + 3),
+                     dtype=torch.uint8, device="cuda")
+    rope = sc.sc_rope_table_build(rt, geo.grid_h, geo.grid_w, geo.rope_dims, 3 * B + 3, geo.theta)
+
+    def make(mode_kind=kind):
+        nbytes = sc.sc_cache_pool_bytes(L, geo.heads, geo.head_dim, geo.tokens_per_page,
+                                        geo.frames_per_chunk, n_slots)
+        pool = torch.full((nbytes,), 0xFF, dtype=torch.uint8, device="cuda")
+        cache = sc.sc_cache_create(pool, L, geo.heads, geo.head_dim, geo.tokens_per_page,
+                                   geo.frames_per_chunk, n_slots)
+        xs = noise_dev[:, K + 1].clone()
+        return StackPipeline(layers=weights_dev, cache=cache, rope=rope, xs=xs, noise=noise_dev,
+                             policy=mode_kind, K=K, W=W, B=B, t_sched=T_SCHED, refresh=True)
+    return make, weights_np, noise_exact.reshape(B, K + 2, n, D), keep
+
+
+def test_small_pipeline_matches_oracle_and_schedules_agree():
+    geo, L, B, W = SMALL, 2, 6, 2
+    make, w_np, noise_np, keep = _setup(geo, L, B, W, "prog", seed=21, n_slots=60)
+    torch = torch_mod()
+    runs = {}
+    for mode in ("packed", "sequential", "serial"):
+        p = make()
+        p.run(mode)
+        torch.cuda.synchronize()
+        runs[mode] = from_device(p.xs)
+        assert p.cache.free_slot_count() == 60          # everything released at the end
+    assert np.array_equal(runs["packed"], runs["sequential"])
+    assert np.array_equal(runs["packed"], runs["serial"])
+    shp = BlockShape(geo.hidden, geo.heads, geo.head_dim, geo.mlp, geo.frames_per_chunk,
+                     geo.grid_h, geo.grid_w, geo.rope_dims, geo.theta)
+    outs, _, _ = run_stack(pipeline_rounds(B, geo.K, True), policy("prog", geo.K, W), L,
+                           lambda l: w_np[l], lambda c, j: noise_np[c, j], shp, t_sched=T_SCHED)
+    got = runs["packed"]
+    for c in range(B):
+        want = outs[(c, 1)]                              # x^0 = prediction at t_0 = 0
+        d = np.abs(got[c] - want)
+        lim = 2e-2 * L * np.maximum(1.0, np.abs(want))
+        assert np.all(np.isfinite(got[c]))
+        assert float((d / lim).max()) <= 1.0, (c, float((d / lim).max()))
+        assert d.mean() <= 4e-3 * L * max(1.0, float(np.abs(want).mean())), (c, d.mean())
+
+
+def test_wan_two_layer_pipeline_schedules_agree():
+    """Wan block shapes, 2 layers, 8 chunks: packed == sequential bitwise."""
+    geo, L, B, W = WAN, 2, 8, 6
+    make, _, _, keep = _setup(geo, L, B, W, "prog", seed=22, n_slots=(W + 2 * geo.K + 4) * 3)
+    torch = torch_mod()
+    a = make()
+    a.run("packed")
+    b = make()
+    b.run("sequential")
+    torch.cuda.synchronize()
+    xa, xb = from_device(a.xs), from_device(b.xs)
+    assert np.all(np.isfinite(xa))
+    assert np.array_equal(xa, xb)
