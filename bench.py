@@ -219,12 +219,110 @@ def cpu_baseline(wl, seed=0, row_stride=16):
                        f"x{n / len(rows):.2f}; estimated {est:.1f} s per step")}
 
 
+def stack_weights(n_layers, seed=0):
+    """bf16 device weights of an n-layer Wan-shaped stack (N(0, 0.02))."""
+    import concurrent.futures as cf
+
+    import numpy as np
+    import torch
+
+    import paper_2609_22283_amd as sc
+    from synth import TAG_W_DOWN, TAG_W_O, TAG_W_QKV, TAG_W_UP, bf16_bits, normal
+    from synth.configs import WAN as g
+
+    D, M = g.hidden, g.mlp
+    shapes = [("w_qkv", (3 * D, D), TAG_W_QKV), ("w_o", (D, D), TAG_W_O),
+              ("w_up", (M, D), TAG_W_UP), ("w_down", (D, M), TAG_W_DOWN)]
+    jobs = [(l, name, shp, tag) for l in range(n_layers) for name, shp, tag in shapes]
+
+    def make(job):
+        l, name, shp, tag = job
+        return job, bf16_bits(normal(shp, (seed, tag, l), 0.02))
+
+    dev = {}
+    with cf.ThreadPoolExecutor(min(16, len(os.sched_getaffinity(0)))) as ex:
+        for (l, name, _, _), bits in ex.map(make, jobs):
+            dev[(l, name)] = torch.from_numpy(bits.view(np.int16)).cuda().view(torch.bfloat16)
+    layers = [sc.BlockWeights(D, g.heads, g.head_dim, M, dev[(l, "w_qkv")], dev[(l, "w_o")],
+                              dev[(l, "w_up")], dev[(l, "w_down")]) for l in range(n_layers)]
+    return layers, dev
+
+
+def bench_stack(args):
+    """cfg5: the 30-block stack run as a pipeline over 16 chunks (K = 4, W = 6).
+
+    Steady-state rounds are those with a full pack (4 denoising nodes + the
+    refresh node) whose oldest node already has a full 6-chunk window; each
+    produces one clean chunk (3 latent frames).  Modes: packed (one forward
+    per round), sequential (the same nodes one forward each), and the clean
+    serial baseline of the paper's latency table (clean history, chunk by
+    chunk, 5 forwards per chunk)."""
+    import numpy as np
+    import torch
+
+    import paper_2609_22283_amd as sc
+    from paper_2609_22283_amd.pipeline import StackPipeline
+    from synth import TAG_NOISE, bf16_bits, normal
+    from synth.configs import WAN as g
+
+    L, B, K, W = args.layers, 16, g.K, g.W
+    n, D = g.tokens_per_chunk, g.hidden
+    t0 = time.perf_counter()
+    layers, keep = stack_weights(L)
+    noise = torch.empty((B, K + 2, n, D), dtype=torch.bfloat16, device="cuda")
+    import concurrent.futures as cf
+
+    def draw(cj):
+        return cj, bf16_bits(normal((n, D), (0, TAG_NOISE) + cj))
+    with cf.ThreadPoolExecutor(min(16, len(os.sched_getaffinity(0)))) as ex:
+        for (c, j), bits in ex.map(draw, [(c, j) for c in range(B) for j in range(K + 2)]):
+            noise[c, j].copy_(torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16))
+    rt = torch.empty(sc.sc_rope_table_bytes(g.grid_h, g.grid_w, g.rope_dims, 3 * B + 3),
+                     dtype=torch.uint8, device="cuda")
+    rope = sc.sc_rope_table_build(rt, g.grid_h, g.grid_w, g.rope_dims, 3 * B + 3, g.theta)
+    n_slots = (W + 2 * K + 4) * g.frames_per_chunk
+    nbytes = sc.sc_cache_pool_bytes(L, g.heads, g.head_dim, g.tokens_per_page, g.frames_per_chunk,
+                                    n_slots)
+    pool = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    log(f"[bench] cfg5 setup {time.perf_counter() - t0:.1f} s: {L} layers, pool {nbytes / 2**30:.1f} GiB")
+
+    def pipeline(policy):
+        cache = sc.sc_cache_create(pool, L, g.heads, g.head_dim, g.tokens_per_page,
+                                   g.frames_per_chunk, n_slots)
+        xs = noise[:, K + 1].clone()
+        return StackPipeline(layers=layers, cache=cache, rope=rope, xs=xs, noise=noise,
+                             policy=policy, K=K, W=W, B=B, t_sched=(0.0, 5 / 8, 5 / 6, 15 / 16, 1.0),
+                             refresh=True)
+
+    steady = [r for r in range(K + B) if r - K >= W and r < B]      # full pack, full window
+    res = {}
+    for mode, policy in (("packed", "prog"), ("sequential", "prog")):
+        p = pipeline(policy)
+        ms = p.run(mode, time_rounds=True,
+                   kernel_timer_rounds=(steady[0], steady[-1]) if mode == "packed" else None)
+        if mode == "packed":
+            n_attn, attn_tot = p.kernel_times["attention"]
+            res["attn_ms_per_launch"] = attn_tot / max(1, n_attn)
+            res["attn_launches"] = n_attn
+        res[mode] = float(np.median([ms[r] for r in steady]))
+        log(f"[bench] cfg5 {mode}: median steady round {res[mode]:.2f} ms "
+            f"(rounds {steady[0]}..{steady[-1]})")
+    p = pipeline("clean")
+    ms = p.run("serial", time_rounds=True)                          # one entry per node
+    per_chunk = [sum(ms[c * (K + 1):(c + 1) * (K + 1)]) for c in range(B)]
+    res["clean_serial"] = float(np.median([per_chunk[c] for c in range(W, B)]))
+    log(f"[bench] cfg5 clean serial: median steady chunk {res['clean_serial']:.2f} ms")
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="cfg4", choices=["cfg4", "cfg4R", "cfg3", "cfg2"])
+    ap.add_argument("--workload", default="cfg4", choices=["cfg4", "cfg4R", "cfg3", "cfg2", "cfg5"])
+    ap.add_argument("--layers", type=int, default=30, help="cfg5: blocks in the stack")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sequential", action="store_true")
     args = ap.parse_args()
@@ -236,6 +334,37 @@ def main():
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.workload == "cfg5":
+        from synth.configs import WAN as g
+        r = bench_stack(args)
+        wl5 = workload("cfg4R")                    # the steady round's pack and windows
+        a_flops = attention_flops(wl5, g)
+        attn_tflops = a_flops / (r["attn_ms_per_launch"] * 1e-3) / 1e12
+        value = 3.0 / (r["packed"] * 1e-3) * args.layers
+        result = {
+            "metric": METRIC, "value": round(value, 3), "unit": "latent frames/s per DiT block",
+            "n_gpus": 1, "steps": 20, "warmup": 0, "ms_per_step": round(r["packed"], 3),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic (seeded noise, N(0,0.02) weights)",
+            "config": {"workload": f"cfg5: {args.layers}-block Wan-shaped stack, progressive "
+                                   "pipeline, 16 chunks x 3 latent frames, K=4, W=6, refresh",
+                       "layers": args.layers, "parallelism": "single GPU"},
+            "stack_latent_frames_per_s": round(3.0 / (r["packed"] * 1e-3), 3),
+            "sequential_ms_per_round": round(r["sequential"], 3),
+            "clean_serial_ms_per_chunk": round(r["clean_serial"], 3),
+            "packed_vs_sequential": round(r["sequential"] / r["packed"], 3),
+            "prog_pipeline_vs_clean_serial": round(r["clean_serial"] / r["packed"], 3),
+            "attention_tflops": round(attn_tflops, 1),
+            "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 1), "peak": PEAK_BF16_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                         "traffic": None, "kernel": "attn_bf16_kernel"},
+        }
+        if not args.no_cpu_baseline:
+            cb = cpu_baseline(wl5)
+            cb["sample"] += "; one block of the 5-node steady round (per-block rate)"
+            result["cpu_baseline"] = cb
+        print(json.dumps(result), flush=True)
+        return
     wl = workload(args.workload)
     log(f"[bench] workload {wl.name}: pack {wl.pack}, resident {len(wl.resident)} states")
     setup = Setup(wl)

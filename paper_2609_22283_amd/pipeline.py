@@ -64,11 +64,16 @@ class StackPipeline:
                                    self.stage[i * n:(i + 1) * n], self.noise[c, j],
                                    n * self.hidden, self.stream)
 
-    def run(self, mode: str = "packed", time_rounds: bool = False) -> List[float]:
+    def run(self, mode: str = "packed", time_rounds: bool = False,
+            kernel_timer_rounds: Tuple[int, int] = None) -> List[float]:
         """Run the whole schedule; returns per-round (or per-node for serial)
-        milliseconds when ``time_rounds``."""
+        milliseconds when ``time_rounds``.  With ``kernel_timer_rounds =
+        (first, last)`` the library's kernel timer records the launches of
+        those rounds; ``self.kernel_times`` then maps kernel kinds to
+        (launches, total ms)."""
         torch = self.torch
         times = []
+        self.kernel_times = {}
         if mode == "serial":
             units = [[node] for node in self.serial_nodes()]
             groups = [[u] for u in units]
@@ -78,6 +83,8 @@ class StackPipeline:
         flat = [node for u in units for node in u]
         done = 0
         for g, group in enumerate(groups):
+            if kernel_timer_rounds and g == kernel_timer_rounds[0]:
+                sc.sc_timer_enable(True)
             if time_rounds:
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
@@ -89,6 +96,10 @@ class StackPipeline:
             if time_rounds:
                 e1.record()
                 times.append((e0, e1))
+            if kernel_timer_rounds and g == kernel_timer_rounds[1]:
+                for kind in ("attention", "gemm_qkv", "gemm_out", "gemm_up", "gemm_down"):
+                    self.kernel_times[kind] = sc.sc_timer_read(kind)
+                sc.sc_timer_enable(False)
         if time_rounds:
             torch.cuda.synchronize()
             return [a.elapsed_time(b) for a, b in times]
