@@ -20,12 +20,21 @@ constexpr int GWM = 128, GWN = 64;
 constexpr int G_THREADS = 512;
 constexpr int G_TILE_BYTES = GBM * GBK * 2;  // 32 KB per operand per stage
 
+// GELU_tanh(x) = 0.5 x (1 + tanh(u)) = x * sigmoid(2 u), u = sqrt(2/pi) (x + 0.044715 x^3),
+// evaluated as x / (1 + 2^(-2 u log2 e)).
 __device__ __forceinline__ float gelu_tanh(float x) {
-  const float u = 0.7978845608028654f * fmaf(0.044715f * x, x * x, x);
-  // tanh(u) = 1 - 2 / (exp(2u) + 1), saturating correctly at +-inf
-  const float e = __expf(2.f * u);
-  const float th = 1.f - 2.f / (e + 1.f);
-  return 0.5f * x * (1.f + th);
+  constexpr float k = 2.0f * 0.7978845608028654f * 1.4426950408889634f;  // 2 sqrt(2/pi) log2(e)
+  const float q = x * fmaf(x * x, -k * 0.044715f, -k);
+  const float e = __builtin_amdgcn_exp2f(q);
+  return x * __builtin_amdgcn_rcpf(1.0f + e);
+}
+
+// Direct global -> LDS copy of 16 bytes per lane (lane i lands at LDS base + 16 i).
+__device__ __forceinline__ void gdma16(const char* src, char* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src),
+                                   reinterpret_cast<__attribute__((address_space(3))) void*>(
+                                       reinterpret_cast<uintptr_t>(lds_wave_base)),
+                                   16, 0, 0);
 }
 
 template <int EPI>
@@ -33,7 +42,9 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
                                                                  const uint16_t* __restrict__ X,
                                                                  int32_t F, int32_t T, int32_t Kd,
                                                                  GemmEpilogue ep) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * 2 * G_TILE_BYTES];
+  // stage s: W tile at s * 64 KB, X tile at s * 64 KB + 32 KB; rows of 64 k
+  // (128 B) with 16-byte column c stored at c ^ ((row >> 1) & 7)
+  __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * G_TILE_BYTES];
   const int32_t n_tf = F / GBM, n_tt = (T + GBN - 1) / GBN;
   const uint32_t tile = xcd_remap(blockIdx.x, (uint32_t)(n_tf * n_tt));
   const int32_t tf = tile % n_tf, tt = tile / n_tf;
@@ -43,36 +54,44 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   const int32_t hl = lane >> 5, r32 = lane & 31;
   const int32_t wf = (wave & 1) * GWM, wt = (wave >> 1) * GWN;
 
-  // loader: 4 chunks of 16 B for W and for X per thread per stage
-  u32x4 wpre[4], xpre[4];
-  const uint16_t* wsrc[4];
-  const uint16_t* xsrc[4];
-  int32_t lds_off[4];
+  // copies: each wave moves rows [32 wave, 32 wave + 32) of both operand
+  // tiles, 8 rows (1 KB) per instruction; lane (row, p) fetches column
+  // p ^ ((row >> 1) & 7).  Byte offsets are fixed per lane; the k offset is
+  // folded into the (wave-uniform) base pointer.
+  uint32_t woff[4], xoff[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int32_t c = tid + G_THREADS * i;  // 0..2047
-    const int32_t row = c >> 3, col = c & 7;
-    wsrc[i] = W + (size_t)(f0 + row) * Kd + col * 8;
+  for (int j = 0; j < 4; ++j) {
+    const int32_t row = 32 * wave + 8 * j + (lane >> 3);
+    const int32_t col = (lane & 7) ^ ((row >> 1) & 7);
+    woff[j] = ((uint32_t)(f0 + row) * Kd + col * 8) * 2;
     const int32_t trow = min(t0 + row, T - 1);
-    xsrc[i] = X + (size_t)trow * Kd + col * 8;
-    lds_off[i] = row * 128 + ((col ^ ((row >> 1) & 7)) << 4);
+    xoff[j] = ((uint32_t)trow * Kd + col * 8) * 2;
   }
-  auto issue = [&](int32_t k0) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      wpre[i] = *reinterpret_cast<const u32x4*>(wsrc[i] + k0);
-      xpre[i] = *reinterpret_cast<const u32x4*>(xsrc[i] + k0);
-    }
-  };
-  auto stash = [&](int buf) {
+  const char* wbase = reinterpret_cast<const char*>(W);
+  const char* xbase = reinterpret_cast<const char*>(X);
+  auto issue = [&](int32_t k0, int buf) {
     char* a = smem + buf * 2 * G_TILE_BYTES;
     char* b = a + G_TILE_BYTES;
+    const char* wk = wbase + (size_t)k0 * 2;
+    const char* xk = xbase + (size_t)k0 * 2;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      *reinterpret_cast<u32x4*>(a + lds_off[i]) = wpre[i];
-      *reinterpret_cast<u32x4*>(b + lds_off[i]) = xpre[i];
+    for (int j = 0; j < 4; ++j) {
+      gdma16(wk + woff[j], a + (32 * wave + 8 * j) * 128);
+      gdma16(xk + xoff[j], b + (32 * wave + 8 * j) * 128);
     }
   };
+  auto landed = [&]() {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  };
+
+  // LDS read offsets of this lane's fragments (16-byte column 2 s + hl)
+  uint32_t aoff[4], boff[2];
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) aoff[mb] = (uint32_t)(wf + 32 * mb + r32) * 128;
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) boff[nb] = (uint32_t)(wt + 32 * nb + r32) * 128;
+  const int32_t swz = (r32 >> 1) & 7;  // rows wf + 32 mb + r32 share (row >> 1) & 7
 
   f32x16 acc[4][2];
 #pragma unroll
@@ -80,57 +99,63 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = f32x16{};
 
+  auto frags = [&](const char* a, const char* b, int s, bf16x8 (&af)[4], bf16x8 (&bf)[2]) {
+    const uint32_t c = (uint32_t)(((2 * s + hl) ^ swz) << 4);
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) af[mb] = *reinterpret_cast<const bf16x8*>(a + aoff[mb] + c);
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) bf[nb] = *reinterpret_cast<const bf16x8*>(b + boff[nb] + c);
+  };
+
   const int32_t nk = Kd / GBK;
-  issue(0);
-  stash(0);
-  __syncthreads();
+  issue(0, 0);
+  landed();
   for (int32_t kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) issue((kt + 1) * GBK);
+    if (kt + 1 < nk) issue((kt + 1) * GBK, (kt + 1) & 1);
     const char* a = smem + (kt & 1) * 2 * G_TILE_BYTES;
     const char* b = a + G_TILE_BYTES;
+    bf16x8 af[2][4], bfr[2][2];
+    frags(a, b, 0, af[0], bfr[0]);
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      const int32_t col = 2 * s + hl;
-      bf16x8 af[4], bfr[2];
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb) {
-        const int32_t row = wf + 32 * mb + r32;
-        af[mb] = *reinterpret_cast<const bf16x8*>(a + row * 128 + ((col ^ ((row >> 1) & 7)) << 4));
-      }
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb) {
-        const int32_t row = wt + 32 * nb + r32;
-        bfr[nb] = *reinterpret_cast<const bf16x8*>(b + row * 128 + ((col ^ ((row >> 1) & 7)) << 4));
-      }
+      if (s + 1 < 4) frags(a, b, s + 1, af[(s + 1) & 1], bfr[(s + 1) & 1]);
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb)
-          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bfr[nb], acc[mb][nb], 0, 0, 0);
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s & 1][mb], bfr[s & 1][nb],
+                                                                acc[mb][nb], 0, 0, 0);
     }
-    if (kt + 1 < nk) stash((kt + 1) & 1);
-    __syncthreads();
+    landed();
   }
 
   // epilogue: lane holds D[f][t] for t = t0 + wt + 32 nb + r32 and
   // f = f0 + wf + 32 mb + 8 g + 4 hl + e (e = 0..3)
+  if constexpr (EPI == EPI_QKV) {
+    // a 256-feature tile lies in one of q, k, v (hidden is a multiple of 256)
+    // and each wave's 128 features in one head (head_dim 128)
+    const int32_t sec = f0 / ep.hidden;
+    const int32_t hf0 = f0 - sec * ep.hidden + wf;       // wave's first feature in its section
+    const int32_t head = hf0 / ep.head_dim;
+    const int32_t dbase = hf0 - head * ep.head_dim + 4 * hl;
 #pragma unroll
-  for (int nb = 0; nb < 2; ++nb) {
-    const int32_t t = t0 + wt + 32 * nb + r32;
-    if (t >= T) continue;
-    if constexpr (EPI == EPI_QKV) {
+    for (int nb = 0; nb < 2; ++nb) {
+      const int32_t t = t0 + wt + 32 * nb + r32;
+      if (t >= T) continue;
       const int32_t node = t / ep.nq, tok = t - node * ep.nq;
       const int32_t frame = tok / ep.tpp, n = tok - frame * ep.tpp;
       const int32_t pos_t = ep.node_chunk[node] * ep.ppc + frame;
       const int32_t pos_h = n / ep.grid_w, pos_w = n - pos_h * ep.grid_w;
       char* slot_base = ep.layer_base + (size_t)ep.node_slot[node * ep.ppc + frame] * ep.slot_bytes;
+      uint16_t* qrow = ep.q_out + (size_t)t * ep.hidden + hf0 + 4 * hl;
+      uint16_t* krow = reinterpret_cast<uint16_t*>(slot_base) + ((size_t)head * ep.tpp + n) * ep.head_dim;
+      uint16_t* vcol = reinterpret_cast<uint16_t*>(slot_base + ep.kv_half) +
+                       (size_t)head * ep.head_dim * ep.tpp + n;
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int32_t f = f0 + wf + 32 * mb + 8 * g + 4 * hl;
-          const int32_t sec = f / ep.hidden, hf = f - sec * ep.hidden;
-          const int32_t head = hf / ep.head_dim, d = hf - head * ep.head_dim;
+          const int32_t d = dbase + 32 * mb + 8 * g;
           float v0 = acc[mb][nb][4 * g + 0], v1 = acc[mb][nb][4 * g + 1];
           float v2 = acc[mb][nb][4 * g + 2], v3 = acc[mb][nb][4 * g + 3];
           if (sec < 2 && ep.rope_table) {
@@ -152,29 +177,32 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
           pk.x = pack_bf16x2(v0, v1);
           pk.y = pack_bf16x2(v2, v3);
           if (sec == 0) {
-            *reinterpret_cast<u32x2*>(ep.q_out + (size_t)t * ep.hidden + hf) = pk;
+            *reinterpret_cast<u32x2*>(qrow + 32 * mb + 8 * g) = pk;
           } else if (sec == 1) {
-            uint16_t* kd = reinterpret_cast<uint16_t*>(slot_base) + ((size_t)head * ep.tpp + n) * ep.head_dim + d;
-            *reinterpret_cast<u32x2*>(kd) = pk;
+            *reinterpret_cast<u32x2*>(krow + d) = pk;
           } else {
-            uint16_t* vd = reinterpret_cast<uint16_t*>(slot_base + ep.kv_half) +
-                           ((size_t)head * ep.head_dim + d) * ep.tpp + n;
+            uint16_t* vd = vcol + (size_t)d * ep.tpp;
             vd[0] = (uint16_t)(pk.x & 0xffff);
             vd[ep.tpp] = (uint16_t)(pk.x >> 16);
             vd[2 * ep.tpp] = (uint16_t)(pk.y & 0xffff);
             vd[3 * ep.tpp] = (uint16_t)(pk.y >> 16);
           }
         }
-    } else {
+    }
+  } else {
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const int32_t t = t0 + wt + 32 * nb + r32;
+      if (t >= T) continue;
+      uint16_t* orow = ep.out + (size_t)t * ep.ld_out + f0 + wf + 4 * hl;
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int32_t f = f0 + wf + 32 * mb + 8 * g + 4 * hl;
           float v[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] = acc[mb][nb][4 * g + e];
-          uint16_t* dst = ep.out + (size_t)t * ep.ld_out + f;
+          uint16_t* dst = orow + 32 * mb + 8 * g;
           if constexpr (EPI == EPI_RESIDUAL) {
             const u32x2 r = *reinterpret_cast<const u32x2*>(dst);
             v[0] += __uint_as_float(r.x << 16);
@@ -199,6 +227,10 @@ int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, i
   if (F % GBM || Kd % GBK || T <= 0)
     return fail(SC_EUNSUPPORTED, "gemm needs F %% %d == 0, K %% %d == 0 (F=%d K=%d T=%d)", GBM, GBK,
                 F, Kd, T);
+  if ((uint64_t)F * Kd * 2 > 0xffffffffull || (uint64_t)T * Kd * 2 > 0xffffffffull)
+    return fail(SC_EUNSUPPORTED, "gemm operands beyond 4 GB");
+  if (epi == EPI_QKV && (ep.hidden % GBM || ep.head_dim != GWM))
+    return fail(SC_EUNSUPPORTED, "QKV epilogue needs hidden %% %d == 0 and head_dim %d", GBM, GWM);
   const uint32_t tiles = (uint32_t)(F / GBM) * (uint32_t)((T + GBN - 1) / GBN);
   timer_begin(timer_kind, stream);
   switch (epi) {
