@@ -46,8 +46,14 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   // (128 B) with 16-byte column c stored at c ^ ((row >> 1) & 7)
   __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * G_TILE_BYTES];
   const int32_t n_tf = F / GBM, n_tt = (T + GBN - 1) / GBN;
-  const uint32_t tile = xcd_remap(blockIdx.x, (uint32_t)(n_tf * n_tt));
-  const int32_t tf = tile % n_tf, tt = tile / n_tf;
+  // Each XCD takes a contiguous run of logical tiles; the run is walked in
+  // groups of GT token tiles, feature tiles outermost within a group, so the
+  // ~32 tiles an XCD holds at once share 4-5 weight and 8 token panels in L2.
+  constexpr int32_t GT = 8;
+  const int32_t tile = (int32_t)xcd_remap(blockIdx.x, (uint32_t)(n_tf * n_tt));
+  const int32_t group = tile / (GT * n_tf), in_group = tile - group * GT * n_tf;
+  const int32_t gt = min(GT, n_tt - group * GT);
+  const int32_t tf = in_group / gt, tt = group * GT + in_group % gt;
   const int32_t f0 = tf * GBM, t0 = tt * GBN;
 
   const int32_t tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
