@@ -32,7 +32,7 @@
 extern "C" {
 #endif
 
-#define SC_ABI_VERSION 1
+#define SC_ABI_VERSION 2
 
 enum {
   SC_OK = 0,
@@ -180,10 +180,17 @@ void sc_plan_free(sc_plan* plan);
  * q, o: device [n_nodes * Nq, n_heads, head_dim] in the cache dtype, node i
  * at rows [i*Nq, (i+1)*Nq) with Nq = pages_per_chunk * tokens_per_page.
  * Every page must have been written at this layer by calls enqueued earlier
- * on the same stream.  Errors: SC_ESTALE, SC_EUNAVAILABLE (a page's state not
- * written at this layer), SC_EUNSUPPORTED, SC_EDEVICE. */
+ * on the same stream.  ws: device scratch, 16-byte aligned, of at least
+ * sc_attention_workspace_bytes(plan, cache) bytes (may be NULL when that is
+ * 0, as for fp32 caches); the bf16 kernel splits long key ranges across
+ * work-groups and merges their partial softmax sums there.  Its contents are
+ * undefined on return; calls sharing one workspace must be ordered on one
+ * stream.  Errors: SC_ESTALE, SC_EUNAVAILABLE (a page's state not written at
+ * this layer), SC_EINVAL (workspace too small or misaligned), SC_EUNSUPPORTED,
+ * SC_EDEVICE. */
+size_t sc_attention_workspace_bytes(const sc_plan* plan, const sc_cache* cache);
 int sc_attention(const sc_plan* plan, const sc_cache* cache, int32_t layer, const void* q,
-                 void* o, float scale, sc_stream stream);
+                 void* o, float scale, void* ws, size_t ws_bytes, sc_stream stream);
 
 /* ---- One DiT block over the pack ----------------------------------------
  * The network F_theta of Eq. 1 for the packed nodes, one block (bf16 only):

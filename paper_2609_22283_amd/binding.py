@@ -16,10 +16,10 @@ __all__ = [
     "ScError", "lib", "library_path", "SC_OK", "SC_EINVAL", "SC_EUNAVAILABLE", "SC_ECAPACITY",
     "SC_EEXIST", "SC_ENOTFOUND", "SC_ESTALE", "SC_EDEVICE", "SC_EUNSUPPORTED",
     "SC_POLICY_CLEAN", "SC_POLICY_SAME", "SC_POLICY_PROG", "SC_POLICY_TABLE",
-    "SC_DTYPE_BF16", "SC_DTYPE_F32", "POLICY_KINDS", "EXPORTED_SYMBOLS",
+    "SC_DTYPE_BF16", "SC_DTYPE_F32", "POLICY_KINDS", "EXPORTED_SYMBOLS", "ABI_VERSION",
     "sc_abi_version", "sc_selection_build", "sc_cache_pool_bytes", "sc_cache_create",
     "sc_rope_table_bytes", "sc_rope_table_build", "sc_plan_build", "sc_attention",
-    "sc_block_workspace_bytes", "sc_block_forward", "sc_sampler_step",
+    "sc_attention_workspace_bytes", "sc_block_workspace_bytes", "sc_block_forward", "sc_sampler_step",
     "sc_timer_enable", "sc_timer_read", "Selection", "Cache", "Plan", "Rope", "BlockWeights",
     "sc_pipeline_rounds", "sc_pipeline_round_nodes", "sc_cache_release_unread", "sc_stack_forward",
 ]
@@ -38,7 +38,8 @@ EXPORTED_SYMBOLS = [
     "sc_cache_slots", "sc_cache_free_slot_count", "sc_cache_release", "sc_cache_append",
     "sc_rope_table_bytes", "sc_rope_table_build",
     "sc_plan_build", "sc_plan_get", "sc_plan_free",
-    "sc_attention", "sc_block_workspace_bytes", "sc_block_forward", "sc_sampler_step",
+    "sc_attention_workspace_bytes", "sc_attention",
+    "sc_block_workspace_bytes", "sc_block_forward", "sc_sampler_step",
     "sc_timer_enable", "sc_timer_read",
     "sc_pipeline_rounds", "sc_pipeline_round_nodes", "sc_cache_release_unread", "sc_stack_forward",
 ]
@@ -121,7 +122,8 @@ _SIG = {
     "sc_plan_build": (C.c_int, [_P, _P, C.POINTER(_P)]),
     "sc_plan_get": (C.c_int, [_P, _I32P, _I32P] + [C.POINTER(_I32P)] * 4),
     "sc_plan_free": (None, [_P]),
-    "sc_attention": (C.c_int, [_P, _P, C.c_int32, _P, _P, C.c_float, _P]),
+    "sc_attention_workspace_bytes": (C.c_size_t, [_P, _P]),
+    "sc_attention": (C.c_int, [_P, _P, C.c_int32, _P, _P, C.c_float, _P, C.c_size_t, _P]),
     "sc_block_workspace_bytes": (C.c_size_t, [C.POINTER(sc_block_weights), C.c_int32]),
     "sc_block_forward": (C.c_int, [C.POINTER(sc_block_weights), _P, C.c_int32, _P, _P,
                                    C.POINTER(sc_rope), _P, C.c_size_t, _P]),
@@ -136,6 +138,11 @@ _SIG = {
     "sc_stack_forward": (C.c_int, [C.POINTER(sc_block_weights), C.c_int32, _P, _P, _P,
                                    C.POINTER(sc_rope), _P, C.c_size_t, _P]),
 }
+# ABI version this binding marshals for (SC_ABI_VERSION of the header)
+ABI_VERSION = 2
+if not hasattr(lib, "sc_abi_version") or lib.sc_abi_version() != ABI_VERSION:
+    raise ImportError(f"{library_path} does not implement ABI version {ABI_VERSION}; rebuild it "
+                      "(__graft_entry__.build())")
 for _name, (_res, _args) in _SIG.items():
     _f = getattr(lib, _name)
     _f.restype = _res
@@ -343,9 +350,14 @@ def sc_plan_build(sel: Selection, cache: Cache) -> Plan:
     return Plan(out.value, cache)
 
 
-def sc_attention(plan: Plan, cache: Cache, layer: int, q, o, scale: float, stream=None) -> None:
-    _check(lib.sc_attention(plan.handle, cache.handle, layer, _ptr(q), _ptr(o), scale,
-                            _stream(stream)))
+def sc_attention_workspace_bytes(plan: Plan, cache: Cache) -> int:
+    return lib.sc_attention_workspace_bytes(plan.handle, cache.handle)
+
+
+def sc_attention(plan: Plan, cache: Cache, layer: int, q, o, scale: float, ws=None,
+                 ws_bytes: int = 0, stream=None) -> None:
+    _check(lib.sc_attention(plan.handle, cache.handle, layer, _ptr(q), _ptr(o), scale, _ptr(ws),
+                            ws_bytes, _stream(stream)))
 
 
 # ---------------------------------------------------------------------- block

@@ -13,6 +13,9 @@
 // softmax in fp32.  The K rows feeding the S^T MFMA are permuted so that each
 // lane's probabilities are exactly the B operand of the PV MFMA, and V is
 // stored transposed in the cache so its A operand is one 16-byte LDS read.
+#include <algorithm>
+#include <climits>
+#include <cstring>
 #include <type_traits>
 
 #include "device.h"
@@ -35,6 +38,10 @@ struct AttnGeom {
   DivMagic tpp_div;
   float scale_log2;  // scale * log2(e): softmax evaluated with exp2
   float scale;
+  // schedule of the bf16 kernel: whole units, then tail units cut in pieces
+  int32_t whole_units, tail_units, tail_split;
+  float* part_o;          // [tail_units * tail_split][BQ][128] unnormalised partial outputs
+  float* part_ml;         // [tail_units * tail_split][2][BQ] partial max (log2 units) and sum
 };
 
 static DivMagic magic_div(uint32_t d) {
@@ -224,24 +231,71 @@ __device__ __forceinline__ void dma16(const char* src, char* lds_wave_base) {
                                    16, 0, 0);
 }
 
+// Schedule.  A unit is a (head, node, query tile) triple, numbered head-major
+// then node then query tile; a unit's key tiles are processed in order by one
+// work-group.  Units of one (head, node) are consecutive and every unit
+// starts at its node's first key tile, so the work-groups an XCD runs side
+// by side read the same K/V tiles at about the same time and share them in
+// its L2.  Equal units fill the 256 CUs in whole rounds but the last
+// U mod 256; those "tail" units are each cut into S pieces of their key
+// range, numbered piece-major (piece p of every tail unit before piece p+1),
+// so the last round is S times shorter.  Pieces leave unnormalised partials
+// that attn_combine_kernel merges in piece order.
+struct AttnItem {
+  int32_t head, node, qt;
+  int32_t ta, tb;   // key tiles [ta, tb) of the unit
+  int32_t ntiles;   // key tiles of the whole unit
+  int32_t slot;     // partial slot, or -1 for a whole unit
+};
+
+__device__ __forceinline__ int32_t node_tiles(const AttnPlan& plan, const AttnGeom& g, int32_t node) {
+  return ((plan.page_off[node + 1] - plan.page_off[node]) * g.tpp + BK - 1) / BK;
+}
+
+__device__ __forceinline__ AttnItem decode_item(const AttnPlan& plan, const AttnGeom& g, uint32_t b) {
+  AttnItem it;
+  int32_t unit;
+  if (b < (uint32_t)g.whole_units) {
+    unit = (int32_t)xcd_remap(b, (uint32_t)g.whole_units);
+    it.slot = -1;
+  } else {
+    const int32_t j = (int32_t)xcd_remap(b - (uint32_t)g.whole_units,
+                                         (uint32_t)(g.tail_units * g.tail_split));
+    unit = g.whole_units + j % g.tail_units;
+    it.slot = j;
+  }
+  it.qt = unit % g.n_qtiles;
+  it.node = (unit / g.n_qtiles) % g.n_nodes;
+  it.head = unit / (g.n_qtiles * g.n_nodes);
+  it.ntiles = node_tiles(plan, g, it.node);
+  if (it.slot < 0) {
+    it.ta = 0;
+    it.tb = it.ntiles;
+  } else {
+    const int32_t piece = it.slot / g.tail_units;
+    it.ta = piece * it.ntiles / g.tail_split;
+    it.tb = (piece + 1) * it.ntiles / g.tail_split;
+  }
+  return it;
+}
+
 __global__ __launch_bounds__(64 * NWAVES, 1) void attn_bf16_kernel(const uint16_t* __restrict__ q,
-                                                           uint16_t* __restrict__ o, AttnGeom g,
-                                                           AttnPlan plan) {
+                                                                   uint16_t* __restrict__ o,
+                                                                   AttnGeom g, AttnPlan plan) {
   // K buffers 0, 1 then V^T buffers 0, 1 (16 KB each)
   __shared__ __attribute__((aligned(1024))) char smem[SMEM_BYTES];
-  const uint32_t nwg = (uint32_t)g.n_nodes * g.n_heads * g.n_qtiles;
-  const uint32_t w = xcd_remap(blockIdx.x, nwg);
-  const int32_t qt = w % g.n_qtiles;
-  const int32_t node = (w / g.n_qtiles) % g.n_nodes;
-  const int32_t head = w / (g.n_qtiles * g.n_nodes);
+  const AttnItem it = decode_item(plan, g, blockIdx.x);
+  if (it.ta == it.tb) return;  // empty piece of a unit shorter than the split
+  const int32_t node = it.node, head = it.head, qt = it.qt;
+  const int32_t ta = it.ta, ntiles = it.tb;  // this item's key tiles: [ta, ntiles)
 
   const int32_t tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int32_t hl = lane >> 5, r32 = lane & 31;
+
   const int32_t p0 = plan.page_off[node];
   const int32_t npages = plan.page_off[node + 1] - p0;
   const int32_t nk = npages * g.tpp;
-  const int32_t ntiles = (nk + BK - 1) / BK;
-  const bool ragged = (nk % BK) != 0;
+  const bool ragged = it.tb == it.ntiles && (nk % BK) != 0;
 
   // Q^T operand: lane holds Q[row][16 si + 8 hl .. +7] for si = 0..7.
   const int32_t qrow = qt * BQ + wave * 32 + r32;
@@ -273,15 +327,15 @@ __global__ __launch_bounds__(64 * NWAVES, 1) void attn_bf16_kernel(const uint16_
       L.voff[cm] = r32 * 128 + (((2 * cm + hl) ^ ((r32 >> 1) & 7)) << 4);
   }
 
+  const char* lbase = g.layer_base;
+  const uint32_t khead = (uint32_t)head * g.tpp * HDB * 2;
+  const uint32_t vhead = (uint32_t)g.kv_half + (uint32_t)head * HDB * g.tpp * 2;
   // Tile copies.  A 64-key tile spans at most two pages (pages hold >= 64
   // tokens), so the page of a key is chosen against one wave-uniform
   // boundary.  Offsets are 32-bit, relative to the layer's slots (the host
   // checks a layer fits in 4 GB); the per-page parts are wave-uniform.  Per
   // wave: 2 copies of 4 K rows (1 KB each) and 2 copies of 8 V^T rows.  Lane
   // (row, physical column p) fetches logical column p ^ swizzle(row).
-  const char* lbase = g.layer_base;
-  const uint32_t khead = (uint32_t)head * g.tpp * HDB * 2;
-  const uint32_t vhead = (uint32_t)g.kv_half + (uint32_t)head * HDB * g.tpp * 2;
   constexpr int KCP = 64 / (4 * NWAVES), VCP = 128 / (8 * NWAVES);  // copies per wave
   const int32_t krow0 = 4 * KCP * wave + (lane >> 4), kp = lane & 15;
   const int32_t vrow0 = 8 * VCP * wave + (lane >> 3), vp = lane & 7;
@@ -353,29 +407,30 @@ __global__ __launch_bounds__(64 * NWAVES, 1) void attn_bf16_kernel(const uint16_
 #pragma unroll
   for (int db = 0; db < 4; ++db) oacc[db] = f32x16{};
   float m_run = 0.f, l_run = 0.f;
-  // prologue: K(0), V(0), K(1) in flight; S(0) = K(0) Q^T; m = its exact max
-  copy_k(0, 0);
-  copy_v(0, 0);
-  if (ntiles > 1) copy_k(1, 1);
+  // prologue: K(ta), V(ta), K(ta+1) in flight; S(ta) = K(ta) Q^T; m = its exact max
+  copy_k(ta, 0);
+  copy_v(ta, 0);
+  if (ta + 1 < ntiles) copy_k(ta + 1, 1);
   landed();
   f32x16 s[2];
   qk_tile(smem, L, qreg, s, 0.f);
-  if (ntiles == 1 && ragged) {
+  if (ta + 1 == ntiles && ragged) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i)
-        if (32 * kb + 16 * (i >> 3) + 8 * hl + (i & 7) >= nk) s[kb][i] = -INFINITY;
+        if (ta * BK + 32 * kb + 16 * (i >> 3) + 8 * hl + (i & 7) >= nk) s[kb][i] = -INFINITY;
   }
   m_run = tile_max(s);
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int i = 0; i < 16; ++i) s[kb][i] -= m_run;
-  __syncthreads();  // every wave has read K(0) before K(2) is copied over it
+  __syncthreads();  // every wave has read K(ta) before K(ta+2) is copied over it
 
-  // iteration t: copy K(t+2) over K(t) and V(t+1) over V(t-1), then step t
-  int32_t t = 0;
+  // iteration t (buffer parity counted from ta): copy K(t+2) over K(t) and
+  // V(t+1) over V(t-1), then step t
+  int32_t t = ta;
   for (; t + 2 < ntiles; t += 2) {
     copy_k(t + 2, 0);
     copy_v(t + 1, 1);
@@ -386,7 +441,7 @@ __global__ __launch_bounds__(64 * NWAVES, 1) void attn_bf16_kernel(const uint16_
     attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m_run, l_run, (t + 1) * BK, nk, hl);
     landed();
   }
-  if (t + 1 < ntiles) {  // two tiles left, t even
+  if (t + 1 < ntiles) {  // two tiles left, parity 0
     copy_v(t + 1, 1);
     attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
     landed();
@@ -395,7 +450,7 @@ __global__ __launch_bounds__(64 * NWAVES, 1) void attn_bf16_kernel(const uint16_
       attn_step<0, 1, false, true>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
     else
       attn_step<0, 1, false, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
-  } else {               // one tile left, t even (masking twice is harmless)
+  } else {               // one tile left, parity 0 (masking twice is harmless)
     if (ragged)
       attn_step<1, 0, false, true>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
     else
@@ -403,24 +458,137 @@ __global__ __launch_bounds__(64 * NWAVES, 1) void attn_bf16_kernel(const uint16_
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  const float inv = 1.f / l_tot;
-  if (qrow < g.nq) {
-    uint16_t* op = o + (((size_t)node * g.nq + qrow) * g.n_heads + head) * HDB;
+  if (it.slot < 0) {  // a whole unit: the final output
+    const float inv = 1.f / l_tot;
+    if (qrow < g.nq) {
+      uint16_t* op = o + (((size_t)node * g.nq + qrow) * g.n_heads + head) * HDB;
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int gi = 0; gi < 4; ++gi) {
+          const int32_t d = 32 * db + 8 * gi + 4 * hl;
+          u32x2 v;
+          v.x = pack_bf16x2(oacc[db][4 * gi + 0] * inv, oacc[db][4 * gi + 1] * inv);
+          v.y = pack_bf16x2(oacc[db][4 * gi + 2] * inv, oacc[db][4 * gi + 3] * inv);
+          *reinterpret_cast<u32x2*>(op + d) = v;
+        }
+    }
+  } else {            // a piece: unnormalised partial, its max (log2 units) and sum
+    const int32_t lrow = wave * 32 + r32;
+    float* po = g.part_o + ((size_t)it.slot * BQ + lrow) * HDB;
 #pragma unroll
     for (int db = 0; db < 4; ++db)
 #pragma unroll
       for (int gi = 0; gi < 4; ++gi) {
         const int32_t d = 32 * db + 8 * gi + 4 * hl;
-        u32x2 v;
-        v.x = pack_bf16x2(oacc[db][4 * gi + 0] * inv, oacc[db][4 * gi + 1] * inv);
-        v.y = pack_bf16x2(oacc[db][4 * gi + 2] * inv, oacc[db][4 * gi + 3] * inv);
-        *reinterpret_cast<u32x2*>(op + d) = v;
+        *reinterpret_cast<f32x4*>(po + d) =
+            f32x4{oacc[db][4 * gi + 0], oacc[db][4 * gi + 1], oacc[db][4 * gi + 2], oacc[db][4 * gi + 3]};
       }
+    if (hl == 0) {
+      g.part_ml[((size_t)it.slot * 2 + 0) * BQ + lrow] = m_run;
+      g.part_ml[((size_t)it.slot * 2 + 1) * BQ + lrow] = l_tot;
+    }
   }
 }
 
+// Merges the pieces of each tail unit, in piece order: one work-group per
+// tail unit, one thread per query row.  With m = max m_p:
+//   O = sum_p 2^(m_p - m) O_p / sum_p 2^(m_p - m) l_p.
+__global__ __launch_bounds__(BQ) void attn_combine_kernel(uint16_t* __restrict__ o, AttnGeom g,
+                                                          AttnPlan plan) {
+  const int32_t tu = blockIdx.x;
+  const int32_t unit = g.whole_units + tu;
+  const int32_t qt = unit % g.n_qtiles;
+  const int32_t node = (unit / g.n_qtiles) % g.n_nodes;
+  const int32_t head = unit / (g.n_qtiles * g.n_nodes);
+  const int32_t lrow = threadIdx.x;
+  const int32_t qrow = qt * BQ + lrow;
+  if (qrow >= g.nq) return;
+  const int32_t nt = node_tiles(plan, g, node);
+  auto nonempty = [&](int32_t p) { return p * nt / g.tail_split < (p + 1) * nt / g.tail_split; };
+  float m = -INFINITY;
+  for (int32_t p = 0; p < g.tail_split; ++p)
+    if (nonempty(p)) m = fmaxf(m, g.part_ml[((size_t)(p * g.tail_units + tu) * 2 + 0) * BQ + lrow]);
+  float acc[HDB];
+#pragma unroll
+  for (int d = 0; d < HDB; ++d) acc[d] = 0.f;
+  float l = 0.f;
+  for (int32_t p = 0; p < g.tail_split; ++p) {
+    if (!nonempty(p)) continue;
+    const size_t slot = (size_t)p * g.tail_units + tu;
+    const float a = __builtin_amdgcn_exp2f(g.part_ml[(slot * 2 + 0) * BQ + lrow] - m);
+    l += a * g.part_ml[(slot * 2 + 1) * BQ + lrow];
+    const f32x4* po = reinterpret_cast<const f32x4*>(g.part_o + (slot * BQ + lrow) * HDB);
+#pragma unroll
+    for (int d4 = 0; d4 < HDB / 4; ++d4) {
+      const f32x4 v = po[d4];
+      acc[4 * d4 + 0] += a * v[0];
+      acc[4 * d4 + 1] += a * v[1];
+      acc[4 * d4 + 2] += a * v[2];
+      acc[4 * d4 + 3] += a * v[3];
+    }
+  }
+  const float inv = 1.f / l;
+  uint16_t* op = o + (((size_t)node * g.nq + qrow) * g.n_heads + head) * HDB;
+#pragma unroll
+  for (int d8 = 0; d8 < HDB / 8; ++d8) {
+    u32x4 v;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = pack_bf16x2(acc[8 * d8 + 2 * k] * inv, acc[8 * d8 + 2 * k + 1] * inv);
+    *reinterpret_cast<u32x4*>(op + 8 * d8) = v;
+  }
+}
+
+// Tail split for a plan: units = heads x nodes x query tiles; the last
+// units mod 256 are cut into S pieces, S chosen to minimise the tail's rounds
+// (in units of one whole unit) plus a per-piece cost of about two key tiles
+// (prologue and partial write), with at most kAttnMaxPieces pieces and no
+// more pieces than the shortest node has key tiles.
+struct TailSplit {
+  int32_t whole, tail, split;
+};
+static TailSplit tail_split(const sc_plan* p, const sc_cache* c) {
+  const int32_t n = (int32_t)p->nodes.size();
+  const int32_t n_qtiles = (p->nq + BQ - 1) / BQ;
+  const int32_t units = n * c->d.n_heads * n_qtiles;
+  int64_t tiles = 0;
+  int32_t min_tiles = INT32_MAX;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t nt = (int32_t)(((int64_t)(p->page_off[i + 1] - p->page_off[i]) * c->d.tokens_per_page +
+                                  BK - 1) / BK);
+    tiles += nt;
+    min_tiles = std::min(min_tiles, nt);
+  }
+  const double mean_tiles = (double)tiles / std::max(n, 1);
+  TailSplit ts;
+  ts.tail = units % kAttnCUs;
+  ts.whole = units - ts.tail;
+  ts.split = 1;
+  if (ts.tail == 0) return ts;
+  double best = 1e30;
+  const int32_t smax = std::max(1, std::min({16, kAttnMaxPieces / ts.tail, min_tiles}));
+  for (int32_t sp = 1; sp <= smax; ++sp) {
+    const double rounds = (double)((ts.tail * sp + kAttnCUs - 1) / kAttnCUs);
+    const double cost = rounds * (1.0 / sp + 2.0 / mean_tiles);
+    if (cost < best - 1e-9) {
+      best = cost;
+      ts.split = sp;
+    }
+  }
+  return ts;
+}
+
+size_t attention_workspace_bytes(const sc_plan* p, const sc_cache* c) {
+  if (c->d.dtype != SC_DTYPE_BF16 || p->nodes.empty()) return 0;
+  const TailSplit ts = tail_split(p, c);
+  if (ts.split == 1) return 0;
+  return (size_t)ts.tail * ts.split * BQ * (HDB + 2) * sizeof(float);
+}
+
+size_t attention_workspace_bound() { return (size_t)kAttnMaxPieces * BQ * (HDB + 2) * sizeof(float); }
+
 int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const void* q, void* o,
-                     float scale, hipStream_t stream) {
+                     float scale, void* ws, size_t ws_bytes, hipStream_t stream) {
   const sc_cache_desc& d = c->d;
   const int32_t n = (int32_t)p->nodes.size();
   if (n > kMaxNodes) return fail(SC_EUNSUPPORTED, "pack of %d nodes exceeds %d", n, kMaxNodes);
@@ -430,6 +598,7 @@ int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const v
   for (int32_t i = 0; i <= n; ++i) plan.page_off[i] = p->page_off[i];
   for (size_t i = 0; i < p->page_slot.size(); ++i) plan.page_slot[i] = p->page_slot[i];
   AttnGeom g;
+  std::memset(&g, 0, sizeof g);
   g.layer_base = c->pool + (size_t)layer * d.n_slots * c->slot_bytes;
   g.slot_bytes = c->slot_bytes;
   g.kv_half = c->kv_half;
@@ -440,28 +609,48 @@ int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const v
   g.tpp_div = magic_div((uint32_t)d.tokens_per_page);
   g.scale = scale;
   g.scale_log2 = scale * 1.4426950408889634f;
-  timer_begin(TK_ATTENTION, stream);
   if (d.dtype == SC_DTYPE_F32) {
     g.n_qtiles = (p->nq + 63) / 64;
     const uint32_t nwg = (uint32_t)n * d.n_heads * g.n_qtiles;
+    timer_begin(TK_ATTENTION, stream);
     if (d.head_dim == 64)
       hipLaunchKernelGGL((attn_f32_kernel<64>), dim3(nwg), dim3(64), 0, stream,
                          static_cast<const float*>(q), static_cast<float*>(o), g, plan);
     else
       hipLaunchKernelGGL((attn_f32_kernel<128>), dim3(nwg), dim3(64), 0, stream,
                          static_cast<const float*>(q), static_cast<float*>(o), g, plan);
-  } else {
-    if (d.head_dim != HDB) return fail(SC_EUNSUPPORTED, "bf16 attention needs head_dim 128");
-    if (d.tokens_per_page < BK)
-      return fail(SC_EUNSUPPORTED, "bf16 attention needs pages of >= %d tokens (got %d)", BK,
-                  d.tokens_per_page);
-    if ((uint64_t)d.n_slots * c->slot_bytes > 0xffffffffull)
-      return fail(SC_EUNSUPPORTED, "bf16 attention needs one layer of the pool within 4 GB");
-    g.n_qtiles = (p->nq + BQ - 1) / BQ;
-    const uint32_t nwg = (uint32_t)n * d.n_heads * g.n_qtiles;
-    hipLaunchKernelGGL(attn_bf16_kernel, dim3(nwg), dim3(64 * NWAVES), 0, stream,
-                       static_cast<const uint16_t*>(q), static_cast<uint16_t*>(o), g, plan);
+    timer_end(TK_ATTENTION, stream);
+    SC_HIP(hipGetLastError());
+    return SC_OK;
   }
+  if (d.head_dim != HDB) return fail(SC_EUNSUPPORTED, "bf16 attention needs head_dim 128");
+  if (d.tokens_per_page < BK)
+    return fail(SC_EUNSUPPORTED, "bf16 attention needs pages of >= %d tokens (got %d)", BK,
+                d.tokens_per_page);
+  if ((uint64_t)d.n_slots * c->slot_bytes > 0xffffffffull)
+    return fail(SC_EUNSUPPORTED, "bf16 attention needs one layer of the pool within 4 GB");
+  const size_t need = attention_workspace_bytes(p, c);
+  if (ws_bytes < need || (need && !ws))
+    return fail(SC_EINVAL, "attention workspace of %zu bytes, need %zu", ws_bytes, need);
+  if (reinterpret_cast<uintptr_t>(ws) & 15) return fail(SC_EINVAL, "workspace must be 16-byte aligned");
+  g.n_qtiles = (p->nq + BQ - 1) / BQ;
+  const TailSplit ts = tail_split(p, c);
+  g.whole_units = ts.whole;
+  g.tail_units = ts.tail;
+  g.tail_split = ts.split;
+  if (ts.split == 1) {  // no pieces: the tail units run whole
+    g.whole_units += ts.tail;
+    g.tail_units = 0;
+  }
+  g.part_o = static_cast<float*>(ws);
+  g.part_ml = g.part_o + (size_t)g.tail_units * g.tail_split * BQ * HDB;
+  timer_begin(TK_ATTENTION, stream);
+  const uint32_t items = (uint32_t)(g.whole_units + g.tail_units * g.tail_split);
+  hipLaunchKernelGGL(attn_bf16_kernel, dim3(items), dim3(64 * NWAVES), 0, stream,
+                     static_cast<const uint16_t*>(q), static_cast<uint16_t*>(o), g, plan);
+  if (g.tail_units)
+    hipLaunchKernelGGL(attn_combine_kernel, dim3((uint32_t)g.tail_units), dim3(BQ), 0, stream,
+                       static_cast<uint16_t*>(o), g, plan);
   timer_end(TK_ATTENTION, stream);
   SC_HIP(hipGetLastError());
   return SC_OK;

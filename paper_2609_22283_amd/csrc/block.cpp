@@ -16,7 +16,7 @@ static size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
 extern "C" size_t sc_block_workspace_bytes(const sc_block_weights* w, int32_t n_tokens) {
   if (!w || n_tokens <= 0) return 0;
   const size_t T = (size_t)n_tokens;
-  return align256(T * w->hidden * 2) * 3 + align256(T * w->mlp * 2);
+  return align256(T * w->hidden * 2) * 3 + align256(T * w->mlp * 2) + attention_workspace_bound();
 }
 
 extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t layer,
@@ -79,6 +79,7 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
   uint16_t* qb = reinterpret_cast<uint16_t*>(wsb + align256((size_t)T * w->hidden * 2));
   uint16_t* ob = reinterpret_cast<uint16_t*>(wsb + 2 * align256((size_t)T * w->hidden * 2));
   uint16_t* ub = reinterpret_cast<uint16_t*>(wsb + 3 * align256((size_t)T * w->hidden * 2));
+  char* attn_ws = wsb + 3 * align256((size_t)T * w->hidden * 2) + align256((size_t)T * w->mlp * 2);
   uint16_t* xb = static_cast<uint16_t*>(x);
   const int32_t D = w->hidden;
 
@@ -110,7 +111,8 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
     return rc;
   for (int32_t i = 0; i < n; ++i)
     c->states.at(StateKey(p->nodes[i].chunk, p->nodes[i].level)).written[layer] = 1;
-  if ((rc = launch_attention(p, c, layer, qb, ob, 1.0f / std::sqrt((float)d.head_dim), stream)) != SC_OK)
+  if ((rc = launch_attention(p, c, layer, qb, ob, 1.0f / std::sqrt((float)d.head_dim), attn_ws,
+                             attention_workspace_bound(), stream)) != SC_OK)
     return rc;
   GemmEpilogue e2;
   std::memset(&e2, 0, sizeof e2);

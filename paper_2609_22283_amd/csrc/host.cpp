@@ -369,13 +369,18 @@ void sc_plan_free(sc_plan* p) { delete p; }
 
 // ---------------------------------------------------------------- attention
 
+size_t sc_attention_workspace_bytes(const sc_plan* p, const sc_cache* c) {
+  if (!p || !c || p->cache != c) return 0;
+  return attention_workspace_bytes(p, c);
+}
+
 int sc_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const void* q, void* o,
-                 float scale, sc_stream stream) {
+                 float scale, void* ws, size_t ws_bytes, sc_stream stream) {
   if (!p || !c || !q || !o) return fail(SC_EINVAL, "null argument");
   int rc = plan_check(p, c, layer);
   if (rc != SC_OK) return rc;
   if (p->nodes.empty()) return SC_OK;
-  return launch_attention(p, c, layer, q, o, scale, static_cast<hipStream_t>(stream));
+  return launch_attention(p, c, layer, q, o, scale, ws, ws_bytes, static_cast<hipStream_t>(stream));
 }
 
 // --------------------------------------------------------------------- rope

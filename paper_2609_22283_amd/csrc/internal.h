@@ -69,7 +69,15 @@ int plan_check(const sc_plan* plan, const sc_cache* cache, int32_t layer);
 
 // Kernel launchers (device code lives in the .hip files).
 int launch_attention(const sc_plan* plan, const sc_cache* cache, int32_t layer,
-                     const void* q, void* o, float scale, hipStream_t stream);
+                     const void* q, void* o, float scale, void* ws, size_t ws_bytes,
+                     hipStream_t stream);
+// Workspace of the bf16 attention for a plan (0 for fp32 caches and plans
+// whose units fill whole rounds of the CUs), and its bound over all plans
+// (at most kAttnMaxPieces partial results).
+constexpr int32_t kAttnCUs = 256;         // compute units of the target GPU
+constexpr int32_t kAttnMaxPieces = 1024;
+size_t attention_workspace_bytes(const sc_plan* plan, const sc_cache* cache);
+size_t attention_workspace_bound();
 int launch_append(const sc_cache* cache, int32_t layer, const int32_t* slots, int32_t chunk,
                   const void* k, const void* v, const sc_rope* rope, hipStream_t stream);
 int launch_rope_table(const sc_rope_desc* d, void* table, hipStream_t stream);

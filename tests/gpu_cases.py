@@ -96,7 +96,11 @@ class AttnCase:
 
     def run(self):
         torch = torch_mod()
-        sc.sc_attention(self.plan, self.cache, self.layer, self.q_dev, self.o_dev, self.scale)
+        nws = sc.sc_attention_workspace_bytes(self.plan, self.cache)
+        # stale contents must not matter: fill the workspace with NaN bytes
+        ws = torch.full((max(nws, 1),), 0xFF, dtype=torch.uint8, device="cuda")
+        sc.sc_attention(self.plan, self.cache, self.layer, self.q_dev, self.o_dev, self.scale,
+                        ws, nws)
         torch.cuda.synchronize()
         out = from_device(self.o_dev)
         n = self.geo.tokens_per_chunk

@@ -5,7 +5,8 @@ policies, several pack shapes), small bf16 packs whose pages (40 tokens) leave
 ragged tails inside 64-key tiles, the Wan-shaped clean / same-level /
 progressive packs on sampled rows, the segment probe, negative controls
 (mistakes planted in the oracle must fail the gates), NaN poisoning of
-unused slots, packed == sequential, and run-to-run determinism.
+unused slots, packed vs sequential, run-to-run determinism and the workspace
+check.
 """
 import numpy as np
 import pytest
@@ -18,7 +19,7 @@ from oracle.policy import select
 from synth.configs import SMALL, TINY, WAN, cfg2_clean, cfg3_same, cfg4_prog
 
 from gpu_cases import (AttnCase, BF16_MAX_ABS, F32_MAX_ABS, bf16_gates, from_device, sample_rows,
-                       to_device)
+                       to_device, torch_mod)
 
 pytestmark = pytest.mark.gpu
 
@@ -64,18 +65,27 @@ def test_small_bf16_packs(kind, pack, resident):
         bf16_gates(out[i], case.oracle(i), f"{kind} node {pack[i]}")
 
 
-def test_small_packed_equals_sequential_bitwise():
+def test_small_packed_matches_sequential():
+    """The same nodes packed and one per call.  The split-key schedule cuts a
+    node's key range where the pack's total work puts the work-group
+    boundaries, so the two runs sum in different orders: they agree within
+    the bf16 gates, not bitwise."""
     kind, pack, resident = SMALL_PACKS[0]
-    packed = AttnCase(SMALL, sc.SC_DTYPE_BF16, kind, pack, resident, seed=3).run()
+    case = AttnCase(SMALL, sc.SC_DTYPE_BF16, kind, pack, resident, seed=3)
+    packed = case.run()
     # the same nodes one per call, ascending chunk (in-pack history comes
     # from the cache, appended by the earlier calls)
     for i, node in enumerate(pack):
         res = resident + pack[:i]
-        alone = AttnCase(SMALL, sc.SC_DTYPE_BF16, kind, [node], res, seed=3).run()[0]
-        assert np.array_equal(alone, packed[i]), node
+        alone = AttnCase(SMALL, sc.SC_DTYPE_BF16, kind, [node], res, seed=3)
+        got = alone.run()[0]
+        bf16_gates(got, packed[i], f"alone vs packed {node}")
+        bf16_gates(got, alone.oracle(0), f"alone {node}")
 
 
 def test_small_deterministic_and_pack_order_free():
+    """Bitwise run-to-run determinism for one plan; a reversed pack agrees
+    within the gates."""
     kind, pack, resident = SMALL_PACKS[1]
     a = AttnCase(SMALL, sc.SC_DTYPE_BF16, kind, pack, resident, seed=4)
     o1 = a.run()
@@ -83,7 +93,24 @@ def test_small_deterministic_and_pack_order_free():
     rev = AttnCase(SMALL, sc.SC_DTYPE_BF16, kind, pack[::-1], resident, seed=4).run()
     for i in range(len(pack)):
         assert np.array_equal(o1[i], o2[i])
-        assert np.array_equal(o1[i], rev[len(pack) - 1 - i])
+        bf16_gates(rev[len(pack) - 1 - i], o1[i], f"reversed {pack[i]}")
+
+
+def test_workspace_checked():
+    """A workspace smaller than the plan needs is refused before any launch."""
+    kind, pack, resident = SMALL_PACKS[0]
+    case = AttnCase(SMALL, sc.SC_DTYPE_BF16, kind, pack, resident, seed=3)
+    torch = torch_mod()
+    need = sc.sc_attention_workspace_bytes(case.plan, case.cache)
+    assert need > 0
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    with pytest.raises(sc.ScError) as e:
+        sc.sc_attention(case.plan, case.cache, case.layer, case.q_dev, case.o_dev, case.scale,
+                        ws, need - 1)
+    assert e.value.code == sc.SC_EINVAL
+    with pytest.raises(sc.ScError) as e:
+        sc.sc_attention(case.plan, case.cache, case.layer, case.q_dev, case.o_dev, case.scale)
+    assert e.value.code == sc.SC_EINVAL
 
 
 def _probe_case(geo, kind, pack, resident):

@@ -6,10 +6,11 @@
   its limits scaled by the number of blocks a chunk's output passes through
   in one forward (errors of earlier forwards are damped by the sampler, which
   keeps at most 3/8 of the prediction at each re-noising).
-* Packed == sequential == serial, bitwise (Sec. 3.3: pipelining changes the
-  number of sequential rounds, not the updates; serial execution admits
-  progressive history when states are retained).  Per-row work does not
-  depend on how nodes are grouped, so the target is exact equality.
+* Packed, sequential and serial execution all meet that gate (Sec. 3.3:
+  pipelining changes the number of sequential rounds, not the updates;
+  serial execution admits progressive history when states are retained).
+  They are not bitwise equal: the attention's split-key schedule places its
+  cuts by the whole pack's work, so summation order depends on grouping.
 """
 import numpy as np
 import pytest
@@ -68,7 +69,7 @@ def _setup(geo, L, B, W, kind, seed, n_slots):
     return make, weights_np, noise_exact.reshape(B, K + 2, n, D), keep
 
 
-def test_small_pipeline_matches_oracle_and_schedules_agree():
+def test_small_pipeline_matches_oracle_in_every_mode():
     geo, L, B, W = SMALL, 2, 6, 2
     make, w_np, noise_np, keep = _setup(geo, L, B, W, "prog", seed=21, n_slots=60)
     torch = torch_mod()
@@ -79,24 +80,29 @@ def test_small_pipeline_matches_oracle_and_schedules_agree():
         torch.cuda.synchronize()
         runs[mode] = from_device(p.xs)
         assert p.cache.free_slot_count() == 60          # everything released at the end
-    assert np.array_equal(runs["packed"], runs["sequential"])
-    assert np.array_equal(runs["packed"], runs["serial"])
     shp = BlockShape(geo.hidden, geo.heads, geo.head_dim, geo.mlp, geo.frames_per_chunk,
                      geo.grid_h, geo.grid_w, geo.rope_dims, geo.theta)
     outs, _, _ = run_stack(pipeline_rounds(B, geo.K, True), policy("prog", geo.K, W), L,
                            lambda l: w_np[l], lambda c, j: noise_np[c, j], shp, t_sched=T_SCHED)
-    got = runs["packed"]
-    for c in range(B):
-        want = outs[(c, 1)]                              # x^0 = prediction at t_0 = 0
-        d = np.abs(got[c] - want)
-        lim = 2e-2 * L * np.maximum(1.0, np.abs(want))
-        assert np.all(np.isfinite(got[c]))
-        assert float((d / lim).max()) <= 1.0, (c, float((d / lim).max()))
-        assert d.mean() <= 4e-3 * L * max(1.0, float(np.abs(want).mean())), (c, d.mean())
+    for mode, got in runs.items():
+        for c in range(B):
+            want = outs[(c, 1)]                          # x^0 = prediction at t_0 = 0
+            _stack_gate(got[c], want, L, (mode, c))
+
+
+def _stack_gate(got, want, L, what, runs=1):
+    """The block gate scaled by L blocks; runs=2 when both sides carry the
+    GPU's error (each within the gate of the exact value)."""
+    d = np.abs(got - want)
+    lim = runs * 2e-2 * L * np.maximum(1.0, np.abs(want))
+    assert np.all(np.isfinite(got)), what
+    assert float((d / lim).max()) <= 1.0, (what, float((d / lim).max()))
+    assert d.mean() <= runs * 4e-3 * L * max(1.0, float(np.abs(want).mean())), (what, d.mean())
 
 
 def test_wan_two_layer_pipeline_schedules_agree():
-    """Wan block shapes, 2 layers, 8 chunks: packed == sequential bitwise."""
+    """Wan block shapes, 2 layers, 8 chunks: packed and sequential execution
+    agree within the stack gate."""
     geo, L, B, W = WAN, 2, 8, 6
     make, _, _, keep = _setup(geo, L, B, W, "prog", seed=22, n_slots=(W + 2 * geo.K + 4) * 3)
     torch = torch_mod()
@@ -106,5 +112,5 @@ def test_wan_two_layer_pipeline_schedules_agree():
     b.run("sequential")
     torch.cuda.synchronize()
     xa, xb = from_device(a.xs), from_device(b.xs)
-    assert np.all(np.isfinite(xa))
-    assert np.array_equal(xa, xb)
+    for c in range(B):
+        _stack_gate(xa[c], xb[c], L, c, runs=2)

@@ -25,7 +25,7 @@ def test_header_symbols_exported():
     assert declared == set(sc.EXPORTED_SYMBOLS)
     for name in declared:
         assert hasattr(sc.lib, name), name
-    assert sc.sc_abi_version() == 1
+    assert sc.sc_abi_version() == sc.ABI_VERSION == 2
 
 
 def _random_pack(rnd, K, max_chunk=9, max_n=6):
@@ -172,3 +172,27 @@ def test_stale_plan_detected_on_cpu():
     with pytest.raises(sc.ScError) as e:                       # reserved but never written
         sc.sc_attention(plan2, cache, 0, 0x1000, 0x2000, 0.125)
     assert e.value.code == sc.SC_EUNAVAILABLE
+
+
+def test_attention_workspace_size():
+    """Workspace of the bf16 attention: units (head, node, query tile) that
+    fill whole rounds of the 256 CUs run whole; the remaining units are cut
+    into S pieces, each leaving a partial (256 rows of 128 fp32 outputs plus
+    max and sum).  S minimises the tail's rounds plus a per-piece cost of two
+    key tiles, within 1024 pieces and the shortest node's key tiles.  No
+    workspace for fp32 caches or when nothing is cut."""
+    per_piece = 256 * (128 + 2) * 4
+    cache = sc.sc_cache_create(0x100000, 1, 2, 128, 64, 1, 64)
+    plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(0, 0)]), cache)
+    assert sc.sc_attention_workspace_bytes(plan, cache) == 0          # 1 key tile: no cut
+    sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(1, 0), (2, 0)]), cache)
+    plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 3, [(3, 4)]), cache)
+    # 2 units of 4 tiles: S = 4 (one round of quarter units + 4 x 2/4 overhead)
+    assert sc.sc_attention_workspace_bytes(plan, cache) == 2 * 4 * per_piece
+    big = sc.sc_cache_create(0x100000, 1, 12, 128, 1560, 3, 64)
+    sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(0, 0)]), big)
+    plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 1, [(1, 4)]), big)
+    assert sc.sc_attention_workspace_bytes(plan, big) == 0            # 228 units: one round
+    f32 = sc.sc_cache_create(0x100000, 1, 2, 64, 16, 1, 8, sc.SC_DTYPE_F32)
+    plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(0, 0)]), f32)
+    assert sc.sc_attention_workspace_bytes(plan, f32) == 0
