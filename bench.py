@@ -137,13 +137,36 @@ def time_steps(setup, fn, steps, warmup, timer=False):
     ms = e0.elapsed_time(e1) / steps
     kernels = {}
     if timer:
-        for kind in ("attention", "gemm_qkv", "gemm_out", "gemm_up", "gemm_down", "rmsnorm",
-                     "sampler"):
+        for kind in ("attention", "attention_combine", "gemm_qkv", "gemm_out", "gemm_up",
+                     "gemm_down", "rmsnorm", "sampler"):
             n, tot = sc.sc_timer_read(kind)
             if n:
                 kernels[kind] = (n, tot / n)
         sc.sc_timer_enable(False)
     return ms, wall / steps * 1e3, kernels
+
+
+def mfma_ceiling(iters=4000, launches=5):
+    """Sustained rate of the library's matrix-core probe (back-to-back bf16
+    MFMAs from registers, no memory traffic), with random and with constant
+    operands: TFLOP/s each.  Random operands draw more power and run at a
+    lower clock; that rate bounds what any bf16 kernel on random data can
+    reach on this device."""
+    import torch
+
+    import paper_2609_22283_amd as sc
+    nb = sc.sc_probe_mfma_out_bytes()
+    out = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    res = {}
+    for rnd in (True, False):
+        sc.sc_probe_mfma(rnd, iters, out, nb)                 # warm-up launch
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fl = sum(sc.sc_probe_mfma(rnd, iters, out, nb) for _ in range(launches))
+        e1.record()
+        torch.cuda.synchronize()
+        res["random" if rnd else "constant"] = round(fl / (e0.elapsed_time(e1) * 1e-3) / 1e12, 1)
+    return res
 
 
 def segment_counts(wl, g):
@@ -325,6 +348,7 @@ def main():
     ap.add_argument("--layers", type=int, default=30, help="cfg5: blocks in the stack")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sequential", action="store_true")
+    ap.add_argument("--no-probe", action="store_true", help="skip the matrix-core ceiling probe")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -407,6 +431,7 @@ def main():
         "attention_tflops": round(attn_tflops, 1),
         "attention_pct_peak": round(100.0 * attn_tflops / PEAK_BF16_TFLOPS, 2),
         "attention_ms": round(attn_ms, 4),
+        "attention_combine_ms": round(kernels["attention_combine"][1], 4) if "attention_combine" in kernels else 0.0,
         "gemm_tflops": round(g_flops / (gemm_ms * 1e-3) / 1e12, 1) if gemm_ms else None,
         "kernel_avg_ms": {k: round(v[1], 4) for k, v in kernels.items()},
         "sequential_ms_per_step": round(seq_ms, 4) if seq_ms else None,
@@ -416,6 +441,11 @@ def main():
                      "traffic": None, "kernel": "attn_bf16_kernel",
                      "algorithmic_per_launch": f"{a_flops:.4e} FLOP"},
     }
+    if not args.no_probe:
+        ceil = mfma_ceiling()
+        log(f"[bench] matrix-core probe: {ceil} TFLOP/s")
+        result["mfma_sustained_tflops"] = ceil
+        result["attention_frac_of_sustained_random"] = round(attn_tflops / ceil["random"], 4)
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on the host (bounded sample)...")
         result["cpu_baseline"] = cpu_baseline(wl)

@@ -259,10 +259,24 @@ int sc_stack_forward(const sc_block_weights* layers, int32_t n_layers, sc_cache*
  * events and returns, for one kernel kind, the number of launches and the
  * summed elapsed milliseconds since the timer was last enabled.  Kinds:
  * "attention", "gemm_qkv", "gemm_out", "gemm_up", "gemm_down", "rmsnorm",
- * "append", "sampler".  Enabling clears earlier records.  Events are created
+ * "append", "sampler", "attention_combine" (the merge of split key ranges;
+ * "attention" is the main kernel alone).  Enabling clears earlier records.  Events are created
  * lazily and reused; the cost is two event records per launch. */
 int sc_timer_enable(int on);
 int sc_timer_read(const char* kind, int32_t* launches, double* total_ms);
+
+/* ---- Matrix-core ceiling probe (measurement support) ------------------
+ * Launches one kernel on `stream` that issues only 32x32x16 bf16 MFMAs from
+ * registers (two 8-wave work-groups per CU, `iters` rounds of 16 MFMAs per
+ * wave) and sets *flops to the work it performs; the caller times it with
+ * its own events.  random_operands != 0 fills the operands with random bf16
+ * values (the sustained rate for data like the attention's; power limits
+ * the clock), else with constants.  out: device scratch of at least
+ * sc_probe_mfma_out_bytes() bytes (one float per thread, written so the
+ * work is not optimised away).  Errors: SC_EINVAL, SC_EDEVICE. */
+size_t sc_probe_mfma_out_bytes(void);
+int sc_probe_mfma(int32_t random_operands, int32_t iters, void* out, size_t out_bytes,
+                  double* flops, sc_stream stream);
 
 #ifdef __cplusplus
 }

@@ -20,7 +20,8 @@ __all__ = [
     "sc_abi_version", "sc_selection_build", "sc_cache_pool_bytes", "sc_cache_create",
     "sc_rope_table_bytes", "sc_rope_table_build", "sc_plan_build", "sc_attention",
     "sc_attention_workspace_bytes", "sc_block_workspace_bytes", "sc_block_forward", "sc_sampler_step",
-    "sc_timer_enable", "sc_timer_read", "Selection", "Cache", "Plan", "Rope", "BlockWeights",
+    "sc_timer_enable", "sc_timer_read", "sc_probe_mfma_out_bytes", "sc_probe_mfma",
+    "Selection", "Cache", "Plan", "Rope", "BlockWeights",
     "sc_pipeline_rounds", "sc_pipeline_round_nodes", "sc_cache_release_unread", "sc_stack_forward",
 ]
 
@@ -40,7 +41,7 @@ EXPORTED_SYMBOLS = [
     "sc_plan_build", "sc_plan_get", "sc_plan_free",
     "sc_attention_workspace_bytes", "sc_attention",
     "sc_block_workspace_bytes", "sc_block_forward", "sc_sampler_step",
-    "sc_timer_enable", "sc_timer_read",
+    "sc_timer_enable", "sc_timer_read", "sc_probe_mfma_out_bytes", "sc_probe_mfma",
     "sc_pipeline_rounds", "sc_pipeline_round_nodes", "sc_cache_release_unread", "sc_stack_forward",
 ]
 
@@ -131,6 +132,8 @@ _SIG = {
                                   _P, _P, _P, C.c_int64, _P]),
     "sc_timer_enable": (C.c_int, [C.c_int]),
     "sc_timer_read": (C.c_int, [C.c_char_p, _I32P, C.POINTER(C.c_double)]),
+    "sc_probe_mfma_out_bytes": (C.c_size_t, []),
+    "sc_probe_mfma": (C.c_int, [C.c_int32, C.c_int32, _P, C.c_size_t, C.POINTER(C.c_double), _P]),
     "sc_pipeline_rounds": (C.c_int, [C.c_int32, C.c_int32, C.c_int32]),
     "sc_pipeline_round_nodes": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                           C.POINTER(sc_node), _I32P]),
@@ -396,6 +399,18 @@ def sc_timer_read(kind: str):
     n, ms = C.c_int32(), C.c_double()
     _check(lib.sc_timer_read(kind.encode(), C.byref(n), C.byref(ms)))
     return n.value, ms.value
+
+
+def sc_probe_mfma_out_bytes() -> int:
+    return lib.sc_probe_mfma_out_bytes()
+
+
+def sc_probe_mfma(random_operands: bool, iters: int, out, out_bytes: int, stream=None) -> float:
+    """Launch the matrix-core probe; returns the FLOPs it performs."""
+    fl = C.c_double()
+    _check(lib.sc_probe_mfma(1 if random_operands else 0, iters, _ptr(out), out_bytes, C.byref(fl),
+                             _stream(stream)))
+    return fl.value
 
 
 # ------------------------------------------------------------------- schedule

@@ -93,6 +93,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 // ------------------------------------------------------------- bf16 kernel
 constexpr int NWAVES = 8;              // waves per work-group, 32 queries each
 constexpr int BQ = 32 * NWAVES;        // queries per work-group
+constexpr int WG_PER_CU = 8 / NWAVES;  // resident work-groups per CU (LDS and registers allow 8 waves)
 constexpr int BK = 64;                 // keys per tile
 constexpr int HDB = 128;               // head dim of the bf16 kernel
 constexpr int KT_BYTES = BK * HDB * 2;  // 16 KB
@@ -279,7 +280,7 @@ __device__ __forceinline__ AttnItem decode_item(const AttnPlan& plan, const Attn
   return it;
 }
 
-__global__ __launch_bounds__(64 * NWAVES, 1) void attn_bf16_kernel(const uint16_t* __restrict__ q,
+__global__ __launch_bounds__(64 * NWAVES, WG_PER_CU) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                                    uint16_t* __restrict__ o,
                                                                    AttnGeom g, AttnPlan plan) {
   // K buffers 0, 1 then V^T buffers 0, 1 (16 KB each)
@@ -561,14 +562,15 @@ static TailSplit tail_split(const sc_plan* p, const sc_cache* c) {
   }
   const double mean_tiles = (double)tiles / std::max(n, 1);
   TailSplit ts;
-  ts.tail = units % kAttnCUs;
+  const int32_t slots = kAttnCUs * WG_PER_CU;  // work-groups resident at once
+  ts.tail = units % slots;
   ts.whole = units - ts.tail;
   ts.split = 1;
   if (ts.tail == 0) return ts;
   double best = 1e30;
   const int32_t smax = std::max(1, std::min({16, kAttnMaxPieces / ts.tail, min_tiles}));
   for (int32_t sp = 1; sp <= smax; ++sp) {
-    const double rounds = (double)((ts.tail * sp + kAttnCUs - 1) / kAttnCUs);
+    const double rounds = (double)((ts.tail * sp + slots - 1) / slots);
     const double cost = rounds * (1.0 / sp + 2.0 / mean_tiles);
     if (cost < best - 1e-9) {
       best = cost;
@@ -644,14 +646,17 @@ int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const v
   }
   g.part_o = static_cast<float*>(ws);
   g.part_ml = g.part_o + (size_t)g.tail_units * g.tail_split * BQ * HDB;
-  timer_begin(TK_ATTENTION, stream);
   const uint32_t items = (uint32_t)(g.whole_units + g.tail_units * g.tail_split);
+  timer_begin(TK_ATTENTION, stream);
   hipLaunchKernelGGL(attn_bf16_kernel, dim3(items), dim3(64 * NWAVES), 0, stream,
                      static_cast<const uint16_t*>(q), static_cast<uint16_t*>(o), g, plan);
-  if (g.tail_units)
+  timer_end(TK_ATTENTION, stream);
+  if (g.tail_units) {
+    timer_begin(TK_ATTN_COMBINE, stream);
     hipLaunchKernelGGL(attn_combine_kernel, dim3((uint32_t)g.tail_units), dim3(BQ), 0, stream,
                        static_cast<uint16_t*>(o), g, plan);
-  timer_end(TK_ATTENTION, stream);
+    timer_end(TK_ATTN_COMBINE, stream);
+  }
   SC_HIP(hipGetLastError());
   return SC_OK;
 }

@@ -85,7 +85,7 @@ int launch_rope_table(const sc_rope_desc* d, void* table, hipStream_t stream);
 // Kernel timer: launchers bracket their kernel with timer_begin/timer_end.
 enum TimerKind {
   TK_ATTENTION = 0, TK_GEMM_QKV, TK_GEMM_OUT, TK_GEMM_UP, TK_GEMM_DOWN, TK_RMSNORM, TK_APPEND,
-  TK_SAMPLER, TK_COUNT
+  TK_SAMPLER, TK_ATTN_COMBINE, TK_COUNT
 };
 void timer_begin(int kind, hipStream_t stream);
 void timer_end(int kind, hipStream_t stream);

@@ -1,0 +1,76 @@
+// Matrix-core ceiling probe (measurement support, not part of the method).
+// A grid of 8-wave work-groups, two per CU, issues back-to-back
+// 32x32x16 bf16 MFMAs on four accumulator chains with operands held in
+// registers: no memory traffic, no vector-ALU work.  With random operands
+// the sustained rate shows the matrix cores' power-limited throughput for
+// data like the attention's; constant operands toggle few bits and run at a
+// higher clock.
+#include "device.h"
+#include "internal.h"
+
+namespace sc {
+namespace {
+
+constexpr int kProbeThreads = 512;
+constexpr int kProbeWGPerCU = 2;
+
+__device__ __forceinline__ uint32_t mix(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x7feb352du;
+  x ^= x >> 15;
+  x *= 0x846ca68bu;
+  x ^= x >> 16;
+  return x;
+}
+
+__global__ __launch_bounds__(kProbeThreads) void mfma_probe_kernel(float* out, int32_t iters,
+                                                                   int32_t random_operands) {
+  bf16x8 a[8], b[8];
+  for (int r = 0; r < 8; ++r)
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t key = (blockIdx.x * kProbeThreads + threadIdx.x) * 64 + r * 8 + i;
+      const float va = random_operands ? (float)(mix(key) & 0xffffu) / 32768.0f - 1.0f : 0.5f;
+      const float vb = random_operands ? (float)(mix(key ^ 0x9e3779b9u) & 0xffffu) / 32768.0f - 1.0f : 0.25f;
+      a[r][i] = static_cast<__bf16>(va);
+      b[r][i] = static_cast<__bf16>(vb);
+    }
+  f32x16 acc[4];
+  for (int j = 0; j < 4; ++j) acc[j] = f32x16{};
+  for (int32_t it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+      acc[j & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[j & 7], b[(3 * j) & 7], acc[j & 3], 0, 0, 0);
+  }
+  float s = 0.f;
+  for (int j = 0; j < 4; ++j)
+    for (int i = 0; i < 16; ++i) s += acc[j][i];
+  out[blockIdx.x * kProbeThreads + threadIdx.x] = s;
+}
+
+}  // namespace
+}  // namespace sc
+
+using namespace sc;
+
+extern "C" size_t sc_probe_mfma_out_bytes(void) {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 0;
+  return (size_t)cus * kProbeWGPerCU * kProbeThreads * sizeof(float);
+}
+
+extern "C" int sc_probe_mfma(int32_t random_operands, int32_t iters, void* out, size_t out_bytes,
+                             double* flops, sc_stream stream) {
+  if (!out || iters <= 0) return fail(SC_EINVAL, "null output or iters <= 0");
+  const size_t need = sc_probe_mfma_out_bytes();
+  if (need == 0) return fail(SC_EDEVICE, "no device");
+  if (out_bytes < need) return fail(SC_EINVAL, "probe output of %zu bytes, need %zu", out_bytes, need);
+  const uint32_t blocks = (uint32_t)(need / (kProbeThreads * sizeof(float)));
+  if (flops) *flops = 2.0 * 32 * 32 * 16 * 16.0 * iters * blocks * (kProbeThreads / 64);
+  hipLaunchKernelGGL(mfma_probe_kernel, dim3(blocks), dim3(kProbeThreads), 0,
+                     static_cast<hipStream_t>(stream), static_cast<float*>(out), iters,
+                     random_operands);
+  SC_HIP(hipGetLastError());
+  return SC_OK;
+}

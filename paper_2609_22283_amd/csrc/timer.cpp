@@ -8,7 +8,8 @@ namespace sc {
 namespace {
 
 const char* const kNames[TK_COUNT] = {"attention", "gemm_qkv", "gemm_out", "gemm_up",
-                                      "gemm_down", "rmsnorm", "append", "sampler"};
+                                      "gemm_down", "rmsnorm", "append", "sampler",
+                                      "attention_combine"};
 
 struct Record {
   int kind;

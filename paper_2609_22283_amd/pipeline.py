@@ -97,7 +97,8 @@ class StackPipeline:
                 e1.record()
                 times.append((e0, e1))
             if kernel_timer_rounds and g == kernel_timer_rounds[1]:
-                for kind in ("attention", "gemm_qkv", "gemm_out", "gemm_up", "gemm_down"):
+                for kind in ("attention", "attention_combine", "gemm_qkv", "gemm_out", "gemm_up",
+                             "gemm_down"):
                     self.kernel_times[kind] = sc.sc_timer_read(kind)
                 sc.sc_timer_enable(False)
         if time_rounds:
