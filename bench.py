@@ -33,6 +33,23 @@ if ROOT not in sys.path:
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 METRIC = "steady-state latent frames/s per DiT block + attention TFLOP/s (% bf16 MFMA peak)"
+# HBM bytes per attn_bf16_kernel launch at the default workload: rocprofv3
+# FETCH_SIZE and WRITE_SIZE per dispatch, scaled by what the same counters
+# read for a plain 256 MiB copy (x2.0 fetch, x1.0 write).  Valid only for the
+# kernel sources it was measured on (hash below); otherwise reported as null.
+ATTN_TRAFFIC = {"sources_sha1": "8feb0c401095f94791b7dcfc923e5425fc027fa4",
+                "fetch_bytes": 1.3620e9, "write_bytes": 1.8264e8}
+
+
+def attn_traffic():
+    import hashlib
+    h = hashlib.sha1()
+    for f in ("attention.hip", "device.h"):
+        with open(os.path.join(ROOT, "paper_2609_22283_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    if h.hexdigest() != ATTN_TRAFFIC["sources_sha1"]:
+        return None
+    return round(ATTN_TRAFFIC["fetch_bytes"] + ATTN_TRAFFIC["write_bytes"], -6)
 
 
 def log(*a):
@@ -349,6 +366,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sequential", action="store_true")
     ap.add_argument("--no-probe", action="store_true", help="skip the matrix-core ceiling probe")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only copy a 256 MiB device buffer 4 times (calibrates the HBM byte "
+                         "counters of a profiler run) and exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -358,6 +378,14 @@ def main():
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.copy_probe:
+        src = torch.ones(256 << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(4):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": 256 << 20, "copies": 4}), flush=True)
+        return
     if args.workload == "cfg5":
         from synth.configs import WAN as g
         r = bench_stack(args)
@@ -438,7 +466,8 @@ def main():
         "packed_vs_sequential": round(seq_ms / ms, 3) if seq_ms else None,
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None, "kernel": "attn_bf16_kernel",
+                     "traffic": attn_traffic() if wl.name == "cfg4-prog" else None,
+                     "kernel": "attn_bf16_kernel",
                      "algorithmic_per_launch": f"{a_flops:.4e} FLOP"},
     }
     if not args.no_probe:
