@@ -289,14 +289,17 @@ def stack_weights(n_layers, seed=0):
 
 
 def bench_stack(args):
-    """cfg5: the 30-block stack run as a pipeline over 16 chunks (K = 4, W = 6).
+    """cfg5: the 30-block stack run as a pipeline over B chunks (K = 4, W = 6;
+    B = 16 by default, 40 for the paper's 477-frame streams).
 
     Steady-state rounds are those with a full pack (4 denoising nodes + the
     refresh node) whose oldest node already has a full 6-chunk window; each
     produces one clean chunk (3 latent frames).  Modes: packed (one forward
     per round), sequential (the same nodes one forward each), and the clean
     serial baseline of the paper's latency table (clean history, chunk by
-    chunk, 5 forwards per chunk)."""
+    chunk, 5 forwards per chunk).  The same-level pipeline (Eq. 7 with the
+    same-level policy: every level's recent window stays cached) is timed
+    packed as well."""
     import numpy as np
     import torch
 
@@ -305,7 +308,7 @@ def bench_stack(args):
     from synth import TAG_NOISE, bf16_bits, normal
     from synth.configs import WAN as g
 
-    L, B, K, W = args.layers, 16, g.K, g.W
+    L, B, K, W = args.layers, args.chunks, g.K, g.W
     n, D = g.tokens_per_chunk, g.hidden
     t0 = time.perf_counter()
     layers, keep = stack_weights(L)
@@ -320,7 +323,9 @@ def bench_stack(args):
     rt = torch.empty(sc.sc_rope_table_bytes(g.grid_h, g.grid_w, g.rope_dims, 3 * B + 3),
                      dtype=torch.uint8, device="cuda")
     rope = sc.sc_rope_table_build(rt, g.grid_h, g.grid_w, g.rope_dims, 3 * B + 3, g.theta)
-    n_slots = (W + 2 * K + 4) * g.frames_per_chunk
+    # progressive: W clean chunks + one round in flight; same-level: a W-chunk
+    # window per level (K + 1 levels) + one round in flight
+    n_slots = ((K + 1) * (W + 1) + K + 2) * g.frames_per_chunk
     nbytes = sc.sc_cache_pool_bytes(L, g.heads, g.head_dim, g.tokens_per_page, g.frames_per_chunk,
                                     n_slots)
     pool = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
@@ -337,16 +342,17 @@ def bench_stack(args):
 
     steady = [r for r in range(K + B) if r - K >= W and r < B]      # full pack, full window
     res = {}
-    for mode, policy in (("packed", "prog"), ("sequential", "prog")):
+    for key, mode, policy in (("packed", "packed", "prog"), ("sequential", "sequential", "prog"),
+                              ("same_packed", "packed", "same")):
         p = pipeline(policy)
         ms = p.run(mode, time_rounds=True,
-                   kernel_timer_rounds=(steady[0], steady[-1]) if mode == "packed" else None)
-        if mode == "packed":
+                   kernel_timer_rounds=(steady[0], steady[-1]) if key == "packed" else None)
+        if key == "packed":
             n_attn, attn_tot = p.kernel_times["attention"]
             res["attn_ms_per_launch"] = attn_tot / max(1, n_attn)
             res["attn_launches"] = n_attn
-        res[mode] = float(np.median([ms[r] for r in steady]))
-        log(f"[bench] cfg5 {mode}: median steady round {res[mode]:.2f} ms "
+        res[key] = float(np.median([ms[r] for r in steady]))
+        log(f"[bench] cfg5 {key}: median steady round {res[key]:.2f} ms "
             f"(rounds {steady[0]}..{steady[-1]})")
     p = pipeline("clean")
     ms = p.run("serial", time_rounds=True)                          # one entry per node
@@ -363,6 +369,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="cfg4", choices=["cfg4", "cfg4R", "cfg3", "cfg2", "cfg5"])
     ap.add_argument("--layers", type=int, default=30, help="cfg5: blocks in the stack")
+    ap.add_argument("--chunks", type=int, default=16,
+                    help="cfg5: chunks in the stream (40 = the paper's 477-frame videos)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sequential", action="store_true")
     ap.add_argument("--no-probe", action="store_true", help="skip the matrix-core ceiling probe")
@@ -399,10 +407,11 @@ def main():
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
             "data": "synthetic (seeded noise, N(0,0.02) weights)",
             "config": {"workload": f"cfg5: {args.layers}-block Wan-shaped stack, progressive "
-                                   "pipeline, 16 chunks x 3 latent frames, K=4, W=6, refresh",
-                       "layers": args.layers, "parallelism": "single GPU"},
+                                   f"pipeline, {args.chunks} chunks x 3 latent frames, K=4, W=6, refresh",
+                       "layers": args.layers, "chunks": args.chunks, "parallelism": "single GPU"},
             "stack_latent_frames_per_s": round(3.0 / (r["packed"] * 1e-3), 3),
             "sequential_ms_per_round": round(r["sequential"], 3),
+            "same_level_packed_ms_per_round": round(r["same_packed"], 3),
             "clean_serial_ms_per_chunk": round(r["clean_serial"], 3),
             "packed_vs_sequential": round(r["sequential"] / r["packed"], 3),
             "prog_pipeline_vs_clean_serial": round(r["clean_serial"] / r["packed"], 3),

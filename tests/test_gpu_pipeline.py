@@ -90,6 +90,30 @@ def test_small_pipeline_matches_oracle_in_every_mode():
             _stack_gate(got[c], want, L, (mode, c))
 
 
+def test_small_same_level_pipeline_matches_oracle():
+    """The same-level pipelined schedule (Eq. 7 with phi_same; the level-j
+    states of earlier chunks are reused from earlier rounds, so the cache
+    keeps every level's recent window): packed and sequential execution
+    against the oracle's run of the same rounds."""
+    geo, L, B, W = SMALL, 2, 6, 2
+    make, w_np, noise_np, keep = _setup(geo, L, B, W, "same", seed=23, n_slots=90)
+    torch = torch_mod()
+    runs = {}
+    for mode in ("packed", "sequential"):
+        p = make()
+        p.run(mode)
+        torch.cuda.synchronize()
+        runs[mode] = from_device(p.xs)
+        assert p.cache.free_slot_count() == 90
+    shp = BlockShape(geo.hidden, geo.heads, geo.head_dim, geo.mlp, geo.frames_per_chunk,
+                     geo.grid_h, geo.grid_w, geo.rope_dims, geo.theta)
+    outs, _, _ = run_stack(pipeline_rounds(B, geo.K, True), policy("same", geo.K, W), L,
+                           lambda l: w_np[l], lambda c, j: noise_np[c, j], shp, t_sched=T_SCHED)
+    for mode, got in runs.items():
+        for c in range(B):
+            _stack_gate(got[c], outs[(c, 1)], L, (mode, c))
+
+
 def _stack_gate(got, want, L, what, runs=1):
     """The block gate scaled by L blocks; runs=2 when both sides carry the
     GPU's error (each within the gate of the exact value)."""
