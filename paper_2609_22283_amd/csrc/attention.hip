@@ -42,6 +42,7 @@ struct AttnGeom {
   int32_t whole_units, tail_units, tail_split;
   float* part_o;          // [tail_units * tail_split][BQ][128] unnormalised partial outputs
   float* part_ml;         // [tail_units * tail_split][2][BQ] partial max (log2 units) and sum
+                          // (BQ: queries per work-group of the instantiation launched)
 };
 
 static DivMagic magic_div(uint32_t d) {
@@ -91,9 +92,17 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 }
 
 // ------------------------------------------------------------- bf16 kernel
-constexpr int NWAVES = 8;              // waves per work-group, 32 queries each
-constexpr int BQ = 32 * NWAVES;        // queries per work-group
-constexpr int WG_PER_CU = 8 / NWAVES;  // resident work-groups per CU (LDS and registers allow 8 waves)
+// The kernel is instantiated for NW = 8 waves (256 queries per work-group,
+// one work-group per CU) and NW = 4 (128 queries, two per CU); both keep 8
+// waves per CU, two per SIMD, within the register budget of that occupancy.
+// The host takes NW = 4 for nodes of at most 128 queries.
+template <int NW> struct Shape {
+  static constexpr int BQ = 32 * NW;              // queries per work-group
+  static constexpr int WG_PER_CU = 8 / NW;        // resident work-groups per CU
+  static constexpr int KCP = 64 / (4 * NW);       // K copy instructions per wave per tile
+  static constexpr int VCP = 128 / (8 * NW);      // V copy instructions per wave per tile
+};
+constexpr int BQ_MAX = 256;
 constexpr int BK = 64;                 // keys per tile
 constexpr int HDB = 128;               // head dim of the bf16 kernel
 constexpr int KT_BYTES = BK * HDB * 2;  // 16 KB
@@ -280,11 +289,13 @@ __device__ __forceinline__ AttnItem decode_item(const AttnPlan& plan, const Attn
   return it;
 }
 
-__global__ __launch_bounds__(64 * NWAVES, WG_PER_CU) void attn_bf16_kernel(const uint16_t* __restrict__ q,
+template <int NW>
+__global__ __launch_bounds__(64 * NW, Shape<NW>::WG_PER_CU) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                                    uint16_t* __restrict__ o,
                                                                    AttnGeom g, AttnPlan plan) {
   // K buffers 0, 1 then V^T buffers 0, 1 (16 KB each)
   __shared__ __attribute__((aligned(1024))) char smem[SMEM_BYTES];
+  constexpr int BQ = Shape<NW>::BQ;
   const AttnItem it = decode_item(plan, g, blockIdx.x);
   if (it.ta == it.tb) return;  // empty piece of a unit shorter than the split
   const int32_t node = it.node, head = it.head, qt = it.qt;
@@ -335,9 +346,9 @@ __global__ __launch_bounds__(64 * NWAVES, WG_PER_CU) void attn_bf16_kernel(const
   // tokens), so the page of a key is chosen against one wave-uniform
   // boundary.  Offsets are 32-bit, relative to the layer's slots (the host
   // checks a layer fits in 4 GB); the per-page parts are wave-uniform.  Per
-  // wave: 2 copies of 4 K rows (1 KB each) and 2 copies of 8 V^T rows.  Lane
+  // wave: KCP copies of 4 K rows (1 KB each) and VCP copies of 8 V^T rows.  Lane
   // (row, physical column p) fetches logical column p ^ swizzle(row).
-  constexpr int KCP = 64 / (4 * NWAVES), VCP = 128 / (8 * NWAVES);  // copies per wave
+  constexpr int KCP = Shape<NW>::KCP, VCP = Shape<NW>::VCP;  // copies per wave
   const int32_t krow0 = 4 * KCP * wave + (lane >> 4), kp = lane & 15;
   const int32_t vrow0 = 8 * VCP * wave + (lane >> 3), vp = lane & 7;
   uint32_t kswz[KCP], vlane[VCP];
@@ -495,8 +506,10 @@ __global__ __launch_bounds__(64 * NWAVES, WG_PER_CU) void attn_bf16_kernel(const
 // Merges the pieces of each tail unit, in piece order: one work-group per
 // tail unit, one thread per query row.  With m = max m_p:
 //   O = sum_p 2^(m_p - m) O_p / sum_p 2^(m_p - m) l_p.
-__global__ __launch_bounds__(BQ) void attn_combine_kernel(uint16_t* __restrict__ o, AttnGeom g,
-                                                          AttnPlan plan) {
+template <int NW>
+__global__ __launch_bounds__(Shape<NW>::BQ) void attn_combine_kernel(uint16_t* __restrict__ o, AttnGeom g,
+                                                                     AttnPlan plan) {
+  constexpr int BQ = Shape<NW>::BQ;
   const int32_t tu = blockIdx.x;
   const int32_t unit = g.whole_units + tu;
   const int32_t qt = unit % g.n_qtiles;
@@ -546,11 +559,15 @@ __global__ __launch_bounds__(BQ) void attn_combine_kernel(uint16_t* __restrict__
 // (prologue and partial write), with at most kAttnMaxPieces pieces and no
 // more pieces than the shortest node has key tiles.
 struct TailSplit {
+  int32_t nw;       // waves per work-group of the instantiation used
   int32_t whole, tail, split;
 };
+static int32_t waves_for(const sc_plan* p) { return p->nq <= Shape<4>::BQ ? 4 : 8; }
 static TailSplit tail_split(const sc_plan* p, const sc_cache* c) {
   const int32_t n = (int32_t)p->nodes.size();
-  const int32_t n_qtiles = (p->nq + BQ - 1) / BQ;
+  const int32_t nw = waves_for(p);
+  const int32_t bq = 32 * nw;
+  const int32_t n_qtiles = (p->nq + bq - 1) / bq;
   const int32_t units = n * c->d.n_heads * n_qtiles;
   int64_t tiles = 0;
   int32_t min_tiles = INT32_MAX;
@@ -562,7 +579,8 @@ static TailSplit tail_split(const sc_plan* p, const sc_cache* c) {
   }
   const double mean_tiles = (double)tiles / std::max(n, 1);
   TailSplit ts;
-  const int32_t slots = kAttnCUs * WG_PER_CU;  // work-groups resident at once
+  ts.nw = nw;
+  const int32_t slots = kAttnCUs * (8 / nw);  // work-groups resident at once
   ts.tail = units % slots;
   ts.whole = units - ts.tail;
   ts.split = 1;
@@ -584,10 +602,10 @@ size_t attention_workspace_bytes(const sc_plan* p, const sc_cache* c) {
   if (c->d.dtype != SC_DTYPE_BF16 || p->nodes.empty()) return 0;
   const TailSplit ts = tail_split(p, c);
   if (ts.split == 1) return 0;
-  return (size_t)ts.tail * ts.split * BQ * (HDB + 2) * sizeof(float);
+  return (size_t)ts.tail * ts.split * (32 * ts.nw) * (HDB + 2) * sizeof(float);
 }
 
-size_t attention_workspace_bound() { return (size_t)kAttnMaxPieces * BQ * (HDB + 2) * sizeof(float); }
+size_t attention_workspace_bound() { return (size_t)kAttnMaxPieces * BQ_MAX * (HDB + 2) * sizeof(float); }
 
 int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const void* q, void* o,
                      float scale, void* ws, size_t ws_bytes, hipStream_t stream) {
@@ -635,8 +653,9 @@ int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const v
   if (ws_bytes < need || (need && !ws))
     return fail(SC_EINVAL, "attention workspace of %zu bytes, need %zu", ws_bytes, need);
   if (reinterpret_cast<uintptr_t>(ws) & 15) return fail(SC_EINVAL, "workspace must be 16-byte aligned");
-  g.n_qtiles = (p->nq + BQ - 1) / BQ;
   const TailSplit ts = tail_split(p, c);
+  const int32_t bq = 32 * ts.nw;
+  g.n_qtiles = (p->nq + bq - 1) / bq;
   g.whole_units = ts.whole;
   g.tail_units = ts.tail;
   g.tail_split = ts.split;
@@ -645,16 +664,24 @@ int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const v
     g.tail_units = 0;
   }
   g.part_o = static_cast<float*>(ws);
-  g.part_ml = g.part_o + (size_t)g.tail_units * g.tail_split * BQ * HDB;
+  g.part_ml = g.part_o + (size_t)g.tail_units * g.tail_split * bq * HDB;
   const uint32_t items = (uint32_t)(g.whole_units + g.tail_units * g.tail_split);
+  const uint16_t* qb = static_cast<const uint16_t*>(q);
+  uint16_t* ob = static_cast<uint16_t*>(o);
   timer_begin(TK_ATTENTION, stream);
-  hipLaunchKernelGGL(attn_bf16_kernel, dim3(items), dim3(64 * NWAVES), 0, stream,
-                     static_cast<const uint16_t*>(q), static_cast<uint16_t*>(o), g, plan);
+  if (ts.nw == 4)
+    hipLaunchKernelGGL(attn_bf16_kernel<4>, dim3(items), dim3(256), 0, stream, qb, ob, g, plan);
+  else
+    hipLaunchKernelGGL(attn_bf16_kernel<8>, dim3(items), dim3(512), 0, stream, qb, ob, g, plan);
   timer_end(TK_ATTENTION, stream);
   if (g.tail_units) {
     timer_begin(TK_ATTN_COMBINE, stream);
-    hipLaunchKernelGGL(attn_combine_kernel, dim3((uint32_t)g.tail_units), dim3(BQ), 0, stream,
-                       static_cast<uint16_t*>(o), g, plan);
+    if (ts.nw == 4)
+      hipLaunchKernelGGL(attn_combine_kernel<4>, dim3((uint32_t)g.tail_units), dim3(128), 0, stream,
+                         ob, g, plan);
+    else
+      hipLaunchKernelGGL(attn_combine_kernel<8>, dim3((uint32_t)g.tail_units), dim3(256), 0, stream,
+                         ob, g, plan);
     timer_end(TK_ATTN_COMBINE, stream);
   }
   SC_HIP(hipGetLastError());

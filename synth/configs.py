@@ -50,6 +50,21 @@ SMALL = Geometry(heads=2, head_dim=128, grid_h=8, grid_w=13, frames_per_chunk=3,
                  hidden=256, mlp=512, rope_dims=(44, 42, 42))
 
 
+# Short nodes (one 96-token latent frame per chunk, 96 queries): the
+# 128-query work-group shape of the bf16 kernel, with pages that end inside
+# 64-key tiles.
+SHORT = Geometry(heads=2, head_dim=128, grid_h=8, grid_w=12, frames_per_chunk=1, K=4, W=6,
+                 hidden=256, mlp=512)
+
+
+def kv_stream(nq: int, W: int = 20) -> Geometry:
+    """Short-context K/V streaming shape: Wan heads (12 x 128), one latent
+    frame of ``nq`` tokens per chunk, up to W + 1 = 21 pages per node."""
+    grid_w = {64: 8, 128: 16}[nq]
+    return Geometry(heads=12, head_dim=128, grid_h=8, grid_w=grid_w, frames_per_chunk=1, K=4, W=W,
+                    hidden=1536, mlp=8960)
+
+
 @dataclass
 class Workload:
     name: str

@@ -16,7 +16,7 @@ from oracle.attention import node_attention
 from oracle.pipeline import pipeline_rounds
 from oracle.policy import policy as oracle_policy
 from oracle.policy import select
-from synth.configs import SMALL, TINY, WAN, cfg2_clean, cfg3_same, cfg4_prog
+from synth.configs import SHORT, SMALL, TINY, WAN, cfg2_clean, cfg3_same, cfg4_prog, kv_stream
 
 from gpu_cases import (AttnCase, BF16_MAX_ABS, F32_MAX_ABS, bf16_gates, from_device, sample_rows,
                        to_device, torch_mod)
@@ -63,6 +63,29 @@ def test_small_bf16_packs(kind, pack, resident):
     out = case.run()
     for i in range(len(pack)):
         bf16_gates(out[i], case.oracle(i), f"{kind} node {pack[i]}")
+
+
+@pytest.mark.parametrize("kind,pack,resident", SMALL_PACKS)
+def test_short_bf16_packs(kind, pack, resident):
+    """Nodes of 96 queries run on the 128-query (4-wave) work-group shape."""
+    case = AttnCase(SHORT, sc.SC_DTYPE_BF16, kind, pack, resident, seed=6)
+    out = case.run()
+    for i in range(len(pack)):
+        bf16_gates(out[i], case.oracle(i), f"short {kind} node {pack[i]}")
+
+
+@pytest.mark.parametrize("nq", [64, 128])
+def test_kv_stream_shape(nq):
+    """The short-context streaming shape (12 heads, one-frame chunks, 21
+    pages per node): three nodes with disjoint windows, every row."""
+    geo = kv_stream(nq)
+    W = geo.W
+    pack = [(21 * i + W, 4) for i in range(3)]
+    resident = [(21 * i + r, 0) for i in range(3) for r in range(W)]
+    case = AttnCase(geo, sc.SC_DTYPE_BF16, "clean", pack, resident, seed=7)
+    out = case.run()
+    for i in range(len(pack)):
+        bf16_gates(out[i], case.oracle(i), f"kv stream nq={nq} node {pack[i]}")
 
 
 def test_small_packed_matches_sequential():
