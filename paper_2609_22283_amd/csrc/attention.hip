@@ -554,10 +554,11 @@ __global__ __launch_bounds__(Shape<NW>::BQ) void attn_combine_kernel(uint16_t* _
 }
 
 // Tail split for a plan: units = heads x nodes x query tiles; the last
-// units mod 256 are cut into S pieces, S chosen to minimise the tail's rounds
-// (in units of one whole unit) plus a per-piece cost of about two key tiles
-// (prologue and partial write), with at most kAttnMaxPieces pieces and no
-// more pieces than the shortest node has key tiles.
+// (units mod resident work-groups) are cut into S pieces, S chosen to
+// minimise the tail's rounds (in units of one whole unit) plus a per-piece
+// cost of about two key tiles (prologue and partial write), with at most
+// kAttnMaxPieces pieces and no more pieces than the shortest node has key
+// tiles.
 struct TailSplit {
   int32_t nw;       // waves per work-group of the instantiation used
   int32_t whole, tail, split;
@@ -584,7 +585,10 @@ static TailSplit tail_split(const sc_plan* p, const sc_cache* c) {
   ts.tail = units % slots;
   ts.whole = units - ts.tail;
   ts.split = 1;
-  if (ts.tail == 0) return ts;
+  // Short units are not cut: the combine launch and the partial traffic are
+  // fixed costs that a few-tile unit cannot repay (measured on the short
+  // K/V streaming sweep).
+  if (ts.tail == 0 || mean_tiles < kAttnMinSplitTiles) return ts;
   double best = 1e30;
   const int32_t smax = std::max(1, std::min({16, kAttnMaxPieces / ts.tail, min_tiles}));
   for (int32_t sp = 1; sp <= smax; ++sp) {

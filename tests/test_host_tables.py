@@ -176,26 +176,29 @@ def test_stale_plan_detected_on_cpu():
 
 def test_attention_workspace_size():
     """Workspace of the bf16 attention: units (head, node, query tile) that
-    fill whole rounds of the CUs' work-group slots run whole; the remaining
-    units are cut into S pieces, each leaving a partial (one row per query of
-    the tile: 128 fp32 outputs plus max and sum).  Nodes of at most 128
-    queries use 128-query tiles (512 slots), larger ones 256-query tiles (256
-    slots).  S minimises the tail's rounds plus a per-piece cost of two key
-    tiles, within 1024 pieces and the shortest node's key tiles.  No
-    workspace for fp32 caches or when nothing is cut."""
+    fill whole rounds of the CUs' work-group slots run whole; when units are
+    long (a mean of at least 32 key tiles) the remaining units are cut into S
+    pieces, each leaving a partial (one row per query of the tile: 128 fp32
+    outputs plus max and sum).  Nodes of at most 128 queries use 128-query
+    tiles (512 slots), larger ones 256-query tiles (256 slots).  S minimises
+    the tail's rounds plus a per-piece cost of two key tiles, within 1024
+    pieces and the shortest node's key tiles.  No workspace for fp32 caches
+    or when nothing is cut."""
     row = (128 + 2) * 4
     cache = sc.sc_cache_create(0x100000, 1, 2, 128, 64, 1, 64)      # 64 queries per node
     plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(0, 0)]), cache)
     assert sc.sc_attention_workspace_bytes(plan, cache) == 0          # 1 key tile: no cut
-    sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(1, 0), (2, 0)]), cache)
-    plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 3, [(3, 4)]), cache)
-    # 2 units of 4 tiles: S = 4 (one round of quarter units + 4 x 2/4 overhead)
-    assert sc.sc_attention_workspace_bytes(plan, cache) == 2 * 4 * 128 * row
+    sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(c, 0) for c in range(1, 40)]), cache)
+    plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 3, [(40, 4)]), cache)
+    assert sc.sc_attention_workspace_bytes(plan, cache) == 0          # 4 tiles: too short to cut
+    plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 39, [(40, 4)]), cache)
+    # 2 units of 40 tiles: S = 16 (one round of sixteenths + 16 x 2/40 overhead)
+    assert sc.sc_attention_workspace_bytes(plan, cache) == 2 * 16 * 128 * row
     wide = sc.sc_cache_create(0x100000, 1, 2, 128, 160, 1, 64)      # 160 queries per node
-    sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(0, 0), (1, 0), (2, 0)]), wide)
-    plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 3, [(3, 4)]), wide)
-    # 2 units of 10 tiles: S = 10 (one round of tenths + 10 x 2/10 overhead)
-    assert sc.sc_attention_workspace_bytes(plan, wide) == 2 * 10 * 256 * row
+    sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(c, 0) for c in range(13)]), wide)
+    plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 13, [(13, 4)]), wide)
+    # 2 units of 35 tiles (14 pages x 160 keys): S = 16 (the cap)
+    assert sc.sc_attention_workspace_bytes(plan, wide) == 2 * 16 * 256 * row
     big = sc.sc_cache_create(0x100000, 1, 12, 128, 1560, 3, 64)
     sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(0, 0)]), big)
     plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 1, [(1, 4)]), big)
