@@ -270,8 +270,8 @@ int sc_timer_read(const char* kind, int32_t* launches, double* total_ms);
  * registers (two 8-wave work-groups per CU, `iters` rounds of 16 MFMAs per
  * wave) and sets *flops to the work it performs; the caller times it with
  * its own events.  random_operands != 0 fills the operands with random bf16
- * values (the sustained rate for data like the attention's; power limits
- * the clock), else with constants.  out: device scratch of at least
+ * values, else with constants; the two rates show how much the
+ * power-limited clock depends on the data.  out: device scratch of at least
  * sc_probe_mfma_out_bytes() bytes (one float per thread, written so the
  * work is not optimised away).  Errors: SC_EINVAL, SC_EDEVICE. */
 size_t sc_probe_mfma_out_bytes(void);

@@ -1,10 +1,9 @@
 // Matrix-core ceiling probe (measurement support, not part of the method).
 // A grid of 8-wave work-groups, two per CU, issues back-to-back
 // 32x32x16 bf16 MFMAs on four accumulator chains with operands held in
-// registers: no memory traffic, no vector-ALU work.  With random operands
-// the sustained rate shows the matrix cores' power-limited throughput for
-// data like the attention's; constant operands toggle few bits and run at a
-// higher clock.
+// registers: no memory traffic, no vector-ALU work.  Random operands toggle
+// many bits and draw more power than constant ones; the two sustained rates
+// show how far the power-limited clock moves with the data.
 #include "device.h"
 #include "internal.h"
 
