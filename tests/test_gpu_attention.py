@@ -8,6 +8,8 @@ progressive packs on sampled rows, the segment probe, negative controls
 unused slots, packed vs sequential, run-to-run determinism and the workspace
 check.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -213,3 +215,29 @@ def test_wan_segment_probe_prog():
             np.testing.assert_allclose(got[:, :, k], want[:, :, k], atol=2e-3)
             if st not in chosen:
                 assert np.all(out[i][:, :, k] == 0.0), (wl.pack[i], st)
+
+
+def test_max_nodes_and_pages():
+    """Pack limits of the attention kernel's plan arguments: 64 nodes run
+    (the first, a middle and the last node checked against the oracle); a
+    65th node, or more than 800 pages in one plan, is refused with
+    SC_EUNSUPPORTED before any launch."""
+    geo1 = dataclasses.replace(SHORT, W=1)
+    pack = [(2 * i + 1, 4) for i in range(64)]
+    resident = [(2 * i, 0) for i in range(64)]
+    case = AttnCase(geo1, sc.SC_DTYPE_BF16, "clean", pack, resident, seed=8)
+    out = case.run()
+    for i in (0, 31, 63):
+        bf16_gates(out[i], case.oracle(i), f"64-node pack node {pack[i]}")
+    big = AttnCase(geo1, sc.SC_DTYPE_BF16, "clean", [(2 * i + 1, 4) for i in range(65)],
+                   [(2 * i, 0) for i in range(65)], seed=8)
+    with pytest.raises(sc.ScError) as e:
+        big.run()
+    assert e.value.code == sc.SC_EUNSUPPORTED
+    # 64 nodes x 13 pages = 832 pages > 800
+    geo12 = dataclasses.replace(SHORT, W=12)
+    wide = AttnCase(geo12, sc.SC_DTYPE_BF16, "clean", [(12 + 13 * i, 4) for i in range(64)],
+                    [(13 * i + r, 0) for i in range(64) for r in range(12)], seed=8)
+    with pytest.raises(sc.ScError) as e:
+        wide.run()
+    assert e.value.code == sc.SC_EUNSUPPORTED

@@ -24,7 +24,7 @@ from oracle.policy import select
 from oracle.rope import chunk_positions, rope
 from synth import (TAG_K, TAG_NOISE, TAG_V, TAG_W_DOWN, TAG_W_O, TAG_W_QKV, TAG_W_UP, TAG_X,
                    normal, normal_parallel)
-from synth.configs import SMALL, WAN, cfg4_prog
+from synth.configs import SHORT, SMALL, WAN, cfg4_prog
 
 from gpu_cases import bf16_gates, from_device, sample_rows, to_device, torch_mod
 
@@ -182,6 +182,28 @@ def test_small_block(kind, pack, resident):
     with pytest.raises(sc.ScError) as e:                      # K/V of the pack already written
         case.run()
     assert e.value.code == sc.SC_EEXIST
+
+
+def test_short_block_prog():
+    """A progressive pack of one-frame, 96-token chunks (the attention's
+    128-query work-group shape inside the block)."""
+    pack = [(6, 0), (7, 1), (8, 2), (9, 3), (10, 4)]
+    case = BlockCase(SHORT, "prog", pack, [(c, 0) for c in range(6)], seed=13)
+    got = case.run()
+    want, _ = case.oracle()
+    for i in range(len(pack)):
+        block_gate(got[i], want[i], f"short node {pack[i]}")
+
+
+def test_block_rejects_oversized_pack():
+    """More pack nodes than the QKV epilogue's node table holds (64) is
+    refused before any launch, leaving the pack's pages unwritten."""
+    import dataclasses
+    geo = dataclasses.replace(SHORT, W=0)                    # each node reads only itself
+    case = BlockCase(geo, "clean", [(c, 4) for c in range(65)], [], seed=14)
+    with pytest.raises(sc.ScError) as e:
+        case.run()
+    assert e.value.code == sc.SC_EUNSUPPORTED
 
 
 def test_wan_block_prog_sampled_rows():

@@ -206,3 +206,14 @@ def test_attention_workspace_size():
     f32 = sc.sc_cache_create(0x100000, 1, 2, 64, 16, 1, 8, sc.SC_DTYPE_F32)
     plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(0, 0)]), f32)
     assert sc.sc_attention_workspace_bytes(plan, f32) == 0
+
+
+def test_empty_pack_is_a_no_op():
+    """An empty pack selects nothing, plans nothing and launches nothing."""
+    sel = sc.sc_selection_build("prog", 4, 6, [])
+    cache = _host_cache(8, 1)
+    plan = sc.sc_plan_build(sel, cache)
+    assert plan.tables() == ([0], [], [], [])
+    sc.sc_attention(plan, cache, 0, 0x1000, 0x2000, 0.125)
+    assert sc.sc_attention_workspace_bytes(plan, cache) == 0
+    assert cache.free_slot_count() == 8
