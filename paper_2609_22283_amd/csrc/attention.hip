@@ -364,27 +364,39 @@ __global__ __launch_bounds__(64 * NW, Shape<NW>::WG_PER_CU) void attn_bf16_kerne
     vkey[j] = 8 * (vp ^ ((d >> 1) & 7));                           // key offset in tile
     vlane[j] = (uint32_t)d * g.tpp * 2 + (uint32_t)vkey[j] * 2;    // plus t0 * 2
   }
+  // Page slots of a tile's keys (two scalar loads from the plan), fetched
+  // one step before the copy that uses them so their latency overlaps the
+  // step in between.  A 64-key tile spans at most two pages.
+  struct Slots {
+    uint32_t lo, hi;  // byte offsets of the slots of the tile's first page and the next one
+    int32_t plo;      // index of the tile's first page within the node
+  };
+  auto slots = [&](int32_t tile) {
+    const int32_t t0 = min(tile, it.ntiles - 1) * BK;  // clamped: prefetches past the end are unused
+    Slots sl;
+    sl.plo = (int32_t)fast_div((uint32_t)t0, g.tpp_div);
+    const int32_t phi = sl.plo + 1 < npages ? sl.plo + 1 : sl.plo;
+    sl.lo = (uint32_t)plan.page_slot[p0 + sl.plo] * (uint32_t)g.slot_bytes;
+    sl.hi = (uint32_t)plan.page_slot[p0 + phi] * (uint32_t)g.slot_bytes;
+    return sl;
+  };
   struct PageSplit {
     uint32_t lo, hi;  // layer-relative byte offset of key t0 on page lo / hi (head included)
     int32_t split;    // tile-relative first key on page hi
   };
-  auto pages = [&](int32_t t0, uint32_t head_off, uint32_t row_bytes) {
-    const int32_t plo = (int32_t)fast_div((uint32_t)t0, g.tpp_div);
-    const int32_t bkey = (plo + 1) * g.tpp;
-    const int32_t phi = plo + 1 < npages ? plo + 1 : plo;
-    const uint32_t slo = (uint32_t)plan.page_slot[p0 + plo] * (uint32_t)g.slot_bytes;
-    const uint32_t shi = (uint32_t)plan.page_slot[p0 + phi] * (uint32_t)g.slot_bytes;
+  auto pages = [&](const Slots& sl, int32_t t0, uint32_t head_off, uint32_t row_bytes) {
+    const int32_t bkey = (sl.plo + 1) * g.tpp;
     PageSplit ps;
-    ps.lo = slo + head_off - (uint32_t)plo * g.tpp * row_bytes + (uint32_t)t0 * row_bytes;
-    ps.hi = shi + head_off - (uint32_t)bkey * row_bytes + (uint32_t)t0 * row_bytes;
+    ps.lo = sl.lo + head_off - (uint32_t)sl.plo * g.tpp * row_bytes + (uint32_t)t0 * row_bytes;
+    ps.hi = sl.hi + head_off - (uint32_t)bkey * row_bytes + (uint32_t)t0 * row_bytes;
     ps.split = bkey - t0;
     return ps;
   };
   // Keys past the node's end (ragged last tile) fetch the tile's first key
   // instead: valid memory, and its probability is masked to zero anyway.
-  auto copy_k = [&](int32_t tile, int buf) {
+  auto copy_k = [&](int32_t tile, int buf, const Slots& sl) {
     const int32_t t0 = tile * BK;
-    const PageSplit ps = pages(t0, khead, 256);
+    const PageSplit ps = pages(sl, t0, khead, 256);
     const int32_t lim = nk - t0;
     char* kl = smem + buf * KT_BYTES;
 #pragma unroll
@@ -396,9 +408,9 @@ __global__ __launch_bounds__(64 * NW, Shape<NW>::WG_PER_CU) void attn_bf16_kerne
       dma16(lbase + (base + lo), kl + (4 * KCP * wave + 4 * j) * 256);
     }
   };
-  auto copy_v = [&](int32_t tile, int buf) {
+  auto copy_v = [&](int32_t tile, int buf, const Slots& sl) {
     const int32_t t0 = tile * BK;
-    const PageSplit ps = pages(t0, vhead, 2);
+    const PageSplit ps = pages(sl, t0, vhead, 2);
     const int32_t lim = nk - t0;
     char* vl = smem + 2 * KT_BYTES + buf * VT_BYTES;
 #pragma unroll
@@ -420,9 +432,12 @@ __global__ __launch_bounds__(64 * NW, Shape<NW>::WG_PER_CU) void attn_bf16_kerne
   for (int db = 0; db < 4; ++db) oacc[db] = f32x16{};
   float m_run = 0.f, l_run = 0.f;
   // prologue: K(ta), V(ta), K(ta+1) in flight; S(ta) = K(ta) Q^T; m = its exact max
-  copy_k(ta, 0);
-  copy_v(ta, 0);
-  if (ta + 1 < ntiles) copy_k(ta + 1, 1);
+  {
+    const Slots s0 = slots(ta);
+    copy_k(ta, 0, s0);
+    copy_v(ta, 0, s0);
+    if (ta + 1 < ntiles) copy_k(ta + 1, 1, slots(ta + 1));
+  }
   landed();
   f32x16 s[2];
   qk_tile(smem, L, qreg, s, 0.f);
@@ -443,18 +458,23 @@ __global__ __launch_bounds__(64 * NW, Shape<NW>::WG_PER_CU) void attn_bf16_kerne
   // iteration t (buffer parity counted from ta): copy K(t+2) over K(t) and
   // V(t+1) over V(t-1), then step t
   int32_t t = ta;
+  Slots sk = slots(ta + 2), sv = slots(ta + 1);  // for the next copies of K and V
   for (; t + 2 < ntiles; t += 2) {
-    copy_k(t + 2, 0);
-    copy_v(t + 1, 1);
+    copy_k(t + 2, 0, sk);
+    copy_v(t + 1, 1, sv);
+    sk = slots(t + 3);
+    sv = slots(t + 2);
     attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
     landed();
-    if (t + 3 < ntiles) copy_k(t + 3, 1);
-    copy_v(t + 2, 0);
+    if (t + 3 < ntiles) copy_k(t + 3, 1, sk);
+    copy_v(t + 2, 0, sv);
+    sk = slots(t + 4);
+    sv = slots(t + 3);
     attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m_run, l_run, (t + 1) * BK, nk, hl);
     landed();
   }
   if (t + 1 < ntiles) {  // two tiles left, parity 0
-    copy_v(t + 1, 1);
+    copy_v(t + 1, 1, sv);
     attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
     landed();
     ++t;
