@@ -11,9 +11,8 @@ namespace sc {
 
 // cos/sin of pos * theta^(-2 i / dim_a) for every (position, pair) of the
 // three axes, computed in double and stored as fp32 (cos, sin).
-__global__ void rope_table_kernel(float2* table, int32_t max_frames, int32_t grid_h, int32_t grid_w,
-                                  int32_t pt, int32_t ph, int32_t pw, int64_t off_h, int64_t off_w,
-                                  int64_t total, float theta) {
+__global__ void rope_table_kernel(float2* table, int32_t pt, int32_t ph, int32_t pw, int64_t off_h,
+                                  int64_t off_w, int64_t total, float theta) {
   int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= total) return;
   int32_t pos, i, dim;
@@ -35,8 +34,8 @@ int launch_rope_table(const sc_rope_desc* d, void* table, hipStream_t stream) {
   const int threads = 256;
   const int64_t blocks = (L.total + threads - 1) / threads;
   hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)blocks), dim3(threads), 0, stream,
-                     static_cast<float2*>(table), d->max_frames, d->grid_h, d->grid_w, L.pairs_t,
-                     L.pairs_h, L.pairs_w, L.off_h, L.off_w, L.total, d->theta);
+                     static_cast<float2*>(table), L.pairs_t, L.pairs_h, L.pairs_w, L.off_h, L.off_w,
+                     L.total, d->theta);
   SC_HIP(hipGetLastError());
   return SC_OK;
 }

@@ -51,7 +51,10 @@ void timer_begin(int kind, hipStream_t stream) {
   if (!g_timer.on) return;
   hipEvent_t e = take_event();
   if (!e) return;
-  hipEventRecord(e, stream);
+  if (hipEventRecord(e, stream) != hipSuccess) {  // an unrecorded launch is not timed
+    g_timer.pool.push_back(e);
+    return;
+  }
   g_timer.open_kind = kind;
   g_timer.open_start = e;
 }
@@ -60,7 +63,10 @@ void timer_end(int kind, hipStream_t stream) {
   if (!g_timer.on || g_timer.open_kind != kind || !g_timer.open_start) return;
   hipEvent_t e = take_event();
   if (!e) return;
-  hipEventRecord(e, stream);
+  if (hipEventRecord(e, stream) != hipSuccess) {
+    g_timer.pool.push_back(e);
+    return;
+  }
   g_timer.records.push_back(Record{kind, g_timer.open_start, e});
   g_timer.open_kind = -1;
   g_timer.open_start = nullptr;
