@@ -32,7 +32,7 @@
 extern "C" {
 #endif
 
-#define SC_ABI_VERSION 2
+#define SC_ABI_VERSION 3
 
 enum {
   SC_OK = 0,
@@ -63,13 +63,18 @@ typedef struct {
  *   SC_POLICY_SAME   phi = j
  *   SC_POLICY_PROG   phi = max(j - r, 0)
  *   SC_POLICY_TABLE  phi = phi_table[j*W + r-1]   (entries in [0, K])
- * The arrays are read during sc_selection_build only. */
+ * Position-dependent policies (Eq. 4's Phi_b and R_b,j may depend on the
+ * chunk): with n_chunks > 0 the tables gain a leading chunk index --
+ * phi_table[(c*(K+1) + j)*W + r-1] and r_mask[(c*(K+1) + j)*W + r-1] -- and
+ * every node must have c < n_chunks.  The arrays are read during the call
+ * only (sc_selection_build, sc_cache_release_unread). */
 typedef struct {
   int32_t kind;
   int32_t K;                 /* number of noise levels above clean, >= 1 */
   int32_t W;                 /* history window in chunks, >= 0           */
-  const int8_t* phi_table;   /* (K+1) x W, kind TABLE only, else NULL    */
-  const uint8_t* r_mask;     /* (K+1) x W or NULL (dense offsets)        */
+  const int8_t* phi_table;   /* [n_chunks x] (K+1) x W, kind TABLE only, else NULL */
+  const uint8_t* r_mask;     /* [n_chunks x] (K+1) x W, or NULL (dense offsets)    */
+  int32_t n_chunks;          /* 0: tables independent of the chunk          */
 } sc_policy;
 
 typedef struct sc_selection sc_selection;
@@ -87,8 +92,9 @@ const char* sc_status_name(int status);
  * its own tokens (Eq. 6 text: within-chunk attention is bidirectional).
  * seg_src[s] is the index of the pack node that produces state s in this
  * pack (in-pack history, or the node itself), else -1 (must be cached).
- * Errors: SC_EINVAL for K < 1, W < 0, an unknown kind, a phi entry outside
- * [0, K], a node with chunk < 0 or level outside [0, K], or a duplicate node.
+ * Errors: SC_EINVAL for K < 1, W < 0, n_chunks < 0, an unknown kind, a phi
+ * entry outside [0, K], a node with chunk < 0 (or >= n_chunks when
+ * n_chunks > 0) or level outside [0, K], or a duplicate node.
  * The returned handle owns every array; free it with sc_selection_free. */
 int sc_selection_build(const sc_policy* policy, const sc_node* nodes, int32_t n,
                        sc_selection** out);

@@ -11,8 +11,9 @@ the state at level phi(j, r).  The three policies of Eq. 5:
     same   phi(j, r) = j
     prog   phi(j, r) = max(j - r, 0)
 
-A fourth kind, ``table``, takes phi from a user table (the general
-position-independent policy of Eq. 4).  Each node also sees its own chunk at
+A fourth kind, ``table``, takes phi from a user table.  Eq. 4 lets the
+policy and the offset set depend on the chunk (Phi_b, R_b,j): with
+``n_chunks`` > 0 the tables are indexed [c][j][r - 1].  Each node also sees its own chunk at
 its own level (the query chunk's own features, Eq. 6 text; attention inside a
 chunk is bidirectional).
 
@@ -37,24 +38,28 @@ class Policy:
     kind: int
     K: int
     W: int
-    phi_table: Optional[Sequence[Sequence[int]]] = None  # [K+1][W], kind TABLE
-    r_mask: Optional[Sequence[Sequence[int]]] = None      # [K+1][W], None = dense
+    phi_table: Optional[Sequence] = None  # [K+1][W] (or [n_chunks][K+1][W]), kind TABLE
+    r_mask: Optional[Sequence] = None     # [K+1][W] (or [n_chunks][K+1][W]), None = dense
+    n_chunks: int = 0                     # > 0: tables depend on the chunk (Phi_b of Eq. 4)
 
-    def phi(self, j: int, r: int) -> int:
-        """Level selected from chunk c - r for a node at level j (Eq. 5)."""
+    def _entry(self, table, c: int, j: int, r: int):
+        return table[c][j][r - 1] if self.n_chunks > 0 else table[j][r - 1]
+
+    def phi(self, j: int, r: int, c: int = 0) -> int:
+        """Level selected from chunk c - r for a node (c, j) (Eq. 4-5)."""
         if self.kind == CLEAN:
             return 0
         if self.kind == SAME:
             return j
         if self.kind == PROG:
             return max(j - r, 0)
-        return int(self.phi_table[j][r - 1])
+        return int(self._entry(self.phi_table, c, j, r))
 
-    def selected(self, j: int, r: int) -> bool:
-        """Whether offset r is in R for level j (Eq. 4)."""
+    def selected(self, j: int, r: int, c: int = 0) -> bool:
+        """Whether offset r is in R_b,j for node (c, j) (Eq. 4)."""
         if self.r_mask is None:
             return True
-        return bool(self.r_mask[j][r - 1])
+        return bool(self._entry(self.r_mask, c, j, r))
 
 
 def policy(name: str, K: int, W: int, **kw) -> Policy:
@@ -87,21 +92,28 @@ class Selection:
 def _validate(pol: Policy, nodes: Sequence[Tuple[int, int]]) -> None:
     if pol.kind not in (CLEAN, SAME, PROG, TABLE):
         raise SelectionError("unknown policy kind")
-    if pol.K < 1 or pol.W < 0:
-        raise SelectionError("K must be >= 1 and W >= 0")
+    if pol.K < 1 or pol.W < 0 or pol.n_chunks < 0:
+        raise SelectionError("K must be >= 1, W >= 0 and n_chunks >= 0")
+
+    def check_shape(table, what, entries_ok):
+        per_chunk = list(table) if pol.n_chunks > 0 else [table]
+        if pol.n_chunks > 0 and len(per_chunk) != pol.n_chunks:
+            raise SelectionError(f"{what} needs n_chunks x (K+1) x W entries")
+        for t in per_chunk:
+            if len(t) != pol.K + 1 or any(len(row) != pol.W for row in t):
+                raise SelectionError(f"{what} must be (K+1) x W per chunk")
+            if any(not entries_ok(int(v)) for row in t for v in row):
+                raise SelectionError(f"{what} entries out of range")
     if pol.kind == TABLE:
-        if pol.phi_table is None or len(pol.phi_table) != pol.K + 1:
-            raise SelectionError("table policy needs a (K+1) x W phi table")
-        for row in pol.phi_table:
-            if len(row) != pol.W or any(not (0 <= int(v) <= pol.K) for v in row):
-                raise SelectionError("phi table entries must lie in [0, K]")
+        if pol.phi_table is None:
+            raise SelectionError("table policy needs a phi table")
+        check_shape(pol.phi_table, "phi table", lambda v: 0 <= v <= pol.K)
     if pol.r_mask is not None:
-        if len(pol.r_mask) != pol.K + 1 or any(len(row) != pol.W for row in pol.r_mask):
-            raise SelectionError("r_mask must be (K+1) x W")
+        check_shape(pol.r_mask, "r_mask", lambda v: True)
     seen = set()
     for c, j in nodes:
-        if c < 0 or not (0 <= j <= pol.K):
-            raise SelectionError("node chunk must be >= 0 and level in [0, K]")
+        if c < 0 or (pol.n_chunks > 0 and c >= pol.n_chunks) or not (0 <= j <= pol.K):
+            raise SelectionError("node chunk must be in [0, n_chunks) and level in [0, K]")
         if (c, j) in seen:
             raise SelectionError("duplicate node in pack")
         seen.add((c, j))
@@ -117,8 +129,8 @@ def select(pol: Policy, nodes: Sequence[Tuple[int, int]]) -> Selection:
     for i, (c, j) in enumerate(nodes):
         segs = []
         for r in range(min(pol.W, c), 0, -1):          # oldest history first
-            if pol.selected(j, r):
-                segs.append((c - r, pol.phi(j, r)))
+            if pol.selected(j, r, c):
+                segs.append((c - r, pol.phi(j, r, c)))
         segs.append((c, j))                             # own chunk, own level
         for (sc, sl) in segs:
             sel.seg_chunk.append(sc)

@@ -74,7 +74,8 @@ class sc_node(C.Structure):
 
 class sc_policy(C.Structure):
     _fields_ = [("kind", C.c_int32), ("K", C.c_int32), ("W", C.c_int32),
-                ("phi_table", C.POINTER(C.c_int8)), ("r_mask", C.POINTER(C.c_uint8))]
+                ("phi_table", C.POINTER(C.c_int8)), ("r_mask", C.POINTER(C.c_uint8)),
+                ("n_chunks", C.c_int32)]
 
 
 class sc_cache_desc(C.Structure):
@@ -142,7 +143,7 @@ _SIG = {
                                    C.POINTER(sc_rope), _P, C.c_size_t, _P]),
 }
 # ABI version this binding marshals for (SC_ABI_VERSION of the header)
-ABI_VERSION = 2
+ABI_VERSION = 3
 if not hasattr(lib, "sc_abi_version") or lib.sc_abi_version() != ABI_VERSION:
     raise ImportError(f"{library_path} does not implement ABI version {ABI_VERSION}; rebuild it "
                       "(__graft_entry__.build())")
@@ -217,18 +218,27 @@ class Selection:
         return states, rows
 
 
-def _policy_struct(kind, K, W, phi_table=None, r_mask=None):
+def _flatten(t):
+    """Nested [c][j][r] or [j][r] table -> flat list (row-major)."""
+    if isinstance(t, (list, tuple)) and t and isinstance(t[0], (list, tuple)):
+        return [v for row in t for v in _flatten(row)]
+    return [int(v) for v in t]
+
+
+def _policy_struct(kind, K, W, phi_table=None, r_mask=None, n_chunks=0):
+    """phi_table / r_mask: [K+1][W], or [n_chunks][K+1][W] when n_chunks > 0
+    (position-dependent policy)."""
     pol = sc_policy()
     pol.kind = POLICY_KINDS[kind] if isinstance(kind, str) else int(kind)
-    pol.K, pol.W = int(K), int(W)
+    pol.K, pol.W, pol.n_chunks = int(K), int(W), int(n_chunks)
     keep = []
     if phi_table is not None:
-        flat = [int(v) for row in phi_table for v in row]
+        flat = _flatten(phi_table)
         buf = (C.c_int8 * max(1, len(flat)))(*flat)
         keep.append(buf)
         pol.phi_table = C.cast(buf, C.POINTER(C.c_int8))
     if r_mask is not None:
-        flat = [int(v) for row in r_mask for v in row]
+        flat = _flatten(r_mask)
         buf = (C.c_uint8 * max(1, len(flat)))(*flat)
         keep.append(buf)
         pol.r_mask = C.cast(buf, C.POINTER(C.c_uint8))
@@ -236,8 +246,8 @@ def _policy_struct(kind, K, W, phi_table=None, r_mask=None):
 
 
 def sc_selection_build(kind, K, W, nodes: Sequence[Tuple[int, int]], phi_table=None,
-                       r_mask=None) -> Selection:
-    pol, keep = _policy_struct(kind, K, W, phi_table, r_mask)
+                       r_mask=None, n_chunks=0) -> Selection:
+    pol, keep = _policy_struct(kind, K, W, phi_table, r_mask, n_chunks)
     arr = (sc_node * max(1, len(nodes)))(*[sc_node(int(c), int(j)) for c, j in nodes])
     out = C.c_void_p()
     _check(lib.sc_selection_build(C.byref(pol), arr, len(nodes), C.byref(out)))
@@ -426,9 +436,10 @@ def sc_pipeline_round_nodes(K: int, B: int, refresh: bool, n: int):
     return [(buf[i].chunk, buf[i].level) for i in range(m.value)]
 
 
-def sc_cache_release_unread(cache: "Cache", kind, K, W, future, phi_table=None, r_mask=None) -> int:
+def sc_cache_release_unread(cache: "Cache", kind, K, W, future, phi_table=None, r_mask=None,
+                            n_chunks=0) -> int:
     """Release every cached state none of the future nodes reads; returns the count."""
-    pol, keep = _policy_struct(kind, K, W, phi_table, r_mask)
+    pol, keep = _policy_struct(kind, K, W, phi_table, r_mask, n_chunks)
     arr = (sc_node * max(1, len(future)))(*[sc_node(int(c), int(j)) for c, j in future])
     n = _check(lib.sc_cache_release_unread(cache.handle, C.byref(pol), arr, len(future)))
     del keep

@@ -45,6 +45,40 @@ int plan_check(const sc_plan* plan, const sc_cache* cache, int32_t layer) {
   return SC_OK;
 }
 
+int policy_check(const sc_policy* p) {
+  if (p->kind < SC_POLICY_CLEAN || p->kind > SC_POLICY_TABLE)
+    return fail(SC_EINVAL, "unknown policy kind %d", p->kind);
+  if (p->K < 1 || p->W < 0 || p->n_chunks < 0)
+    return fail(SC_EINVAL, "need K >= 1, W >= 0, n_chunks >= 0 (K=%d W=%d n_chunks=%d)", p->K, p->W,
+                p->n_chunks);
+  if (p->kind == SC_POLICY_TABLE && p->W > 0) {
+    if (!p->phi_table) return fail(SC_EINVAL, "table policy without phi table");
+    const int64_t n = (int64_t)std::max(p->n_chunks, 1) * (p->K + 1) * p->W;
+    for (int64_t i = 0; i < n; ++i)
+      if (p->phi_table[i] < 0 || p->phi_table[i] > p->K)
+        return fail(SC_EINVAL, "phi table entry %d outside [0, K]", (int)p->phi_table[i]);
+  }
+  return SC_OK;
+}
+
+static int64_t policy_index(const sc_policy* p, int32_t c, int32_t j, int32_t r) {
+  const int64_t row = p->n_chunks > 0 ? (int64_t)c * (p->K + 1) + j : j;
+  return row * p->W + (r - 1);
+}
+
+bool policy_selects(const sc_policy* p, int32_t c, int32_t j, int32_t r) {
+  return !p->r_mask || p->r_mask[policy_index(p, c, j, r)] != 0;
+}
+
+int32_t policy_level(const sc_policy* p, int32_t c, int32_t j, int32_t r) {
+  switch (p->kind) {
+    case SC_POLICY_CLEAN: return 0;
+    case SC_POLICY_SAME: return j;
+    case SC_POLICY_PROG: return j - r > 0 ? j - r : 0;
+    default: return p->phi_table[policy_index(p, c, j, r)];
+  }
+}
+
 RopeLayout rope_layout(const sc_rope_desc* d) {
   RopeLayout L;
   L.pairs_t = d->dim_t / 2;
@@ -84,31 +118,16 @@ const char* sc_status_name(int status) {
 
 // ---------------------------------------------------------------- selection
 
-static int policy_level(const sc_policy* p, int32_t j, int32_t r) {
-  switch (p->kind) {
-    case SC_POLICY_CLEAN: return 0;
-    case SC_POLICY_SAME: return j;
-    case SC_POLICY_PROG: return j - r > 0 ? j - r : 0;
-    default: return p->phi_table[j * p->W + (r - 1)];
-  }
-}
-
 int sc_selection_build(const sc_policy* p, const sc_node* nodes, int32_t n, sc_selection** out) {
   if (!p || !out || n < 0 || (n > 0 && !nodes)) return fail(SC_EINVAL, "null argument");
   *out = nullptr;
-  if (p->kind < SC_POLICY_CLEAN || p->kind > SC_POLICY_TABLE)
-    return fail(SC_EINVAL, "unknown policy kind %d", p->kind);
-  if (p->K < 1 || p->W < 0) return fail(SC_EINVAL, "need K >= 1 and W >= 0 (K=%d W=%d)", p->K, p->W);
-  if (p->kind == SC_POLICY_TABLE) {
-    if (!p->phi_table && p->W > 0) return fail(SC_EINVAL, "table policy without phi table");
-    for (int32_t i = 0; i < (p->K + 1) * p->W; ++i)
-      if (p->phi_table[i] < 0 || p->phi_table[i] > p->K)
-        return fail(SC_EINVAL, "phi table entry %d outside [0, K]", (int)p->phi_table[i]);
-  }
+  int rc = policy_check(p);
+  if (rc != SC_OK) return rc;
   std::map<StateKey, int32_t> index_of;
   for (int32_t i = 0; i < n; ++i) {
-    if (nodes[i].chunk < 0 || nodes[i].level < 0 || nodes[i].level > p->K)
-      return fail(SC_EINVAL, "node %d = (%d,%d) outside chunk >= 0, level in [0, K]", i,
+    if (nodes[i].chunk < 0 || (p->n_chunks > 0 && nodes[i].chunk >= p->n_chunks) ||
+        nodes[i].level < 0 || nodes[i].level > p->K)
+      return fail(SC_EINVAL, "node %d = (%d,%d) outside chunk in [0, n_chunks), level in [0, K]", i,
                   nodes[i].chunk, nodes[i].level);
     if (!index_of.emplace(StateKey(nodes[i].chunk, nodes[i].level), i).second)
       return fail(SC_EINVAL, "duplicate node (%d,%d)", nodes[i].chunk, nodes[i].level);
@@ -129,8 +148,8 @@ int sc_selection_build(const sc_policy* p, const sc_node* nodes, int32_t n, sc_s
     const int32_t c = nodes[i].chunk, j = nodes[i].level;
     const int32_t rmax = std::min(p->W, c);
     for (int32_t r = rmax; r >= 1; --r) {  // oldest history chunk first
-      if (p->r_mask && !p->r_mask[j * p->W + (r - 1)]) continue;
-      emit(c - r, policy_level(p, j, r));
+      if (!policy_selects(p, c, j, r)) continue;
+      emit(c - r, policy_level(p, c, j, r));
     }
     emit(c, j);  // the node's own chunk at its own level
     s->seg_off.push_back((int32_t)s->seg_chunk.size());

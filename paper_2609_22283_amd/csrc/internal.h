@@ -67,6 +67,13 @@ namespace sc {
 // written flags).  Returns SC_OK or an error code with the message set.
 int plan_check(const sc_plan* plan, const sc_cache* cache, int32_t layer);
 
+// Policy helpers shared by the selection builder and the release rule:
+// validation (SC_OK or SC_EINVAL with the message set), whether offset r is
+// selected for node (c, j), and the level it reads (Eq. 4-5).
+int policy_check(const sc_policy* p);
+bool policy_selects(const sc_policy* p, int32_t c, int32_t j, int32_t r);
+int32_t policy_level(const sc_policy* p, int32_t c, int32_t j, int32_t r);
+
 // Kernel launchers (device code lives in the .hip files).
 int launch_attention(const sc_plan* plan, const sc_cache* cache, int32_t layer,
                      const void* q, void* o, float scale, void* ws, size_t ws_bytes,

@@ -26,35 +26,24 @@ extern "C" int sc_pipeline_round_nodes(int32_t K, int32_t B, int32_t refresh, in
   return SC_OK;
 }
 
-static int read_level(const sc_policy* p, int32_t j, int32_t r) {
-  switch (p->kind) {
-    case SC_POLICY_CLEAN: return 0;
-    case SC_POLICY_SAME: return j;
-    case SC_POLICY_PROG: return j - r > 0 ? j - r : 0;
-    default: return p->phi_table[j * p->W + (r - 1)];
-  }
-}
-
 extern "C" int sc_cache_release_unread(sc_cache* c, const sc_policy* p, const sc_node* future,
                                        int32_t n_future) {
   if (!c || !p || (n_future > 0 && !future)) return fail(SC_EINVAL, "null argument");
-  if (p->K < 1 || p->W < 0 || p->kind < SC_POLICY_CLEAN || p->kind > SC_POLICY_TABLE ||
-      (p->kind == SC_POLICY_TABLE && p->W > 0 && !p->phi_table))
-    return fail(SC_EINVAL, "bad policy");
+  int rc = policy_check(p);
+  if (rc != SC_OK) return rc;
   std::set<StateKey> needed;
   for (int32_t i = 0; i < n_future; ++i) {
     const int32_t cc = future[i].chunk, j = future[i].level;
-    if (cc < 0 || j < 0 || j > p->K) return fail(SC_EINVAL, "bad future node (%d,%d)", cc, j);
-    for (int32_t r = 1; r <= p->W && r <= cc; ++r) {
-      if (p->r_mask && !p->r_mask[j * p->W + (r - 1)]) continue;
-      needed.insert(StateKey(cc - r, read_level(p, j, r)));
-    }
+    if (cc < 0 || (p->n_chunks > 0 && cc >= p->n_chunks) || j < 0 || j > p->K)
+      return fail(SC_EINVAL, "bad future node (%d,%d)", cc, j);
+    for (int32_t r = 1; r <= p->W && r <= cc; ++r)
+      if (policy_selects(p, cc, j, r)) needed.insert(StateKey(cc - r, policy_level(p, cc, j, r)));
   }
   std::vector<StateKey> drop;
   for (const auto& kv : c->states)
     if (!needed.count(kv.first)) drop.push_back(kv.first);
   for (const auto& k : drop) {
-    int rc = sc_cache_release(c, sc_node{k.first, k.second});
+    rc = sc_cache_release(c, sc_node{k.first, k.second});
     if (rc != SC_OK) return rc;
   }
   return (int)drop.size();

@@ -51,9 +51,10 @@ class AttnCase:
     unreserved slots are NaN, so a stray page read shows up in the output)."""
 
     def __init__(self, geo, dtype, kind, pack, resident, seed=0, n_slots=None, value_fn=None,
-                 n_layers=1, layer=0):
+                 n_layers=1, layer=0, policy_kw=None):
         torch = torch_mod()
         self.geo, self.dtype, self.kind, self.pack, self.seed = geo, dtype, kind, list(pack), seed
+        self.policy_kw = dict(policy_kw or {})  # phi_table / r_mask / n_chunks
         self.layer = layer
         ppc, tpp = geo.frames_per_chunk, geo.tokens_per_page
         states = list(dict.fromkeys(list(resident) + list(pack)))
@@ -69,7 +70,7 @@ class AttnCase:
         self._dev = []
         for st in resident:
             self._append(st, gen, shape, value_fn)
-        self.sel = sc.sc_selection_build(kind, geo.K, geo.W, self.pack)
+        self.sel = sc.sc_selection_build(kind, geo.K, geo.W, self.pack, **self.policy_kw)
         self.plan = sc.sc_plan_build(self.sel, self.cache)
         for st in self.pack:
             if st not in self.kv:
@@ -108,7 +109,7 @@ class AttnCase:
 
     def oracle(self, i, rows=None, segments=None):
         segs = segments if segments is not None else select(
-            oracle_policy(self.kind, self.geo.K, self.geo.W), self.pack).segments(i)
+            oracle_policy(self.kind, self.geo.K, self.geo.W, **self.policy_kw), self.pack).segments(i)
         return node_attention(self.q[i], segs, self.kv.__getitem__, self.scale, rows)
 
 

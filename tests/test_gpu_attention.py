@@ -90,6 +90,24 @@ def test_kv_stream_shape(nq):
         bf16_gates(out[i], case.oracle(i), f"kv stream nq={nq} node {pack[i]}")
 
 
+def test_position_dependent_policy():
+    """A chunk-dependent policy (Eq. 4's Phi_b and R_b,j: random per-chunk
+    phi tables and offset masks) through the plan and the bf16 kernel."""
+    import random
+    rnd = random.Random(9)
+    K, W, n = SMALL.K, SMALL.W, 10
+    phi = [[[rnd.randint(0, K) for _ in range(W)] for _ in range(K + 1)] for _ in range(n)]
+    mask = [[[int(rnd.random() < 0.7) for _ in range(W)] for _ in range(K + 1)] for _ in range(n)]
+    kw = dict(phi_table=phi, r_mask=mask, n_chunks=n)
+    pack = [(7, 1), (8, 3), (9, 4)]
+    sel = select(oracle_policy("table", K, W, **kw), pack)
+    resident = [s for s in sel.states if s not in pack]
+    case = AttnCase(SMALL, sc.SC_DTYPE_BF16, "table", pack, resident, seed=10, policy_kw=kw)
+    out = case.run()
+    for i in range(len(pack)):
+        bf16_gates(out[i], case.oracle(i), f"position-dependent node {pack[i]}")
+
+
 def test_small_packed_matches_sequential():
     """The same nodes packed and one per call.  The split-key schedule cuts a
     node's key range where the pack's total work puts the work-group

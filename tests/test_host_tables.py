@@ -25,12 +25,12 @@ def test_header_symbols_exported():
     assert declared == set(sc.EXPORTED_SYMBOLS)
     for name in declared:
         assert hasattr(sc.lib, name), name
-    assert sc.sc_abi_version() == sc.ABI_VERSION == 2
+    assert sc.sc_abi_version() == sc.ABI_VERSION == 3
 
 
 def _random_pack(rnd, K, max_chunk=9, max_n=6):
     cand = [(c, j) for c in range(max_chunk) for j in range(K + 1)]
-    return rnd.sample(cand, rnd.randint(1, max_n))
+    return rnd.sample(cand, rnd.randint(1, min(max_n, len(cand))))
 
 
 def _oracle_policy(kind, K, W, phi, mask):
@@ -217,3 +217,36 @@ def test_empty_pack_is_a_no_op():
     sc.sc_attention(plan, cache, 0, 0x1000, 0x2000, 0.125)
     assert sc.sc_attention_workspace_bytes(plan, cache) == 0
     assert cache.free_slot_count() == 8
+
+
+def test_position_dependent_selection_bit_exact():
+    """Chunk-dependent phi tables and offset masks (Eq. 4's Phi_b, R_b,j)
+    through the C ABI against the oracle."""
+    rnd = random.Random(2)
+    for trial in range(200):
+        K, W, n = rnd.randint(1, 5), rnd.randint(0, 6), rnd.randint(1, 10)
+        kind = rnd.choice(["clean", "same", "prog", "table"])
+        phi = ([[[rnd.randint(0, K) for _ in range(W)] for _ in range(K + 1)] for _ in range(n)]
+               if kind == "table" else None)
+        mask = None
+        if kind != "table" or rnd.random() < 0.5:
+            mask = [[[rnd.randint(0, 1) for _ in range(W)] for _ in range(K + 1)] for _ in range(n)]
+        pack = _random_pack(rnd, K, max_chunk=n)
+        want = select(Policy({"clean": 0, "same": 1, "prog": 2, "table": 3}[kind], K, W, phi, mask,
+                             n_chunks=n), pack)
+        got = sc.sc_selection_build(kind, K, W, pack, phi_table=phi, r_mask=mask, n_chunks=n)
+        off, ch, lv, src = got.tables()
+        assert off == want.seg_off and ch == want.seg_chunk
+        assert lv == want.seg_level and src == want.seg_src
+    K, W, n = 2, 2, 3
+    phi = [[[0, 0] for _ in range(K + 1)] for _ in range(n)]
+    with pytest.raises(sc.ScError) as e:                       # node beyond the tables
+        sc.sc_selection_build("table", K, W, [(3, 1)], phi_table=phi, n_chunks=n)
+    assert e.value.code == sc.SC_EINVAL
+    phi[2][1][0] = 3                                           # entry > K in the last chunk's table
+    with pytest.raises(sc.ScError) as e:
+        sc.sc_selection_build("table", K, W, [(0, 1)], phi_table=phi, n_chunks=n)
+    assert e.value.code == sc.SC_EINVAL
+    with pytest.raises(sc.ScError) as e:
+        sc.sc_selection_build("prog", K, W, [(0, 1)], n_chunks=-1)
+    assert e.value.code == sc.SC_EINVAL

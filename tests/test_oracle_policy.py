@@ -206,3 +206,45 @@ def test_plan_pages_and_slots():
     with pytest.raises(PlanError) as e:
         build_plan(select(policy("prog", K, W), [(0, 1), (1, 2)]), small, 7)
     assert e.value.code == "ECAPACITY" and small.slots == {}
+
+
+def test_position_dependent_policy_by_hand():
+    """Eq. 4 lets Phi_b and R_b,j depend on the chunk.  K = 2, W = 2, chunks
+    0-1 read clean history and chunks 2-3 same-level history; chunk 3 at
+    level 2 skips offset 1."""
+    K, W = 2, 2
+    clean = [[0, 0] for _ in range(K + 1)]
+    same = [[j, j] for j in range(K + 1)]
+    phi = [clean, clean, same, same]
+    mask = [[[1, 1] for _ in range(K + 1)] for _ in range(4)]
+    mask[3][2] = [0, 1]
+    pol = Policy(3, K, W, phi_table=phi, r_mask=mask, n_chunks=4)
+    assert select(pol, [(1, 2)]).segments(0) == [(0, 0), (1, 2)]
+    assert select(pol, [(2, 1)]).segments(0) == [(0, 1), (1, 1), (2, 1)]
+    assert select(pol, [(3, 1)]).segments(0) == [(1, 1), (2, 1), (3, 1)]
+    assert select(pol, [(3, 2)]).segments(0) == [(1, 2), (3, 2)]
+    with pytest.raises(SelectionError):
+        select(pol, [(4, 0)])                                # beyond the tables
+
+
+def test_chunk_constant_tables_equal_position_independent():
+    """Repeating one (K+1) x W table for every chunk gives the
+    position-independent policy exactly (tables of the three named policies
+    included)."""
+    rnd = random.Random(5)
+    for _ in range(60):
+        K, W, n = rnd.randint(1, 5), rnd.randint(0, 6), 10
+        kind = rnd.choice(["clean", "same", "prog", "table"])
+        if kind == "table":
+            t = [[rnd.randint(0, K) for _ in range(W)] for _ in range(K + 1)]
+        else:
+            t = [[policy(kind, K, W).phi(j, r) for r in range(1, W + 1)] for j in range(K + 1)]
+        base = Policy(3, K, W, phi_table=t)
+        per_chunk = Policy(3, K, W, phi_table=[t] * n, n_chunks=n)
+        pack = rnd.sample([(c, j) for c in range(n) for j in range(K + 1)], rnd.randint(1, 6))
+        a, b = select(base, pack), select(per_chunk, pack)
+        assert (a.seg_off, a.seg_chunk, a.seg_level, a.seg_src) == \
+            (b.seg_off, b.seg_chunk, b.seg_level, b.seg_src)
+        if kind != "table":
+            c_ = select(policy(kind, K, W), pack)
+            assert (c_.seg_chunk, c_.seg_level) == (b.seg_chunk, b.seg_level)

@@ -80,3 +80,21 @@ def test_serial_schedule_with_release_is_available():
             sc.sc_plan_build(sc.sc_selection_build(kind, K, W, [node]), cache)
             sc.sc_cache_release_unread(cache, kind, K, W, order[i + 1:])
         assert cache.free_slot_count() == 1024
+
+
+def test_release_rule_with_position_dependent_policy():
+    """A policy that switches from same-level to progressive history after
+    the first chunks (chunk-dependent tables; both are available under Eq. 8):
+    the pipelined schedule, with the release rule evaluated under the same
+    tables, keeps every plan available and ends with an empty cache."""
+    K, B, W = 4, 10, 3
+    same = [[j] * W for j in range(K + 1)]
+    prog = [[max(j - r, 0) for r in range(1, W + 1)] for j in range(K + 1)]
+    phi = [same if c < 4 else prog for c in range(B)]
+    cache = _host_cache(1024)
+    rounds = pipeline_rounds(B, K, refresh=True)
+    for n, pack in enumerate(rounds):
+        sc.sc_plan_build(sc.sc_selection_build("table", K, W, pack, phi_table=phi, n_chunks=B), cache)
+        future = [node for p in rounds[n + 1:] for node in p]
+        sc.sc_cache_release_unread(cache, "table", K, W, future, phi_table=phi, n_chunks=B)
+    assert cache.free_slot_count() == 1024
