@@ -32,7 +32,7 @@
 extern "C" {
 #endif
 
-#define SC_ABI_VERSION 3
+#define SC_ABI_VERSION 4
 
 enum {
   SC_OK = 0,
@@ -208,13 +208,26 @@ int sc_attention(const sc_plan* plan, const sc_cache* cache, int32_t layer, cons
  * (Wqkv is [3*hidden, hidden] = Wq;Wk;Wv).  x: device bf16
  * [n_nodes * Nq, hidden], updated in place.  ws: device workspace of at least
  * sc_block_workspace_bytes() bytes.  The block form is the Wan-shaped
- * reading of the workload (the paper does not define the network). */
+ * reading of the workload (the paper does not define the network).
+ *
+ * Noise-level conditioning (optional, mod != NULL): the denoiser of Eq. 1
+ * depends on the node's level j.  mod is a device fp32 table
+ * [mod_levels][6][hidden] of per-level vectors (shift_a, scale_a, gate_a,
+ * shift_m, scale_m, gate_m), e.g. a timestep embedding projected per layer
+ * (computed by the caller); every pack node needs j < mod_levels.  With it:
+ *   h  = RMSNorm(x)  * (1 + scale_a[j]) + shift_a[j]
+ *   x' = x + gate_a[j] * (o Wo^T)
+ *   h2 = RMSNorm(x') * (1 + scale_m[j]) + shift_m[j]
+ *   x  = x' + gate_m[j] * (GELU_tanh(h2 Wup^T) Wdown^T)
+ * (elementwise over hidden).  mod == NULL is the unconditioned form above. */
 typedef struct {
   int32_t hidden, n_heads, head_dim, mlp;
   const void* w_qkv;  /* [3*hidden, hidden] */
   const void* w_o;    /* [hidden, hidden]   */
   const void* w_up;   /* [mlp, hidden]      */
   const void* w_down; /* [hidden, mlp]      */
+  const float* mod;   /* [mod_levels][6][hidden] fp32, or NULL */
+  int32_t mod_levels;
 } sc_block_weights;
 size_t sc_block_workspace_bytes(const sc_block_weights* w, int32_t n_tokens);
 int sc_block_forward(const sc_block_weights* w, sc_cache* cache, int32_t layer,

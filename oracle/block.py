@@ -12,6 +12,17 @@ real model; no trained weights exist here):
     x' = x + o Wo^T
     y  = x' + GELU_tanh(RMSNorm(x') Wup^T) Wdown^T
 
+Noise-level conditioning (optional): the denoiser of Eq. 1 takes the node's
+level j.  With a per-level table mod[j] = (shift_a, scale_a, gate_a,
+shift_m, scale_m, gate_m) the block is
+
+    h  = RMSNorm(x) (1 + scale_a) + shift_a
+    x' = x + gate_a (o Wo^T)
+    y  = x' + gate_m (GELU_tanh((RMSNorm(x') (1 + scale_m) + shift_m) Wup^T) Wdown^T)
+
+(an adaLN-style reading; the table itself, e.g. a projected timestep
+embedding, is an input).  Without it the block is the form above.
+
 Weights are in [out, in] layout (y = x W^T); Wqkv stacks Wq, Wk, Wv along
 its output axis.  Every product here is an fp64 numpy matmul.  The K and V a
 node produces become the cached representation of its state (Sec. 3.2,
@@ -53,10 +64,21 @@ class BlockShape:
         return self.frames_per_chunk * self.grid_h * self.grid_w
 
 
-def project_kv(x: np.ndarray, chunk: int, w_qkv: np.ndarray, shp: BlockShape):
+def modulated_norm(x: np.ndarray, mod_row: Optional[np.ndarray], which: int) -> np.ndarray:
+    """RMSNorm(x), then * (1 + scale) + shift of part ``which`` (0 attention,
+    1 MLP) of one level's modulation row [6][hidden]; plain without a row."""
+    h = rmsnorm(x)
+    if mod_row is None:
+        return h
+    shift = np.asarray(mod_row[3 * which], dtype=np.float64)
+    scale = np.asarray(mod_row[3 * which + 1], dtype=np.float64)
+    return h * (1.0 + scale) + shift
+
+
+def project_kv(x: np.ndarray, chunk: int, w_qkv: np.ndarray, shp: BlockShape, mod_row=None):
     """Rotated K and plain V of one node's tokens: x [Nq, hidden] -> [Nq, H, d] x 2."""
     D = shp.hidden
-    h = rmsnorm(x)
+    h = modulated_norm(x, mod_row, 0)
     w = np.asarray(w_qkv, dtype=np.float64)
     k = (h @ w[D:2 * D].T).reshape(-1, shp.heads, shp.head_dim)
     v = (h @ w[2 * D:3 * D].T).reshape(-1, shp.heads, shp.head_dim)
@@ -64,31 +86,37 @@ def project_kv(x: np.ndarray, chunk: int, w_qkv: np.ndarray, shp: BlockShape):
     return rope(k, pos, shp.rope_dims, shp.theta), v
 
 
-def project_q(x: np.ndarray, chunk: int, w_qkv: np.ndarray, shp: BlockShape, rows=None):
+def project_q(x: np.ndarray, chunk: int, w_qkv: np.ndarray, shp: BlockShape, rows=None,
+              mod_row=None):
     D = shp.hidden
     x = np.asarray(x, dtype=np.float64)
     pos = chunk_positions(chunk, shp.frames_per_chunk, shp.grid_h, shp.grid_w)
     if rows is not None:
         x, pos = x[rows], pos[rows]
-    h = rmsnorm(x)
+    h = modulated_norm(x, mod_row, 0)
     q = (h @ np.asarray(w_qkv, dtype=np.float64)[0:D].T).reshape(-1, shp.heads, shp.head_dim)
     return rope(q, pos, shp.rope_dims, shp.theta)
 
 
 def block_forward(sel, x_of: Callable[[int], np.ndarray], weights: Dict[str, np.ndarray],
                   resident_kv: Callable[[Tuple[int, int]], Tuple[np.ndarray, np.ndarray]],
-                  shp: BlockShape, rows: Optional[Sequence[int]] = None):
+                  shp: BlockShape, rows: Optional[Sequence[int]] = None,
+                  mod: Optional[np.ndarray] = None):
     """Run one block for every node of ``sel``.
 
     x_of(i) gives node i's input [Nq, hidden].  resident_kv(state) gives the
     cached (rotated K, V) of a state that no pack node produces.  ``rows``
     restricts the outputs to those token rows of every node (the K/V of all
-    rows are still computed, since every row reads all of them).
+    rows are still computed, since every row reads all of them).  ``mod``
+    is the optional per-level modulation table [levels][6][hidden].
     Returns ({i: y_i}, {i: (k_i, v_i)}).
     """
+    def mod_row(j):
+        return None if mod is None else np.asarray(mod[j], dtype=np.float64)
+
     new_kv = {}
     for i, (c, j) in enumerate(sel.nodes):
-        new_kv[i] = project_kv(x_of(i), c, weights["w_qkv"], shp)
+        new_kv[i] = project_kv(x_of(i), c, weights["w_qkv"], shp, mod_row(j))
     index_of = {node: i for i, node in enumerate(sel.nodes)}
 
     def kv_of(state):
@@ -99,12 +127,15 @@ def block_forward(sel, x_of: Callable[[int], np.ndarray], weights: Dict[str, np.
     scale = 1.0 / math.sqrt(shp.head_dim)
     out = {}
     for i, (c, j) in enumerate(sel.nodes):
+        m = mod_row(j)
         x = np.asarray(x_of(i), dtype=np.float64)
         if rows is not None:
             x = x[rows]
-        q = project_q(x_of(i), c, weights["w_qkv"], shp, rows)
+        q = project_q(x_of(i), c, weights["w_qkv"], shp, rows, m)
         o = node_attention(q, sel.segments(i), kv_of, scale).reshape(q.shape[0], -1)
-        x1 = x + o @ np.asarray(weights["w_o"], dtype=np.float64).T
-        u = rmsnorm(x1) @ np.asarray(weights["w_up"], dtype=np.float64).T
-        out[i] = x1 + gelu_tanh(u) @ np.asarray(weights["w_down"], dtype=np.float64).T
+        a = o @ np.asarray(weights["w_o"], dtype=np.float64).T
+        x1 = x + (a if m is None else m[2] * a)
+        u = modulated_norm(x1, m, 1) @ np.asarray(weights["w_up"], dtype=np.float64).T
+        f = gelu_tanh(u) @ np.asarray(weights["w_down"], dtype=np.float64).T
+        out[i] = x1 + (f if m is None else m[5] * f)
     return out, new_kv

@@ -97,7 +97,8 @@ class sc_rope(C.Structure):
 class sc_block_weights(C.Structure):
     _fields_ = [("hidden", C.c_int32), ("n_heads", C.c_int32), ("head_dim", C.c_int32),
                 ("mlp", C.c_int32), ("w_qkv", C.c_void_p), ("w_o", C.c_void_p),
-                ("w_up", C.c_void_p), ("w_down", C.c_void_p)]
+                ("w_up", C.c_void_p), ("w_down", C.c_void_p), ("mod", C.c_void_p),
+                ("mod_levels", C.c_int32)]
 
 
 _P = C.c_void_p
@@ -143,7 +144,7 @@ _SIG = {
                                    C.POINTER(sc_rope), _P, C.c_size_t, _P]),
 }
 # ABI version this binding marshals for (SC_ABI_VERSION of the header)
-ABI_VERSION = 3
+ABI_VERSION = 4
 if not hasattr(lib, "sc_abi_version") or lib.sc_abi_version() != ABI_VERSION:
     raise ImportError(f"{library_path} does not implement ABI version {ABI_VERSION}; rebuild it "
                       "(__graft_entry__.build())")
@@ -375,10 +376,14 @@ def sc_attention(plan: Plan, cache: Cache, layer: int, q, o, scale: float, ws=No
 
 # ---------------------------------------------------------------------- block
 class BlockWeights:
-    def __init__(self, hidden, n_heads, head_dim, mlp, w_qkv, w_o, w_up, w_down):
-        self.tensors = (w_qkv, w_o, w_up, w_down)
+    """Device weights of one block; ``mod`` is the optional fp32 per-level
+    modulation table [levels][6][hidden] (noise-level conditioning)."""
+
+    def __init__(self, hidden, n_heads, head_dim, mlp, w_qkv, w_o, w_up, w_down, mod=None):
+        self.tensors = (w_qkv, w_o, w_up, w_down, mod)
+        levels = 0 if mod is None else int(mod.shape[0])
         self.struct = sc_block_weights(hidden, n_heads, head_dim, mlp, _ptr(w_qkv), _ptr(w_o),
-                                       _ptr(w_up), _ptr(w_down))
+                                       _ptr(w_up), _ptr(w_down), _ptr(mod), levels)
 
 
 def sc_block_workspace_bytes(w: BlockWeights, n_tokens: int) -> int:

@@ -36,6 +36,20 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
   if (n > kGemmMaxNodes || n * d.pages_per_chunk > kGemmMaxNodePages)
     return fail(SC_EUNSUPPORTED, "pack too large for the QKV epilogue (%d nodes)", n);
   const int32_t T = n * p->nq;
+  if (w->mod) {
+    if (reinterpret_cast<uintptr_t>(w->mod) & 15) return fail(SC_EINVAL, "modulation table must be 16-byte aligned");
+    for (int32_t i = 0; i < n; ++i)
+      if (p->nodes[i].level >= w->mod_levels)
+        return fail(SC_EINVAL, "node (%d,%d) has no row in a %d-level modulation table",
+                    p->nodes[i].chunk, p->nodes[i].level, w->mod_levels);
+  }
+  NormMod nm_a;
+  std::memset(&nm_a, 0, sizeof nm_a);
+  nm_a.mod = w->mod;
+  nm_a.nq = p->nq;
+  for (int32_t i = 0; i < n; ++i) nm_a.node_level[i] = p->nodes[i].level;
+  NormMod nm_m = nm_a;
+  nm_m.which = 1;
   if (ws_bytes < sc_block_workspace_bytes(w, T))
     return fail(SC_EINVAL, "workspace of %zu bytes, need %zu", ws_bytes, sc_block_workspace_bytes(w, T));
   if (rope) {
@@ -106,7 +120,7 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
   }
 
   int rc;
-  if ((rc = launch_rmsnorm(xb, hn, T, D, stream)) != SC_OK) return rc;
+  if ((rc = launch_rmsnorm(xb, hn, T, D, nm_a, stream)) != SC_OK) return rc;
   if ((rc = launch_gemm(EPI_QKV, TK_GEMM_QKV, static_cast<const uint16_t*>(w->w_qkv), hn, 3 * D, T, D, ep, stream)) != SC_OK)
     return rc;
   for (int32_t i = 0; i < n; ++i)
@@ -118,16 +132,22 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
   std::memset(&e2, 0, sizeof e2);
   e2.out = xb;
   e2.ld_out = D;
+  e2.nq = p->nq;
+  e2.mod = w->mod;
+  e2.gate_row = 2;  // gate_a
+  for (int32_t i = 0; i < n; ++i) e2.node_level[i] = p->nodes[i].level;
   if ((rc = launch_gemm(EPI_RESIDUAL, TK_GEMM_OUT, static_cast<const uint16_t*>(w->w_o), ob, D, T, D, e2, stream)) != SC_OK)
     return rc;
-  if ((rc = launch_rmsnorm(xb, hn, T, D, stream)) != SC_OK) return rc;
+  if ((rc = launch_rmsnorm(xb, hn, T, D, nm_m, stream)) != SC_OK) return rc;
   GemmEpilogue e3;
   std::memset(&e3, 0, sizeof e3);
   e3.out = ub;
   e3.ld_out = w->mlp;
   if ((rc = launch_gemm(EPI_GELU, TK_GEMM_UP, static_cast<const uint16_t*>(w->w_up), hn, w->mlp, T, D, e3, stream)) != SC_OK)
     return rc;
-  if ((rc = launch_gemm(EPI_RESIDUAL, TK_GEMM_DOWN, static_cast<const uint16_t*>(w->w_down), ub, D, T, w->mlp, e2, stream)) != SC_OK)
+  GemmEpilogue e4 = e2;
+  e4.gate_row = 5;  // gate_m
+  if ((rc = launch_gemm(EPI_RESIDUAL, TK_GEMM_DOWN, static_cast<const uint16_t*>(w->w_down), ub, D, T, w->mlp, e4, stream)) != SC_OK)
     return rc;
   return SC_OK;
 }

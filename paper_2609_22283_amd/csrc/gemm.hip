@@ -201,6 +201,10 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
       const int32_t t = t0 + wt + 32 * nb + r32;
       if (t >= T) continue;
       uint16_t* orow = ep.out + (size_t)t * ep.ld_out + f0 + wf + 4 * hl;
+      // noise-level gate of this token's node (residual epilogue only)
+      const float* gate = nullptr;
+      if (EPI == EPI_RESIDUAL && ep.mod)
+        gate = ep.mod + ((size_t)ep.node_level[t / ep.nq] * 6 + ep.gate_row) * F + f0 + wf + 4 * hl;
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
@@ -210,6 +214,11 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
           for (int e = 0; e < 4; ++e) v[e] = acc[mb][nb][4 * g + e];
           uint16_t* dst = orow + 32 * mb + 8 * g;
           if constexpr (EPI == EPI_RESIDUAL) {
+            if (gate) {
+              const f32x4 gv = *reinterpret_cast<const f32x4*>(gate + 32 * mb + 8 * g);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] *= gv[e];
+            }
             const u32x2 r = *reinterpret_cast<const u32x2*>(dst);
             v[0] += __uint_as_float(r.x << 16);
             v[1] += __uint_as_float(r.x & 0xffff0000u);
@@ -262,10 +271,11 @@ int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, i
 }
 
 // ------------------------------------------------------------------ RMSNorm
-// y = x / sqrt(mean(x^2) + eps), one wave per row, fp32 math, bf16 in/out.
+// y = x / sqrt(mean(x^2) + eps), one wave per row, fp32 math, bf16 in/out;
+// with a modulation table, y * (1 + scale) + shift of the row's node level.
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict__ x,
                                                       uint16_t* __restrict__ y, int32_t rows,
-                                                      int32_t D, float eps) {
+                                                      int32_t D, float eps, NormMod nm) {
   const int32_t row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int32_t lane = threadIdx.x & 63;
   if (row >= rows) return;
@@ -284,22 +294,43 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
   const float inv = rsqrtf(ss / (float)D + eps);
+  const float *shift = nullptr, *scale = nullptr;
+  if (nm.mod) {
+    const int32_t lev = nm.node_level[row / nm.nq];
+    shift = nm.mod + ((size_t)lev * 6 + 3 * nm.which) * D;
+    scale = shift + D;
+  }
   for (int32_t v = lane; v < nv; v += 64) {
     const u32x4 a = xr[v];
-    u32x4 r;
+    float f[8];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const float lo = __uint_as_float(a[k] << 16), hi = __uint_as_float(a[k] & 0xffff0000u);
-      r[k] = pack_bf16x2(lo * inv, hi * inv);
+      f[2 * k] = __uint_as_float(a[k] << 16) * inv;
+      f[2 * k + 1] = __uint_as_float(a[k] & 0xffff0000u) * inv;
     }
+    if (shift) {
+      const f32x4* sh = reinterpret_cast<const f32x4*>(shift + 8 * v);
+      const f32x4* sc = reinterpret_cast<const f32x4*>(scale + 8 * v);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const f32x4 s0 = sh[h], s1 = sc[h];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) f[4 * h + e] = fmaf(f[4 * h + e], 1.0f + s1[e], s0[e]);
+      }
+    }
+    u32x4 r;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) r[k] = pack_bf16x2(f[2 * k], f[2 * k + 1]);
     yr[v] = r;
   }
 }
 
-int launch_rmsnorm(const uint16_t* x, uint16_t* y, int32_t rows, int32_t D, hipStream_t stream) {
+int launch_rmsnorm(const uint16_t* x, uint16_t* y, int32_t rows, int32_t D, const NormMod& nm,
+                   hipStream_t stream) {
   if (D % 8) return fail(SC_EUNSUPPORTED, "rmsnorm needs D %% 8 == 0");
   timer_begin(TK_RMSNORM, stream);
-  hipLaunchKernelGGL(rmsnorm_kernel, dim3((rows + 3) / 4), dim3(256), 0, stream, x, y, rows, D, 1e-6f);
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3((rows + 3) / 4), dim3(256), 0, stream, x, y, rows, D, 1e-6f,
+                     nm);
   timer_end(TK_RMSNORM, stream);
   SC_HIP(hipGetLastError());
   return SC_OK;

@@ -96,9 +96,19 @@ def _weights(geo, layer, seed):
     return dev, exact
 
 
+def _mod_table(geo, seed):
+    """Random per-level modulation [K+1][6][hidden] fp32 (gates around 1)."""
+    m = np.stack([np.stack([normal((geo.hidden,), (seed, 30, j, r), 0.2) for r in range(6)])
+                  for j in range(geo.K + 1)]).astype(np.float32)
+    m[:, 2] += 1.0
+    m[:, 5] += 1.0
+    return m
+
+
 class BlockCase:
-    def __init__(self, geo, kind, pack, resident, seed=0):
+    def __init__(self, geo, kind, pack, resident, seed=0, mod=None):
         torch = torch_mod()
+        self.mod = mod                                   # host fp32 table or None
         self.geo, self.kind, self.pack = geo, kind, pack
         ppc, tpp = geo.frames_per_chunk, geo.tokens_per_page
         n_slots = (len(resident) + len(pack) + 2) * ppc
@@ -127,8 +137,10 @@ class BlockCase:
         n = geo.tokens_per_chunk
         self.x = [xv[i * n:(i + 1) * n] for i in range(len(pack))]
         self.w_dev, self.w = _weights(geo, 0, seed)
+        self.mod_dev = None if mod is None else torch.from_numpy(mod).cuda()
         self.bw = sc.BlockWeights(geo.hidden, geo.heads, geo.head_dim, geo.mlp, self.w_dev["w_qkv"],
-                                  self.w_dev["w_o"], self.w_dev["w_up"], self.w_dev["w_down"])
+                                  self.w_dev["w_o"], self.w_dev["w_up"], self.w_dev["w_down"],
+                                  mod=self.mod_dev)
         T = len(pack) * n
         self.ws_bytes = sc.sc_block_workspace_bytes(self.bw, T)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device="cuda")
@@ -147,7 +159,7 @@ class BlockCase:
     def oracle(self, rows=None):
         sel = select(oracle_policy(self.kind, self.geo.K, self.geo.W), self.pack)
         return block_forward(sel, lambda i: self.x[i], self.w, self.res_kv.__getitem__, self.shape,
-                             rows=rows)
+                             rows=rows, mod=self.mod)
 
 
 def block_gate(got, want, what):
@@ -184,6 +196,21 @@ def test_small_block(kind, pack, resident):
     assert e.value.code == sc.SC_EEXIST
 
 
+@pytest.mark.parametrize("kind,pack,resident", SMALL_BLOCK_PACKS[:2])
+def test_small_block_level_modulation(kind, pack, resident):
+    """Noise-level conditioning: per-level shift/scale after both RMSNorms
+    and gates on both residual branches, each node using its own level's
+    row."""
+    case = BlockCase(SMALL, kind, pack, resident, seed=15, mod=_mod_table(SMALL, 15))
+    got = case.run()
+    want, new_kv = case.oracle()
+    for i in range(len(pack)):
+        block_gate(got[i], want[i], f"modulated {kind} node {pack[i]}")
+        k_got, v_got = read_pages(case.pool, SMALL, case.n_slots, case.cache.slots(pack[i]))
+        bf16_gates(k_got, new_kv[i][0], "cached K (modulated)")
+        bf16_gates(v_got, new_kv[i][1], "cached V (modulated)")
+
+
 def test_short_block_prog():
     """A progressive pack of one-frame, 96-token chunks (the attention's
     128-query work-group shape inside the block)."""
@@ -193,6 +220,15 @@ def test_short_block_prog():
     want, _ = case.oracle()
     for i in range(len(pack)):
         block_gate(got[i], want[i], f"short node {pack[i]}")
+
+
+def test_block_rejects_level_beyond_modulation_table():
+    mod = _mod_table(SMALL, 16)[:3]                       # levels 0..2 only
+    case = BlockCase(SMALL, "prog", [(6, 1), (7, 2), (8, 3)], [(c, 0) for c in range(6)], seed=16,
+                     mod=mod)
+    with pytest.raises(sc.ScError) as e:
+        case.run()
+    assert e.value.code == sc.SC_EINVAL
 
 
 def test_block_rejects_oversized_pack():

@@ -129,6 +129,70 @@ def test_block_rows_subset_matches_full():
         np.testing.assert_array_equal(part[i], full[i][rows])
 
 
+def _mod_table(shp, K, seed, neutral=False):
+    """[K+1][6][hidden]: shift_a, scale_a, gate_a, shift_m, scale_m, gate_m."""
+    m = np.zeros((K + 1, 6, shp.hidden))
+    if neutral:
+        m[:, 2] = 1.0
+        m[:, 5] = 1.0
+        return m
+    for j in range(K + 1):
+        for r in range(6):
+            m[j, r] = normal((shp.hidden,), (seed, 30, j, r), 0.2).astype(np.float64)
+        m[j, 2] += 1.0
+        m[j, 5] += 1.0
+    return m
+
+
+def test_block_neutral_modulation_is_unconditioned_block():
+    """shift = scale = 0 and gate = 1 at every level reproduce the
+    unconditioned block exactly."""
+    shp = _tiny_shape()
+    pack = [(1, 1), (2, 2), (3, 3)]
+    sel = select(policy("prog", 4, 2), pack)
+    xs = [normal((shp.tokens_per_chunk, shp.hidden), (5, i)).astype(np.float64) for i in range(3)]
+    res = {(0, 0): tuple(normal((shp.tokens_per_chunk, 2, 16), (5, t, 0)).astype(np.float64)
+                         for t in (2, 3))}
+    plain, kv0 = block_forward(sel, lambda i: xs[i], _weights(shp, 0), res.__getitem__, shp)
+    neutral, kv1 = block_forward(sel, lambda i: xs[i], _weights(shp, 0), res.__getitem__, shp,
+                                 mod=_mod_table(shp, 4, 0, neutral=True))
+    for i in range(3):
+        np.testing.assert_array_equal(neutral[i], plain[i])
+        np.testing.assert_array_equal(kv0[i][0], kv1[i][0])
+
+
+def test_block_modulation_gates():
+    """Zero gates make the block the identity whatever the shifts and scales;
+    with the MLP gate at zero, the residual update is linear in the attention
+    gate; and the level of each node picks its own row."""
+    shp = _tiny_shape()
+    pack = [(0, 3), (1, 4)]
+    sel = select(policy("prog", 4, 2), pack)
+    xs = [normal((shp.tokens_per_chunk, shp.hidden), (6, i)).astype(np.float64) for i in range(2)]
+    m = _mod_table(shp, 4, 1)
+    m0 = m.copy()
+    m0[:, 2] = 0.0
+    m0[:, 5] = 0.0
+    y, _ = block_forward(sel, lambda i: xs[i], _weights(shp, 0), None, shp, mod=m0)
+    for i in range(2):
+        np.testing.assert_array_equal(y[i], xs[i])
+    m1 = m.copy()
+    m1[:, 5] = 0.0
+    m2 = m1.copy()
+    m2[:, 2] *= 2.0
+    y1, _ = block_forward(sel, lambda i: xs[i], _weights(shp, 0), None, shp, mod=m1)
+    y2, _ = block_forward(sel, lambda i: xs[i], _weights(shp, 0), None, shp, mod=m2)
+    for i in range(2):
+        np.testing.assert_allclose(y2[i] - xs[i], 2.0 * (y1[i] - xs[i]), rtol=1e-12, atol=1e-12)
+    # changing the row of a level no pack node has leaves the outputs unchanged
+    m3 = m.copy()
+    m3[2] += 5.0
+    ya, _ = block_forward(sel, lambda i: xs[i], _weights(shp, 0), None, shp, mod=m)
+    yb, _ = block_forward(sel, lambda i: xs[i], _weights(shp, 0), None, shp, mod=m3)
+    for i in range(2):
+        np.testing.assert_array_equal(ya[i], yb[i])
+
+
 def test_pipeline_counts():
     """K + B - 1 rounds and B*K updates (Sec. 3.3); with the refresh node
     K + B rounds and B*(K+1) forwards; first clean chunk after K rounds."""
