@@ -92,22 +92,15 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 }
 
 // ------------------------------------------------------------- bf16 kernel
-// The kernel is instantiated for NW = 8 waves (256 queries per work-group,
-// one work-group per CU) and NW = 4 (128 queries, two per CU); both keep 8
-// waves per CU, two per SIMD, within the register budget of that occupancy.
-// The host takes NW = 4 for nodes of at most 128 queries.
-template <int NW> struct Shape {
-  static constexpr int BQ = 32 * NW;              // queries per work-group
-  static constexpr int WG_PER_CU = 8 / NW;        // resident work-groups per CU
-  static constexpr int KCP = 64 / (4 * NW);       // K copy instructions per wave per tile
-  static constexpr int VCP = 128 / (8 * NW);      // V copy instructions per wave per tile
-};
-constexpr int BQ_MAX = 256;
-constexpr int BK = 64;                 // keys per tile
-constexpr int HDB = 128;               // head dim of the bf16 kernel
+// Two work-group shapes, both with two waves per SIMD: 8 waves x 32 queries
+// (256 per work-group, one work-group per CU) and 4 waves x 32 queries (128,
+// two per CU), the latter for nodes of at most 128 queries.
+constexpr int BK = 64;                 // keys per LDS tile
+constexpr int HDB = 128;               // head dim of the bf16 kernels
 constexpr int KT_BYTES = BK * HDB * 2;  // 16 KB
 constexpr int VT_BYTES = HDB * BK * 2;  // 16 KB
 constexpr int SMEM_BYTES = 2 * (KT_BYTES + VT_BYTES);
+constexpr int BQ_SMALL = 128, BQ_MAX = 256;  // queries per work-group of the two shapes
 // Softmax bookkeeping.  Q is pre-scaled by scale*log2(e), so S is in log2
 // units, and each S tile starts its accumulation at -m (the running
 // maximum): p = exp2(S) directly.  m is the exact maximum of the first tile
@@ -118,117 +111,70 @@ constexpr float GROW_LIMIT = 18446744073709551616.0f;  // 2^64
 
 struct AttnLane {
   // per-lane LDS read offsets (bytes) inside one buffer
-  uint32_t koff[8];   // K row sigma, 16-byte column 2 si + hl   (kb adds 8192)
+  uint32_t koff[8];   // K row sigma, 16-byte column 2 si + hl   (second 32 rows add 8192)
   uint32_t voff[4];   // V^T row r32, column 4 kb + 2 mm + hl    (db adds 4096)
 };
 
-// S^T blocks of one tile, s[kb] = K_kb Q^T - m for the two 32-key halves.
-__device__ __forceinline__ void qk_tile(const char* kl, const AttnLane& L, const bf16x8 (&qreg)[8],
-                                        f32x16 (&s)[2], float m) {
+// Row sigma of the S^T MFMA holds key sigma: each lane's probabilities are
+// then keys 8 hl .. 8 hl + 7 (+16) of every 32-key block -- exactly the B
+// operand layout of the PV MFMA.
+__device__ __forceinline__ AttnLane attn_lane(int32_t r32, int32_t hl) {
+  AttnLane L;
+  const int32_t sa = r32 >> 3, sh = (r32 >> 2) & 1, sb = r32 & 3;
+  const int32_t sigma = 16 * (sa >> 1) + 8 * sh + 4 * (sa & 1) + sb;
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
+  for (int si = 0; si < 8; ++si) L.koff[si] = sigma * 256 + (((2 * si + hl) ^ (sigma & 15)) << 4);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) s[kb][i] = -m;
+  for (int cm = 0; cm < 4; ++cm) L.voff[cm] = r32 * 128 + (((2 * cm + hl) ^ ((r32 >> 1) & 7)) << 4);
+  return L;
+}
+
+// Q^T operand of a 32-query block: lane holds Q[row][16 si + 8 hl .. +7],
+// pre-scaled to log2 units.  Rows past the node's end repeat its last row.
+__device__ __forceinline__ void load_q(const uint16_t* q, const AttnGeom& g, int32_t node, int32_t head,
+                                       int32_t qrow, int32_t hl, bf16x8 (&qreg)[8]) {
+  const int32_t qrow_c = qrow < g.nq ? qrow : g.nq - 1;
+  const uint16_t* qp = q + (((size_t)node * g.nq + qrow_c) * g.n_heads + head) * HDB + 8 * hl;
 #pragma unroll
-    for (int si = 0; si < 8; ++si) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + L.koff[si] + kb * 8192);
-      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[si], s[kb], 0, 0, 0);
-    }
+  for (int si = 0; si < 8; ++si) {
+    const bf16x8 raw = *reinterpret_cast<const bf16x8*>(qp + 16 * si);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) qreg[si][e] = static_cast<__bf16>(static_cast<float>(raw[e]) * g.scale_log2);
   }
 }
 
-__device__ __forceinline__ float tile_max(const f32x16 (&s)[2]) {
-  float mx = fmaxf(s[0][0], s[0][1]);
+// Maximum over one lane's 16 logits and its partner half (the other 16 keys
+// of the same query column).
+__device__ __forceinline__ float col_max16(const f32x16& s) {
+  float mx = fmaxf(s[0], s[1]);
 #pragma unroll
-  for (int i = 2; i < 16; ++i) mx = fmaxf(mx, s[0][i]);
-#pragma unroll
-  for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[1][i]);
+  for (int i = 2; i < 16; ++i) mx = fmaxf(mx, s[i]);
   return fmaxf(mx, __shfl_xor(mx, 32));
 }
 
-// p = exp2(s) rounded to bf16 (the B operands of the PV MFMA) and the sum of
-// the rounded values.
-__device__ __forceinline__ float probs(const f32x16 (&s)[2], bf16x8 (&pb)[2][2]) {
+// Keys at or past the node's end get no weight: value i of a lane is key
+// key0 + 16 (i / 8) + 8 hl + i % 8 of the 32-key block starting at key0.
+__device__ __forceinline__ void mask32(f32x16& s, int32_t key0, int32_t nk, int32_t hl) {
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int mm = 0; mm < 2; ++mm)
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        pb[kb][mm][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(s[kb][8 * mm + e]));
-  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
-  float l0 = 0.f, l1 = 0.f;
+  for (int i = 0; i < 16; ++i)
+    if (key0 + 16 * (i >> 3) + 8 * hl + (i & 7) >= nk) s[i] = -INFINITY;
+}
+
+// p = exp2(s) rounded to bf16 for one 32-key block (two B operands of the PV
+// MFMA) and the sum of the rounded values.
+__device__ __forceinline__ float probs32(const f32x16& s, bf16x8 (&pb)[2]) {
 #pragma unroll
   for (int mm = 0; mm < 2; ++mm)
 #pragma unroll
-    for (int e = 0; e < 8; e += 2) {
-      const bf16x2 p0 = {pb[0][mm][e], pb[0][mm][e + 1]};
-      const bf16x2 p1 = {pb[1][mm][e], pb[1][mm][e + 1]};
-      l0 = __builtin_amdgcn_fdot2_f32_bf16(p0, ones, l0, false);
-      l1 = __builtin_amdgcn_fdot2_f32_bf16(p1, ones, l1, false);
-    }
+    for (int e = 0; e < 8; ++e) pb[mm][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(s[8 * mm + e]));
+  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+  float l0 = 0.f, l1 = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; e += 2) {
+    l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[0][e], pb[0][e + 1]}, ones, l0, false);
+    l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[1][e], pb[1][e + 1]}, ones, l1, false);
+  }
   return l0 + l1;
-}
-
-// One step of the software-pipelined loop, for tile t: probabilities of
-// S(t) (held in s), the next tile's S(t+1) = K(t+1) Q^T - m on the matrix
-// cores while the exponentials of tile t run on the vector ALUs, then
-// O^T += V(t)^T P(t).  K runs one tile ahead of V: K(t+1) sits in K buffer
-// KN, V(t) in V buffer VC.
-template <int KN, int VC, bool NEXT, bool MASK>
-__device__ __forceinline__ void attn_step(const char* smem, const AttnLane& L, const bf16x8 (&qreg)[8],
-                                          f32x16 (&oacc)[4], f32x16 (&s)[2], float& m_run,
-                                          float& l_run, int32_t t0, int32_t nk, int32_t hl) {
-  if constexpr (MASK) {  // keys past the node's last key get no weight
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int32_t key = t0 + 32 * kb + 16 * (i >> 3) + 8 * hl + (i & 7);
-        if (key >= nk) s[kb][i] = -INFINITY;
-      }
-  }
-  bf16x8 pb[2][2];
-  float l_tile = probs(s, pb);
-  f32x16 sn[2];
-  if constexpr (NEXT) qk_tile(smem + KN * KT_BYTES, L, qreg, sn, m_run);
-  if (__builtin_amdgcn_ballot_w64(!(l_tile < GROW_LIMIT))) {
-    // rare: raise the running maximum to this tile's and redo the tile (the
-    // next tile's logits were offset by the old maximum).  The opaque
-    // statement keeps this a wave-uniform branch.
-    asm volatile("" ::: "memory");
-    const float grow = fmaxf(tile_max(s), 0.f);
-    const float alpha = __builtin_amdgcn_exp2f(-grow);
-    m_run += grow;
-    l_run *= alpha;
-#pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        s[kb][i] -= grow;
-        if constexpr (NEXT) sn[kb][i] -= grow;
-      }
-    l_tile = probs(s, pb);
-  }
-  l_run += l_tile;
-  const char* vl = smem + 2 * KT_BYTES + VC * VT_BYTES;
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int mm = 0; mm < 2; ++mm)
-#pragma unroll
-      for (int db = 0; db < 4; ++db) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(vl + L.voff[2 * kb + mm] + db * 4096);
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kb][mm], oacc[db], 0, 0, 0);
-      }
-  if constexpr (NEXT) {
-    s[0] = sn[0];
-    s[1] = sn[1];
-  }
 }
 
 // Direct global -> LDS copy of 16 bytes per lane (gfx950 LDS DMA): lane i
@@ -241,13 +187,113 @@ __device__ __forceinline__ void dma16(const char* src, char* lds_wave_base) {
                                    16, 0, 0);
 }
 
+// Copies of 64-key K and V^T tiles of one (node, head) from the paged cache
+// into LDS, split over the NW waves of a work-group.  64 keys span at most
+// two pages (pages hold >= 64 tokens), so the page of a key is chosen against
+// one wave-uniform boundary.
+// Offsets are 32-bit, relative to the layer's slots (the host checks that a
+// layer fits in 4 GB); the per-page parts are wave-uniform.  Each wave copies
+// 16 / NW groups of 4 K rows (1 KB each) and 16 / NW groups of 8 V^T rows; lane
+// (row, physical column p) fetches logical column p ^ swizzle(row).  K rows
+// of keys past the node's end fetch its last key, V^T columns the tile's
+// first key (valid memory; their probabilities are zero).
+template <int NW>
+struct KvTiles {
+  static constexpr int KCP = 64 / (4 * NW), VCP = 128 / (8 * NW);
+  struct Slots {
+    uint32_t lo, hi;  // byte offsets of the slots of the tile's first page and the next one
+    int32_t plo;      // index of the tile's first page within the node
+  };
+  const char* lbase;
+  const int32_t* page_slot;  // the node's page slots
+  int32_t npages, nk, tpp, wave;
+  uint32_t slot_bytes, khead, vhead, kbad;
+  DivMagic tpp_div;
+  uint32_t kswz[KCP], vlane[VCP];
+  int32_t vkey[VCP], krow0;
+
+  __device__ __forceinline__ KvTiles(const AttnPlan& plan, const AttnGeom& g, int32_t node, int32_t head,
+                                     int32_t wave_, int32_t lane) {
+    const int32_t p0 = plan.page_off[node];
+    lbase = g.layer_base;
+    page_slot = plan.page_slot + p0;
+    npages = plan.page_off[node + 1] - p0;
+    tpp = g.tpp;
+    nk = npages * tpp;
+    wave = wave_;
+    slot_bytes = (uint32_t)g.slot_bytes;
+    tpp_div = g.tpp_div;
+    khead = (uint32_t)head * tpp * HDB * 2;
+    vhead = (uint32_t)g.kv_half + (uint32_t)head * HDB * tpp * 2;
+    kbad = (uint32_t)page_slot[npages - 1] * slot_bytes + khead + (uint32_t)(tpp - 1) * 256;
+    krow0 = 4 * KCP * wave + (lane >> 4);
+    const int32_t kp = lane & 15;
+    const int32_t vrow0 = 8 * VCP * wave + (lane >> 3), vp = lane & 7;
+#pragma unroll
+    for (int j = 0; j < KCP; ++j) {
+      const int32_t row = krow0 + 4 * j;
+      kswz[j] = (uint32_t)row * 256 + ((kp ^ (row & 15)) << 4);  // plus key t0 * 256
+    }
+#pragma unroll
+    for (int j = 0; j < VCP; ++j) {
+      const int32_t d = vrow0 + 8 * j;
+      vkey[j] = 8 * (vp ^ ((d >> 1) & 7));                           // key offset in tile
+      vlane[j] = (uint32_t)d * tpp * 2 + (uint32_t)vkey[j] * 2;      // plus key t0 * 2
+    }
+  }
+  // Page slots of the tile starting at key t0 >= 0 (two scalar loads),
+  // fetched one step before the copy that uses them so their latency
+  // overlaps the step in between.  Clamped to the node's pages: a tile past
+  // the end is never read.
+  __device__ __forceinline__ Slots slots(int32_t t0) const {
+    Slots sl;
+    sl.plo = min((int32_t)fast_div((uint32_t)t0, tpp_div), npages - 1);
+    const int32_t phi = sl.plo + 1 < npages ? sl.plo + 1 : sl.plo;
+    sl.lo = (uint32_t)page_slot[sl.plo] * slot_bytes;
+    sl.hi = (uint32_t)page_slot[phi] * slot_bytes;
+    return sl;
+  }
+  __device__ __forceinline__ void copy_k(int32_t t0, char* kl, const Slots& sl) const {
+    const int32_t bkey = (sl.plo + 1) * tpp;
+    const uint32_t lo = sl.lo + khead + (uint32_t)(t0 - sl.plo * tpp) * 256;
+    const uint32_t hi = sl.hi + khead + (uint32_t)(t0 - bkey) * 256;
+    const int32_t lim = nk - t0, split = bkey - t0;
+#pragma unroll
+    for (int j = 0; j < KCP; ++j) {
+      const int32_t rk = krow0 + 4 * j;  // tile-relative key
+      const uint32_t src = rk >= lim ? kbad + (kswz[j] - (uint32_t)rk * 256)
+                                     : (rk >= split ? hi : lo) + kswz[j];
+      dma16(lbase + src, kl + (4 * KCP * wave + 4 * j) * 256);
+    }
+  }
+  __device__ __forceinline__ void copy_v(int32_t t0, char* vl, const Slots& sl) const {
+    const int32_t bkey = (sl.plo + 1) * tpp;
+    const uint32_t lo = sl.lo + vhead + (uint32_t)(t0 - sl.plo * tpp) * 2;
+    const uint32_t hi = sl.hi + vhead + (uint32_t)(t0 - bkey) * 2;
+    const int32_t lim = nk - t0, split = bkey - t0;
+#pragma unroll
+    for (int j = 0; j < VCP; ++j) {
+      const int32_t rk = vkey[j];
+      const bool in = rk < lim;
+      const uint32_t off = in ? vlane[j] : vlane[j] - (uint32_t)rk * 2;
+      const uint32_t base = (in && rk >= split) ? hi : lo;
+      dma16(lbase + (base + off), vl + (8 * VCP * wave + 8 * j) * 128);
+    }
+  }
+};
+
+__device__ __forceinline__ void landed() {  // this wave's copies are in LDS, then everyone's
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+}
+
 // Schedule.  A unit is a (head, node, query tile) triple, numbered head-major
 // then node then query tile; a unit's key tiles are processed in order by one
 // work-group.  Units of one (head, node) are consecutive and every unit
 // starts at its node's first key tile, so the work-groups an XCD runs side
 // by side read the same K/V tiles at about the same time and share them in
-// its L2.  Equal units fill the 256 CUs in whole rounds but the last
-// U mod 256; those "tail" units are each cut into S pieces of their key
+// its L2.  Equal units fill the resident work-groups in whole rounds but the
+// last U mod R; those "tail" units are each cut into S pieces of their key
 // range, numbered piece-major (piece p of every tail unit before piece p+1),
 // so the last round is S times shorter.  Pieces leave unnormalised partials
 // that attn_combine_kernel merges in piece order.
@@ -289,211 +335,18 @@ __device__ __forceinline__ AttnItem decode_item(const AttnPlan& plan, const Attn
   return it;
 }
 
-template <int NW>
-__global__ __launch_bounds__(64 * NW, Shape<NW>::WG_PER_CU) void attn_bf16_kernel(const uint16_t* __restrict__ q,
-                                                                   uint16_t* __restrict__ o,
-                                                                   AttnGeom g, AttnPlan plan) {
-  // K buffers 0, 1 then V^T buffers 0, 1 (16 KB each)
-  __shared__ __attribute__((aligned(1024))) char smem[SMEM_BYTES];
-  constexpr int BQ = Shape<NW>::BQ;
-  const AttnItem it = decode_item(plan, g, blockIdx.x);
-  if (it.ta == it.tb) return;  // empty piece of a unit shorter than the split
-  const int32_t node = it.node, head = it.head, qt = it.qt;
-  const int32_t ta = it.ta, ntiles = it.tb;  // this item's key tiles: [ta, ntiles)
-
-  const int32_t tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int32_t hl = lane >> 5, r32 = lane & 31;
-
-  const int32_t p0 = plan.page_off[node];
-  const int32_t npages = plan.page_off[node + 1] - p0;
-  const int32_t nk = npages * g.tpp;
-  const bool ragged = it.tb == it.ntiles && (nk % BK) != 0;
-
-  // Q^T operand: lane holds Q[row][16 si + 8 hl .. +7] for si = 0..7.
-  const int32_t qrow = qt * BQ + wave * 32 + r32;
-  bf16x8 qreg[8];
-  {
-    const int32_t qrow_c = qrow < g.nq ? qrow : g.nq - 1;
-    const uint16_t* qp = q + (((size_t)node * g.nq + qrow_c) * g.n_heads + head) * HDB + 8 * hl;
-#pragma unroll
-    for (int si = 0; si < 8; ++si) {
-      const bf16x8 raw = *reinterpret_cast<const bf16x8*>(qp + 16 * si);
-#pragma unroll
-      for (int e = 0; e < 8; ++e)  // logits in log2 units: Q * scale * log2(e)
-        qreg[si][e] = static_cast<__bf16>(static_cast<float>(raw[e]) * g.scale_log2);
-    }
-  }
-
-  // Row sigma of the S^T MFMA holds key sigma: each lane's probabilities are
-  // then keys 8 hl .. 8 hl + 7 (+16) of every 32-key block -- exactly the B
-  // operand layout of the PV MFMA.
-  AttnLane L;
-  {
-    const int32_t sa = r32 >> 3, sh = (r32 >> 2) & 1, sb = r32 & 3;
-    const int32_t sigma = 16 * (sa >> 1) + 8 * sh + 4 * (sa & 1) + sb;
-#pragma unroll
-    for (int si = 0; si < 8; ++si)
-      L.koff[si] = sigma * 256 + (((2 * si + hl) ^ (sigma & 15)) << 4);
-#pragma unroll
-    for (int cm = 0; cm < 4; ++cm)
-      L.voff[cm] = r32 * 128 + (((2 * cm + hl) ^ ((r32 >> 1) & 7)) << 4);
-  }
-
-  const char* lbase = g.layer_base;
-  const uint32_t khead = (uint32_t)head * g.tpp * HDB * 2;
-  const uint32_t vhead = (uint32_t)g.kv_half + (uint32_t)head * HDB * g.tpp * 2;
-  // Tile copies.  A 64-key tile spans at most two pages (pages hold >= 64
-  // tokens), so the page of a key is chosen against one wave-uniform
-  // boundary.  Offsets are 32-bit, relative to the layer's slots (the host
-  // checks a layer fits in 4 GB); the per-page parts are wave-uniform.  Per
-  // wave: KCP copies of 4 K rows (1 KB each) and VCP copies of 8 V^T rows.  Lane
-  // (row, physical column p) fetches logical column p ^ swizzle(row).
-  constexpr int KCP = Shape<NW>::KCP, VCP = Shape<NW>::VCP;  // copies per wave
-  const int32_t krow0 = 4 * KCP * wave + (lane >> 4), kp = lane & 15;
-  const int32_t vrow0 = 8 * VCP * wave + (lane >> 3), vp = lane & 7;
-  uint32_t kswz[KCP], vlane[VCP];
-  int32_t vkey[VCP];
-#pragma unroll
-  for (int j = 0; j < KCP; ++j) {
-    const int32_t row = krow0 + 4 * j;
-    kswz[j] = (uint32_t)row * 256 + ((kp ^ (row & 15)) << 4);   // plus t0 * 256
-  }
-#pragma unroll
-  for (int j = 0; j < VCP; ++j) {
-    const int32_t d = vrow0 + 8 * j;
-    vkey[j] = 8 * (vp ^ ((d >> 1) & 7));                           // key offset in tile
-    vlane[j] = (uint32_t)d * g.tpp * 2 + (uint32_t)vkey[j] * 2;    // plus t0 * 2
-  }
-  // Page slots of a tile's keys (two scalar loads from the plan), fetched
-  // one step before the copy that uses them so their latency overlaps the
-  // step in between.  A 64-key tile spans at most two pages.
-  struct Slots {
-    uint32_t lo, hi;  // byte offsets of the slots of the tile's first page and the next one
-    int32_t plo;      // index of the tile's first page within the node
-  };
-  auto slots = [&](int32_t tile) {
-    const int32_t t0 = min(tile, it.ntiles - 1) * BK;  // clamped: prefetches past the end are unused
-    Slots sl;
-    sl.plo = (int32_t)fast_div((uint32_t)t0, g.tpp_div);
-    const int32_t phi = sl.plo + 1 < npages ? sl.plo + 1 : sl.plo;
-    sl.lo = (uint32_t)plan.page_slot[p0 + sl.plo] * (uint32_t)g.slot_bytes;
-    sl.hi = (uint32_t)plan.page_slot[p0 + phi] * (uint32_t)g.slot_bytes;
-    return sl;
-  };
-  struct PageSplit {
-    uint32_t lo, hi;  // layer-relative byte offset of key t0 on page lo / hi (head included)
-    int32_t split;    // tile-relative first key on page hi
-  };
-  auto pages = [&](const Slots& sl, int32_t t0, uint32_t head_off, uint32_t row_bytes) {
-    const int32_t bkey = (sl.plo + 1) * g.tpp;
-    PageSplit ps;
-    ps.lo = sl.lo + head_off - (uint32_t)sl.plo * g.tpp * row_bytes + (uint32_t)t0 * row_bytes;
-    ps.hi = sl.hi + head_off - (uint32_t)bkey * row_bytes + (uint32_t)t0 * row_bytes;
-    ps.split = bkey - t0;
-    return ps;
-  };
-  // Keys past the node's end (ragged last tile) fetch the tile's first key
-  // instead: valid memory, and its probability is masked to zero anyway.
-  auto copy_k = [&](int32_t tile, int buf, const Slots& sl) {
-    const int32_t t0 = tile * BK;
-    const PageSplit ps = pages(sl, t0, khead, 256);
-    const int32_t lim = nk - t0;
-    char* kl = smem + buf * KT_BYTES;
-#pragma unroll
-    for (int j = 0; j < KCP; ++j) {
-      const int32_t rk = krow0 + 4 * j;  // tile-relative key
-      const bool in = rk < lim;
-      const uint32_t lo = in ? kswz[j] : kswz[j] - (uint32_t)rk * 256;
-      const uint32_t base = (in && rk >= ps.split) ? ps.hi : ps.lo;
-      dma16(lbase + (base + lo), kl + (4 * KCP * wave + 4 * j) * 256);
-    }
-  };
-  auto copy_v = [&](int32_t tile, int buf, const Slots& sl) {
-    const int32_t t0 = tile * BK;
-    const PageSplit ps = pages(sl, t0, vhead, 2);
-    const int32_t lim = nk - t0;
-    char* vl = smem + 2 * KT_BYTES + buf * VT_BYTES;
-#pragma unroll
-    for (int j = 0; j < VCP; ++j) {
-      const int32_t rk = vkey[j];
-      const bool in = rk < lim;
-      const uint32_t lo = in ? vlane[j] : vlane[j] - (uint32_t)rk * 2;
-      const uint32_t base = (in && rk >= ps.split) ? ps.hi : ps.lo;
-      dma16(lbase + (base + lo), vl + (8 * VCP * wave + 8 * j) * 128);
-    }
-  };
-  auto landed = [&]() {  // this wave's copies are in LDS, then everyone's
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-  };
-
-  f32x16 oacc[4];
-#pragma unroll
-  for (int db = 0; db < 4; ++db) oacc[db] = f32x16{};
-  float m_run = 0.f, l_run = 0.f;
-  // prologue: K(ta), V(ta), K(ta+1) in flight; S(ta) = K(ta) Q^T; m = its exact max
-  {
-    const Slots s0 = slots(ta);
-    copy_k(ta, 0, s0);
-    copy_v(ta, 0, s0);
-    if (ta + 1 < ntiles) copy_k(ta + 1, 1, slots(ta + 1));
-  }
-  landed();
-  f32x16 s[2];
-  qk_tile(smem, L, qreg, s, 0.f);
-  if (ta + 1 == ntiles && ragged) {
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i)
-        if (ta * BK + 32 * kb + 16 * (i >> 3) + 8 * hl + (i & 7) >= nk) s[kb][i] = -INFINITY;
-  }
-  m_run = tile_max(s);
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) s[kb][i] -= m_run;
-  __syncthreads();  // every wave has read K(ta) before K(ta+2) is copied over it
-
-  // iteration t (buffer parity counted from ta): copy K(t+2) over K(t) and
-  // V(t+1) over V(t-1), then step t
-  int32_t t = ta;
-  Slots sk = slots(ta + 2), sv = slots(ta + 1);  // for the next copies of K and V
-  for (; t + 2 < ntiles; t += 2) {
-    copy_k(t + 2, 0, sk);
-    copy_v(t + 1, 1, sv);
-    sk = slots(t + 3);
-    sv = slots(t + 2);
-    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
-    landed();
-    if (t + 3 < ntiles) copy_k(t + 3, 1, sk);
-    copy_v(t + 2, 0, sv);
-    sk = slots(t + 4);
-    sv = slots(t + 3);
-    attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m_run, l_run, (t + 1) * BK, nk, hl);
-    landed();
-  }
-  if (t + 1 < ntiles) {  // two tiles left, parity 0
-    copy_v(t + 1, 1, sv);
-    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
-    landed();
-    ++t;
-    if (ragged)
-      attn_step<0, 1, false, true>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
-    else
-      attn_step<0, 1, false, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
-  } else {               // one tile left, parity 0 (masking twice is harmless)
-    if (ragged)
-      attn_step<1, 0, false, true>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
-    else
-      attn_step<1, 0, false, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
-  }
-
+// The result of a work item for one 32-query block: the normalised output of
+// a whole unit, or a piece's unnormalised partial with its max and sum.
+template <int BQ>
+__device__ __forceinline__ void store_rows(const AttnItem& it, const AttnGeom& g, uint16_t* o,
+                                           const f32x16 (&oacc)[4], float m_run, float l_run,
+                                           int32_t lrow, int32_t hl) {
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (it.slot < 0) {  // a whole unit: the final output
+  if (it.slot < 0) {
     const float inv = 1.f / l_tot;
+    const int32_t qrow = it.qt * BQ + lrow;
     if (qrow < g.nq) {
-      uint16_t* op = o + (((size_t)node * g.nq + qrow) * g.n_heads + head) * HDB;
+      uint16_t* op = o + (((size_t)it.node * g.nq + qrow) * g.n_heads + it.head) * HDB;
 #pragma unroll
       for (int db = 0; db < 4; ++db)
 #pragma unroll
@@ -505,8 +358,7 @@ __global__ __launch_bounds__(64 * NW, Shape<NW>::WG_PER_CU) void attn_bf16_kerne
           *reinterpret_cast<u32x2*>(op + d) = v;
         }
     }
-  } else {            // a piece: unnormalised partial, its max (log2 units) and sum
-    const int32_t lrow = wave * 32 + r32;
+  } else {
     float* po = g.part_o + ((size_t)it.slot * BQ + lrow) * HDB;
 #pragma unroll
     for (int db = 0; db < 4; ++db)
@@ -523,13 +375,166 @@ __global__ __launch_bounds__(64 * NW, Shape<NW>::WG_PER_CU) void attn_bf16_kerne
   }
 }
 
+// S^T blocks of one tile, s[kb] = K_kb Q^T - m for the two 32-key halves.
+__device__ __forceinline__ void qk_tile(const char* kl, const AttnLane& L, const bf16x8 (&qreg)[8],
+                                        f32x16 (&s)[2], float m) {
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s[kb][i] = -m;
+#pragma unroll
+    for (int si = 0; si < 8; ++si) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + L.koff[si] + kb * 8192);
+      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[si], s[kb], 0, 0, 0);
+    }
+  }
+}
+
+// One step of the software-pipelined loop, for tile t: probabilities of
+// S(t) (held in s), the next tile's S(t+1) = K(t+1) Q^T - m on the matrix
+// cores while the exponentials of tile t run on the vector ALUs, then
+// O^T += V(t)^T P(t).  K runs one tile ahead of V: K(t+1) sits in K buffer
+// KN, V(t) in V buffer VC.
+template <int KN, int VC, bool NEXT, bool MASK>
+__device__ __forceinline__ void attn_step(const char* smem, const AttnLane& L, const bf16x8 (&qreg)[8],
+                                          f32x16 (&oacc)[4], f32x16 (&s)[2], float& m_run,
+                                          float& l_run, int32_t t0, int32_t nk, int32_t hl) {
+  if constexpr (MASK) {
+    mask32(s[0], t0, nk, hl);
+    mask32(s[1], t0 + 32, nk, hl);
+  }
+  bf16x8 pb[2][2];
+  float l_tile = probs32(s[0], pb[0]) + probs32(s[1], pb[1]);
+  f32x16 sn[2];
+  if constexpr (NEXT) qk_tile(smem + KN * KT_BYTES, L, qreg, sn, m_run);
+  if (__builtin_amdgcn_ballot_w64(!(l_tile < GROW_LIMIT))) {
+    // rare: raise the running maximum to this tile's and redo the tile (the
+    // next tile's logits were offset by the old maximum).  The opaque
+    // statement keeps this a wave-uniform branch.
+    asm volatile("" ::: "memory");
+    const float grow = fmaxf(fmaxf(col_max16(s[0]), col_max16(s[1])), 0.f);
+    const float alpha = __builtin_amdgcn_exp2f(-grow);
+    m_run += grow;
+    l_run *= alpha;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        s[kb][i] -= grow;
+        if constexpr (NEXT) sn[kb][i] -= grow;
+      }
+    l_tile = probs32(s[0], pb[0]) + probs32(s[1], pb[1]);
+  }
+  l_run += l_tile;
+  const char* vl = smem + 2 * KT_BYTES + VC * VT_BYTES;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int mm = 0; mm < 2; ++mm)
+#pragma unroll
+      for (int db = 0; db < 4; ++db) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(vl + L.voff[2 * kb + mm] + db * 4096);
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kb][mm], oacc[db], 0, 0, 0);
+      }
+  if constexpr (NEXT) {
+    s[0] = sn[0];
+    s[1] = sn[1];
+  }
+}
+
+// NW = 8: 256 queries per work-group, one work-group per CU; NW = 4: 128
+// queries, two per CU.  Both keep two waves per SIMD.
+template <int NW>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16_t* __restrict__ q,
+                                                                    uint16_t* __restrict__ o, AttnGeom g,
+                                                                    AttnPlan plan) {
+  constexpr int BQ = 32 * NW;
+  // K buffers 0, 1 then V^T buffers 0, 1 (16 KB each)
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM_BYTES];
+  const AttnItem it = decode_item(plan, g, blockIdx.x);
+  if (it.ta == it.tb) return;  // empty piece of a unit shorter than the split
+  const int32_t ta = it.ta, ntiles = it.tb;  // this item's key tiles: [ta, ntiles)
+  const int32_t tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int32_t hl = lane >> 5, r32 = lane & 31;
+  const KvTiles<NW> kv(plan, g, it.node, it.head, wave, lane);
+  const int32_t nk = kv.nk;
+  const bool ragged = it.tb == it.ntiles && (nk % BK) != 0;
+  const int32_t lrow = wave * 32 + r32;
+  bf16x8 qreg[8];
+  load_q(q, g, it.node, it.head, it.qt * BQ + lrow, hl, qreg);
+  const AttnLane L = attn_lane(r32, hl);
+
+  f32x16 oacc[4];
+#pragma unroll
+  for (int db = 0; db < 4; ++db) oacc[db] = f32x16{};
+  float m_run = 0.f, l_run = 0.f;
+  // prologue: K(ta), V(ta), K(ta+1) in flight; S(ta) = K(ta) Q^T; m = its exact max
+  {
+    const typename KvTiles<NW>::Slots s0 = kv.slots(ta * BK);
+    kv.copy_k(ta * BK, smem, s0);
+    kv.copy_v(ta * BK, smem + 2 * KT_BYTES, s0);
+    if (ta + 1 < ntiles) kv.copy_k((ta + 1) * BK, smem + KT_BYTES, kv.slots((ta + 1) * BK));
+  }
+  landed();
+  f32x16 s[2];
+  qk_tile(smem, L, qreg, s, 0.f);
+  if (ta + 1 == ntiles && ragged) {
+    mask32(s[0], ta * BK, nk, hl);
+    mask32(s[1], ta * BK + 32, nk, hl);
+  }
+  m_run = fmaxf(col_max16(s[0]), col_max16(s[1]));
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s[kb][i] -= m_run;
+  __syncthreads();  // every wave has read K(ta) before K(ta+2) is copied over it
+
+  // iteration t (buffer parity counted from ta): copy K(t+2) over K(t) and
+  // V(t+1) over V(t-1), then step t
+  int32_t t = ta;
+  typename KvTiles<NW>::Slots sk = kv.slots(min(ta + 2, it.ntiles - 1) * BK);
+  typename KvTiles<NW>::Slots sv = kv.slots(min(ta + 1, it.ntiles - 1) * BK);
+  for (; t + 2 < ntiles; t += 2) {
+    kv.copy_k((t + 2) * BK, smem, sk);
+    kv.copy_v((t + 1) * BK, smem + 2 * KT_BYTES + VT_BYTES, sv);
+    sk = kv.slots(min(t + 3, it.ntiles - 1) * BK);
+    sv = kv.slots(min(t + 2, it.ntiles - 1) * BK);
+    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
+    landed();
+    if (t + 3 < ntiles) kv.copy_k((t + 3) * BK, smem + KT_BYTES, sk);
+    kv.copy_v((t + 2) * BK, smem + 2 * KT_BYTES, sv);
+    sk = kv.slots(min(t + 4, it.ntiles - 1) * BK);
+    sv = kv.slots(min(t + 3, it.ntiles - 1) * BK);
+    attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m_run, l_run, (t + 1) * BK, nk, hl);
+    landed();
+  }
+  if (t + 1 < ntiles) {  // two tiles left, parity 0
+    kv.copy_v((t + 1) * BK, smem + 2 * KT_BYTES + VT_BYTES, sv);
+    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
+    landed();
+    ++t;
+    if (ragged)
+      attn_step<0, 1, false, true>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
+    else
+      attn_step<0, 1, false, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
+  } else {               // one tile left, parity 0 (masking twice is harmless)
+    if (ragged)
+      attn_step<1, 0, false, true>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
+    else
+      attn_step<1, 0, false, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
+  }
+  store_rows<BQ>(it, g, o, oacc, m_run, l_run, lrow, hl);
+}
+
 // Merges the pieces of each tail unit, in piece order: one work-group per
 // tail unit, one thread per query row.  With m = max m_p:
 //   O = sum_p 2^(m_p - m) O_p / sum_p 2^(m_p - m) l_p.
-template <int NW>
-__global__ __launch_bounds__(Shape<NW>::BQ) void attn_combine_kernel(uint16_t* __restrict__ o, AttnGeom g,
-                                                                     AttnPlan plan) {
-  constexpr int BQ = Shape<NW>::BQ;
+template <int BQ>
+__global__ __launch_bounds__(BQ) void attn_combine_kernel(uint16_t* __restrict__ o, AttnGeom g, AttnPlan plan) {
   const int32_t tu = blockIdx.x;
   const int32_t unit = g.whole_units + tu;
   const int32_t qt = unit % g.n_qtiles;
@@ -580,14 +585,12 @@ __global__ __launch_bounds__(Shape<NW>::BQ) void attn_combine_kernel(uint16_t* _
 // kAttnMaxPieces pieces and no more pieces than the shortest node has key
 // tiles.
 struct TailSplit {
-  int32_t nw;       // waves per work-group of the instantiation used
+  int32_t bq;       // queries per work-group of the shape used (128 or 256)
   int32_t whole, tail, split;
 };
-static int32_t waves_for(const sc_plan* p) { return p->nq <= Shape<4>::BQ ? 4 : 8; }
 static TailSplit tail_split(const sc_plan* p, const sc_cache* c) {
   const int32_t n = (int32_t)p->nodes.size();
-  const int32_t nw = waves_for(p);
-  const int32_t bq = 32 * nw;
+  const int32_t bq = p->nq <= BQ_SMALL ? BQ_SMALL : BQ_MAX;
   const int32_t n_qtiles = (p->nq + bq - 1) / bq;
   const int32_t units = n * c->d.n_heads * n_qtiles;
   int64_t tiles = 0;
@@ -600,8 +603,8 @@ static TailSplit tail_split(const sc_plan* p, const sc_cache* c) {
   }
   const double mean_tiles = (double)tiles / std::max(n, 1);
   TailSplit ts;
-  ts.nw = nw;
-  const int32_t slots = kAttnCUs * (8 / nw);  // work-groups resident at once
+  ts.bq = bq;
+  const int32_t slots = kAttnCUs * (BQ_MAX / bq);  // work-groups resident at once
   ts.tail = units % slots;
   ts.whole = units - ts.tail;
   ts.split = 1;
@@ -626,7 +629,7 @@ size_t attention_workspace_bytes(const sc_plan* p, const sc_cache* c) {
   if (c->d.dtype != SC_DTYPE_BF16 || p->nodes.empty()) return 0;
   const TailSplit ts = tail_split(p, c);
   if (ts.split == 1) return 0;
-  return (size_t)ts.tail * ts.split * (32 * ts.nw) * (HDB + 2) * sizeof(float);
+  return (size_t)ts.tail * ts.split * ts.bq * (HDB + 2) * sizeof(float);
 }
 
 size_t attention_workspace_bound() { return (size_t)kAttnMaxPieces * BQ_MAX * (HDB + 2) * sizeof(float); }
@@ -678,7 +681,7 @@ int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const v
     return fail(SC_EINVAL, "attention workspace of %zu bytes, need %zu", ws_bytes, need);
   if (reinterpret_cast<uintptr_t>(ws) & 15) return fail(SC_EINVAL, "workspace must be 16-byte aligned");
   const TailSplit ts = tail_split(p, c);
-  const int32_t bq = 32 * ts.nw;
+  const int32_t bq = ts.bq;
   g.n_qtiles = (p->nq + bq - 1) / bq;
   g.whole_units = ts.whole;
   g.tail_units = ts.tail;
@@ -693,18 +696,18 @@ int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const v
   const uint16_t* qb = static_cast<const uint16_t*>(q);
   uint16_t* ob = static_cast<uint16_t*>(o);
   timer_begin(TK_ATTENTION, stream);
-  if (ts.nw == 4)
+  if (bq == BQ_SMALL)
     hipLaunchKernelGGL(attn_bf16_kernel<4>, dim3(items), dim3(256), 0, stream, qb, ob, g, plan);
   else
     hipLaunchKernelGGL(attn_bf16_kernel<8>, dim3(items), dim3(512), 0, stream, qb, ob, g, plan);
   timer_end(TK_ATTENTION, stream);
   if (g.tail_units) {
     timer_begin(TK_ATTN_COMBINE, stream);
-    if (ts.nw == 4)
-      hipLaunchKernelGGL(attn_combine_kernel<4>, dim3((uint32_t)g.tail_units), dim3(128), 0, stream,
+    if (bq == BQ_SMALL)
+      hipLaunchKernelGGL(attn_combine_kernel<BQ_SMALL>, dim3((uint32_t)g.tail_units), dim3(BQ_SMALL), 0, stream,
                          ob, g, plan);
     else
-      hipLaunchKernelGGL(attn_combine_kernel<8>, dim3((uint32_t)g.tail_units), dim3(256), 0, stream,
+      hipLaunchKernelGGL(attn_combine_kernel<BQ_MAX>, dim3((uint32_t)g.tail_units), dim3(BQ_MAX), 0, stream,
                          ob, g, plan);
     timer_end(TK_ATTN_COMBINE, stream);
   }

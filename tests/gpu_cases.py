@@ -51,7 +51,7 @@ class AttnCase:
     unreserved slots are NaN, so a stray page read shows up in the output)."""
 
     def __init__(self, geo, dtype, kind, pack, resident, seed=0, n_slots=None, value_fn=None,
-                 n_layers=1, layer=0, policy_kw=None):
+                 n_layers=1, layer=0, policy_kw=None, key_fn=None, query_fn=None):
         torch = torch_mod()
         self.geo, self.dtype, self.kind, self.pack, self.seed = geo, dtype, kind, list(pack), seed
         self.policy_kw = dict(policy_kw or {})  # phi_table / r_mask / n_chunks
@@ -68,6 +68,7 @@ class AttnCase:
         gen = normal_parallel if big else normal
         self.kv: Dict[Tuple[int, int], Tuple[np.ndarray, np.ndarray]] = {}
         self._dev = []
+        self.key_fn = key_fn
         for st in resident:
             self._append(st, gen, shape, value_fn)
         self.sel = sc.sc_selection_build(kind, geo.K, geo.W, self.pack, **self.policy_kw)
@@ -78,7 +79,7 @@ class AttnCase:
         qs, self.q = [], {}
         for i, st in enumerate(self.pack):
             qf = gen(shape, (seed, TAG_Q) + st)
-            qs.append(qf)
+            qs.append(qf if query_fn is None else query_fn(st, qf))
         qt, qv = to_device(np.concatenate(qs, axis=0), dtype)
         self.q_dev = qt
         for i in range(len(self.pack)):
@@ -88,6 +89,8 @@ class AttnCase:
 
     def _append(self, st, gen, shape, value_fn):
         kf = gen(shape, (self.seed, TAG_K) + tuple(st))
+        if self.key_fn is not None:
+            kf = self.key_fn(st, kf)
         vf = gen(shape, (self.seed, TAG_V) + tuple(st)) if value_fn is None else value_fn(st)
         kd, kv = to_device(kf, self.dtype)
         vd, vv = to_device(vf, self.dtype)

@@ -206,6 +206,38 @@ def test_negative_controls_fail_gates():
             bf16_gates(out[node], want, name)
 
 
+@pytest.mark.parametrize("geo", [SMALL, SHORT], ids=["256-query", "128-query"])
+def test_logits_far_above_first_tile(geo):
+    """K channel 0 is 0 on each node's first page and 600 on most later
+    pages (first page of every state for three-frame chunks; chunks 0..3,
+    the first pages of this pack's nodes, for one-frame chunks), with Q
+    channel 0 = 1: later logits sit about 76 (log2 units) above the maximum
+    of a node's first key tile, past the kernel's 2^64 overflow guard, which
+    raises the running maximum and rescales the accumulated output.  The
+    softmax is still the plain one: compared with the oracle."""
+    kind, pack, resident = SMALL_PACKS[0]
+    tpp = geo.tokens_per_page
+
+    def key_fn(st, k):
+        k = k.copy()
+        k[:, :, 0] = 600.0
+        if geo.frames_per_chunk > 1:
+            k[:tpp, :, 0] = 0.0
+        elif st[0] < 4:
+            k[:, :, 0] = 0.0
+        return k
+
+    def query_fn(st, q):
+        q = q.copy()
+        q[:, :, 0] = 1.0
+        return q
+    case = AttnCase(geo, sc.SC_DTYPE_BF16, kind, pack, resident, seed=11, key_fn=key_fn,
+                    query_fn=query_fn)
+    out = case.run()
+    for i in range(len(pack)):
+        bf16_gates(out[i], case.oracle(i), f"large logits node {pack[i]}")
+
+
 WAN_CASES = [cfg2_clean(4), cfg3_same(2), cfg4_prog(False), cfg4_prog(True)]
 
 
