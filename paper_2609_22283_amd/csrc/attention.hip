@@ -102,12 +102,15 @@ constexpr int VT_BYTES = HDB * BK * 2;  // 16 KB
 constexpr int SMEM_BYTES = 2 * (KT_BYTES + VT_BYTES);
 constexpr int BQ_SMALL = 128, BQ_MAX = 256;  // queries per work-group of the two shapes
 // Softmax bookkeeping.  Q is pre-scaled by scale*log2(e), so S is in log2
-// units, and each S tile starts its accumulation at -m (the running
-// maximum): p = exp2(S) directly.  m is the exact maximum of the first tile
-// and is raised only when a later tile's probabilities overflow 2^64 (their
-// sum is checked); until then p may exceed 1, which fp32 sums and bf16
-// products represent with the same relative precision.
-constexpr float GROW_LIMIT = 18446744073709551616.0f;  // 2^64
+// units, and each S tile starts its accumulation at -m: p = exp2(S)
+// directly.  m is the exact maximum of the work item's first tile and is
+// never raised inside the loop: later probabilities may exceed 1, which fp32
+// sums and bf16 products represent with the same relative precision, up to
+// a guard of 2^64 on each lane's tile sum.  A work-group in which any wave
+// reaches the guard (logits more than 64 log2 units above the first tile's
+// maximum) redoes its item exactly in two passes (attn_exact).  Rescaling in
+// place would keep the accumulators and the recomputation live in the loop.
+constexpr float P_GUARD = 18446744073709551616.0f;  // 2^64
 
 struct AttnLane {
   // per-lane LDS read offsets (bytes) inside one buffer
@@ -392,43 +395,22 @@ __device__ __forceinline__ void qk_tile(const char* kl, const AttnLane& L, const
 
 // One step of the software-pipelined loop, for tile t: probabilities of
 // S(t) (held in s), the next tile's S(t+1) = K(t+1) Q^T - m on the matrix
-// cores while the exponentials of tile t run on the vector ALUs, then
-// O^T += V(t)^T P(t).  K runs one tile ahead of V: K(t+1) sits in K buffer
-// KN, V(t) in V buffer VC.
+// cores while the exponentials of tile t run on the vector ALUs, the guard
+// check, then O^T += V(t)^T P(t).  K runs one tile ahead of V: K(t+1) sits
+// in K buffer KN, V(t) in V buffer VC.
 template <int KN, int VC, bool NEXT, bool MASK>
 __device__ __forceinline__ void attn_step(const char* smem, const AttnLane& L, const bf16x8 (&qreg)[8],
                                           f32x16 (&oacc)[4], f32x16 (&s)[2], float& m_run,
-                                          float& l_run, int32_t t0, int32_t nk, int32_t hl) {
+                                          float& l_run, bool& bad, int32_t t0, int32_t nk, int32_t hl) {
   if constexpr (MASK) {
     mask32(s[0], t0, nk, hl);
     mask32(s[1], t0 + 32, nk, hl);
   }
   bf16x8 pb[2][2];
-  float l_tile = probs32(s[0], pb[0]) + probs32(s[1], pb[1]);
+  const float l_tile = probs32(s[0], pb[0]) + probs32(s[1], pb[1]);
   f32x16 sn[2];
   if constexpr (NEXT) qk_tile(smem + KN * KT_BYTES, L, qreg, sn, m_run);
-  if (__builtin_amdgcn_ballot_w64(!(l_tile < GROW_LIMIT))) {
-    // rare: raise the running maximum to this tile's and redo the tile (the
-    // next tile's logits were offset by the old maximum).  The opaque
-    // statement keeps this a wave-uniform branch.
-    asm volatile("" ::: "memory");
-    const float grow = fmaxf(fmaxf(col_max16(s[0]), col_max16(s[1])), 0.f);
-    const float alpha = __builtin_amdgcn_exp2f(-grow);
-    m_run += grow;
-    l_run *= alpha;
-#pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        s[kb][i] -= grow;
-        if constexpr (NEXT) sn[kb][i] -= grow;
-      }
-    l_tile = probs32(s[0], pb[0]) + probs32(s[1], pb[1]);
-  }
+  bad |= __builtin_amdgcn_ballot_w64(!(l_tile < P_GUARD)) != 0;  // also NaN / inf
   l_run += l_tile;
   const char* vl = smem + 2 * KT_BYTES + VC * VT_BYTES;
 #pragma unroll
@@ -446,6 +428,56 @@ __device__ __forceinline__ void attn_step(const char* smem, const AttnLane& L, c
   }
 }
 
+// Exact two-pass redo of a work item in which a wave reached the 2^64 guard:
+// each query's maximum logit over the item's keys, then the softmax from
+// that maximum (every p <= 1).  Single-buffered K and V tiles; slow, and
+// taken only for logits far above the first tile's maximum.
+template <int NW>
+__device__ __forceinline__ void attn_exact(char* smem, const KvTiles<NW>& kv, const AttnLane& L,
+                                           const bf16x8 (&qreg)[8], f32x16 (&oacc)[4], float& m_run,
+                                           float& l_run, int32_t ta, int32_t ntiles, int32_t hl) {
+  char* const kl = smem;
+  char* const vl = smem + 2 * KT_BYTES;
+  const int32_t nk = kv.nk;
+  float mx = -INFINITY;
+  for (int32_t t = ta; t < ntiles; ++t) {
+    kv.copy_k(t * BK, kl, kv.slots(t * BK));
+    landed();
+    f32x16 s[2];
+    qk_tile(kl, L, qreg, s, 0.f);
+    mask32(s[0], t * BK, nk, hl);
+    mask32(s[1], t * BK + 32, nk, hl);
+    mx = fmaxf(mx, fmaxf(col_max16(s[0]), col_max16(s[1])));
+    __syncthreads();
+  }
+  m_run = mx;
+  l_run = 0.f;
+#pragma unroll
+  for (int db = 0; db < 4; ++db) oacc[db] = f32x16{};
+  for (int32_t t = ta; t < ntiles; ++t) {
+    const typename KvTiles<NW>::Slots sl = kv.slots(t * BK);
+    kv.copy_k(t * BK, kl, sl);
+    kv.copy_v(t * BK, vl, sl);
+    landed();
+    f32x16 s[2];
+    qk_tile(kl, L, qreg, s, m_run);
+    mask32(s[0], t * BK, nk, hl);
+    mask32(s[1], t * BK + 32, nk, hl);
+    bf16x8 pb[2][2];
+    l_run += probs32(s[0], pb[0]) + probs32(s[1], pb[1]);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int mm = 0; mm < 2; ++mm)
+#pragma unroll
+        for (int db = 0; db < 4; ++db) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(vl + L.voff[2 * kb + mm] + db * 4096);
+          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kb][mm], oacc[db], 0, 0, 0);
+        }
+    __syncthreads();
+  }
+}
+
 // NW = 8: 256 queries per work-group, one work-group per CU; NW = 4: 128
 // queries, two per CU.  Both keep two waves per SIMD.
 template <int NW>
@@ -455,11 +487,14 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
   constexpr int BQ = 32 * NW;
   // K buffers 0, 1 then V^T buffers 0, 1 (16 KB each)
   __shared__ __attribute__((aligned(1024))) char smem[SMEM_BYTES];
+  __shared__ int32_t any_bad;
+  bool bad = false;
   const AttnItem it = decode_item(plan, g, blockIdx.x);
   if (it.ta == it.tb) return;  // empty piece of a unit shorter than the split
   const int32_t ta = it.ta, ntiles = it.tb;  // this item's key tiles: [ta, ntiles)
   const int32_t tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int32_t hl = lane >> 5, r32 = lane & 31;
+  if (tid == 0) any_bad = 0;
   const KvTiles<NW> kv(plan, g, it.node, it.head, wave, lane);
   const int32_t nk = kv.nk;
   const bool ragged = it.tb == it.ntiles && (nk % BK) != 0;
@@ -503,30 +538,33 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
     kv.copy_v((t + 1) * BK, smem + 2 * KT_BYTES + VT_BYTES, sv);
     sk = kv.slots(min(t + 3, it.ntiles - 1) * BK);
     sv = kv.slots(min(t + 2, it.ntiles - 1) * BK);
-    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
+    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, bad, t * BK, nk, hl);
     landed();
     if (t + 3 < ntiles) kv.copy_k((t + 3) * BK, smem + KT_BYTES, sk);
     kv.copy_v((t + 2) * BK, smem + 2 * KT_BYTES, sv);
     sk = kv.slots(min(t + 4, it.ntiles - 1) * BK);
     sv = kv.slots(min(t + 3, it.ntiles - 1) * BK);
-    attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m_run, l_run, (t + 1) * BK, nk, hl);
+    attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m_run, l_run, bad, (t + 1) * BK, nk, hl);
     landed();
   }
   if (t + 1 < ntiles) {  // two tiles left, parity 0
     kv.copy_v((t + 1) * BK, smem + 2 * KT_BYTES + VT_BYTES, sv);
-    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
+    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, bad, t * BK, nk, hl);
     landed();
     ++t;
     if (ragged)
-      attn_step<0, 1, false, true>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
+      attn_step<0, 1, false, true>(smem, L, qreg, oacc, s, m_run, l_run, bad, t * BK, nk, hl);
     else
-      attn_step<0, 1, false, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
+      attn_step<0, 1, false, false>(smem, L, qreg, oacc, s, m_run, l_run, bad, t * BK, nk, hl);
   } else {               // one tile left, parity 0 (masking twice is harmless)
     if (ragged)
-      attn_step<1, 0, false, true>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
+      attn_step<1, 0, false, true>(smem, L, qreg, oacc, s, m_run, l_run, bad, t * BK, nk, hl);
     else
-      attn_step<1, 0, false, false>(smem, L, qreg, oacc, s, m_run, l_run, t * BK, nk, hl);
+      attn_step<1, 0, false, false>(smem, L, qreg, oacc, s, m_run, l_run, bad, t * BK, nk, hl);
   }
+  if (bad && lane == 0) atomicOr(&any_bad, 1);
+  __syncthreads();  // every wave is done with the ring; any_bad is final
+  if (any_bad) attn_exact(smem, kv, L, qreg, oacc, m_run, l_run, ta, ntiles, hl);
   store_rows<BQ>(it, g, o, oacc, m_run, l_run, lrow, hl);
 }
 

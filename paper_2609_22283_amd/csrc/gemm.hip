@@ -16,8 +16,12 @@
 namespace sc {
 
 constexpr int GBM = 256, GBN = 256, GBK = 64;
-constexpr int GWM = 128, GWN = 64;
-constexpr int G_THREADS = 512;
+constexpr int GWM = 128;
+constexpr int G_NW = 8;               // waves per work-group, two per SIMD
+constexpr int G_THREADS = 64 * G_NW;
+constexpr int GWN = 2 * GBN / G_NW;   // tokens per wave tile
+constexpr int GNB = GWN / 32;         // 32-token MFMA blocks per wave
+constexpr int GROWS = GBM / G_NW;     // operand rows each wave copies per stage
 constexpr int G_TILE_BYTES = GBM * GBK * 2;  // 32 KB per operand per stage
 
 // GELU_tanh(x) = 0.5 x (1 + tanh(u)) = x * sigmoid(2 u), u = sqrt(2/pi) (x + 0.044715 x^3),
@@ -60,14 +64,15 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   const int32_t hl = lane >> 5, r32 = lane & 31;
   const int32_t wf = (wave & 1) * GWM, wt = (wave >> 1) * GWN;
 
-  // copies: each wave moves rows [32 wave, 32 wave + 32) of both operand
-  // tiles, 8 rows (1 KB) per instruction; lane (row, p) fetches column
-  // p ^ ((row >> 1) & 7).  Byte offsets are fixed per lane; the k offset is
-  // folded into the (wave-uniform) base pointer.
-  uint32_t woff[4], xoff[4];
+  // copies: each wave moves rows [GROWS wave, GROWS wave + GROWS) of both
+  // operand tiles, 8 rows (1 KB) per instruction; lane (row, p) fetches
+  // column p ^ ((row >> 1) & 7).  Byte offsets are fixed per lane; the k
+  // offset is folded into the (wave-uniform) base pointer.
+  constexpr int NCP = GROWS / 8;
+  uint32_t woff[NCP], xoff[NCP];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int32_t row = 32 * wave + 8 * j + (lane >> 3);
+  for (int j = 0; j < NCP; ++j) {
+    const int32_t row = GROWS * wave + 8 * j + (lane >> 3);
     const int32_t col = (lane & 7) ^ ((row >> 1) & 7);
     woff[j] = ((uint32_t)(f0 + row) * Kd + col * 8) * 2;
     const int32_t trow = min(t0 + row, T - 1);
@@ -81,9 +86,9 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
     const char* wk = wbase + (size_t)k0 * 2;
     const char* xk = xbase + (size_t)k0 * 2;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      gdma16(wk + woff[j], a + (32 * wave + 8 * j) * 128);
-      gdma16(xk + xoff[j], b + (32 * wave + 8 * j) * 128);
+    for (int j = 0; j < NCP; ++j) {
+      gdma16(wk + woff[j], a + (GROWS * wave + 8 * j) * 128);
+      gdma16(xk + xoff[j], b + (GROWS * wave + 8 * j) * 128);
     }
   };
   auto landed = [&]() {
@@ -92,25 +97,25 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   };
 
   // LDS read offsets of this lane's fragments (16-byte column 2 s + hl)
-  uint32_t aoff[4], boff[2];
+  uint32_t aoff[4], boff[GNB];
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) aoff[mb] = (uint32_t)(wf + 32 * mb + r32) * 128;
 #pragma unroll
-  for (int nb = 0; nb < 2; ++nb) boff[nb] = (uint32_t)(wt + 32 * nb + r32) * 128;
+  for (int nb = 0; nb < GNB; ++nb) boff[nb] = (uint32_t)(wt + 32 * nb + r32) * 128;
   const int32_t swz = (r32 >> 1) & 7;  // rows wf + 32 mb + r32 share (row >> 1) & 7
 
-  f32x16 acc[4][2];
+  f32x16 acc[4][GNB];
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) acc[mb][nb] = f32x16{};
+    for (int nb = 0; nb < GNB; ++nb) acc[mb][nb] = f32x16{};
 
-  auto frags = [&](const char* a, const char* b, int s, bf16x8 (&af)[4], bf16x8 (&bf)[2]) {
+  auto frags = [&](const char* a, const char* b, int s, bf16x8 (&af)[4], bf16x8 (&bf)[GNB]) {
     const uint32_t c = (uint32_t)(((2 * s + hl) ^ swz) << 4);
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb) af[mb] = *reinterpret_cast<const bf16x8*>(a + aoff[mb] + c);
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) bf[nb] = *reinterpret_cast<const bf16x8*>(b + boff[nb] + c);
+    for (int nb = 0; nb < GNB; ++nb) bf[nb] = *reinterpret_cast<const bf16x8*>(b + boff[nb] + c);
   };
 
   const int32_t nk = Kd / GBK;
@@ -120,7 +125,7 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
     if (kt + 1 < nk) issue((kt + 1) * GBK, (kt + 1) & 1);
     const char* a = smem + (kt & 1) * 2 * G_TILE_BYTES;
     const char* b = a + G_TILE_BYTES;
-    bf16x8 af[2][4], bfr[2][2];
+    bf16x8 af[2][4], bfr[2][GNB];
     frags(a, b, 0, af[0], bfr[0]);
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
@@ -128,7 +133,7 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < GNB; ++nb)
           acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s & 1][mb], bfr[s & 1][nb],
                                                                 acc[mb][nb], 0, 0, 0);
     }
@@ -145,7 +150,7 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
     const int32_t head = hf0 / ep.head_dim;
     const int32_t dbase = hf0 - head * ep.head_dim + 4 * hl;
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
+    for (int nb = 0; nb < GNB; ++nb) {
       const int32_t t = t0 + wt + 32 * nb + r32;
       if (t >= T) continue;
       const int32_t node = t / ep.nq, tok = t - node * ep.nq;
@@ -197,7 +202,7 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
     }
   } else {
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
+    for (int nb = 0; nb < GNB; ++nb) {
       const int32_t t = t0 + wt + 32 * nb + r32;
       if (t >= T) continue;
       uint16_t* orow = ep.out + (size_t)t * ep.ld_out + f0 + wf + 4 * hl;

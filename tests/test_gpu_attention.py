@@ -212,8 +212,8 @@ def test_logits_far_above_first_tile(geo):
     pages (first page of every state for three-frame chunks; chunks 0..3,
     the first pages of this pack's nodes, for one-frame chunks), with Q
     channel 0 = 1: later logits sit about 76 (log2 units) above the maximum
-    of a node's first key tile, past the kernel's 2^64 overflow guard, which
-    raises the running maximum and rescales the accumulated output.  The
+    of a node's first key tile, past the kernel's 2^64 guard on probability
+    sums, so the work items redo their keys in two exact passes.  The
     softmax is still the plain one: compared with the oracle."""
     kind, pack, resident = SMALL_PACKS[0]
     tpp = geo.tokens_per_page
