@@ -7,9 +7,9 @@
 // start at a multiple of 8 lie in one page.
 //
 // bf16 kernel (head_dim 128), per work-group: 256 queries of one (node, head),
-// eight waves of 32 queries.  Key tiles of 64 are copied into LDS (double
-// buffered, XOR-swizzled against bank conflicts); each wave computes
-// S^T = K Q^T and O^T += V^T P^T with 32x32x16 bf16 MFMAs and keeps an online
+// eight waves of two 16-query blocks.  Key tiles of 64 are copied into LDS
+// (double buffered, XOR-swizzled against bank conflicts); each wave computes
+// S^T = K Q^T and O^T += V^T P^T with 16x16x32 bf16 MFMAs and keeps an online
 // softmax in fp32.  The K rows feeding the S^T MFMA are permuted so that each
 // lane's probabilities are exactly the B operand of the PV MFMA, and V is
 // stored transposed in the cache so its A operand is one 16-byte LDS read.
@@ -94,7 +94,8 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 // ------------------------------------------------------------- bf16 kernel
 // Two work-group shapes, both with two waves per SIMD: 8 waves x 32 queries
 // (256 per work-group, one work-group per CU) and 4 waves x 32 queries (128,
-// two per CU), the latter for nodes of at most 128 queries.
+// two per CU), the latter for nodes of at most 128 queries.  A wave's 32
+// queries are two 16-query blocks of the 16x16x32 MFMA.
 constexpr int BK = 64;                 // keys per LDS tile
 constexpr int HDB = 128;               // head dim of the bf16 kernels
 constexpr int KT_BYTES = BK * HDB * 2;  // 16 KB
@@ -112,72 +113,120 @@ constexpr int BQ_SMALL = 128, BQ_MAX = 256;  // queries per work-group of the tw
 // place would keep the accumulators and the recomputation live in the loop.
 constexpr float P_GUARD = 18446744073709551616.0f;  // 2^64
 
+// Matrix-core shape: v_mfma_f32_16x16x32_bf16.  Lane l (g = l / 16,
+// c = l % 16) supplies row c of A and column c of B with 8 consecutive k
+// values 8 g .. 8 g + 7, and receives D[4 g + r][c], r = 0..3.  (The 16x16
+// shape sustains more FLOP/s than 32x32x16 under the power cap: half the
+// accumulator traffic per FLOP.)
+__device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// XOR swizzle of a K tile row: 16-byte column c of row r is stored at
+// c ^ kswz(r).  Bit 4 of the row enters so that the 16 rows one 16-lane
+// group reads for an S^T MFMA (see attn_lane) fall on distinct banks.
+__device__ __forceinline__ uint32_t kswz(int32_t row) { return (uint32_t)((row & 15) ^ ((row >> 2) & 4)); }
+
 struct AttnLane {
   // per-lane LDS read offsets (bytes) inside one buffer
-  uint32_t koff[8];   // K row sigma, 16-byte column 2 si + hl   (second 32 rows add 8192)
-  uint32_t voff[4];   // V^T row r32, column 4 kb + 2 mm + hl    (db adds 4096)
+  uint32_t koff[2][4];  // K row of block b, 16-byte column 4 ds + g (second 32 rows add 8192)
+  uint32_t voff[2];     // V^T row c, 16-byte column 4 h + g           (16-row block db adds 2048)
 };
 
-// Row sigma of the S^T MFMA holds key sigma: each lane's probabilities are
-// then keys 8 hl .. 8 hl + 7 (+16) of every 32-key block -- exactly the B
-// operand layout of the PV MFMA.
-__device__ __forceinline__ AttnLane attn_lane(int32_t r32, int32_t hl) {
+// A row i of the S^T MFMA for 16-key block b of a 32-key half holds key
+// 8 (i / 4) + 4 b + i % 4: each lane's four results of blocks 0 and 1 are
+// then keys 8 g .. 8 g + 7 of the half -- exactly the B operand of the PV
+// MFMA, which therefore needs no shuffle.
+__device__ __forceinline__ AttnLane attn_lane(int32_t c, int32_t g) {
   AttnLane L;
-  const int32_t sa = r32 >> 3, sh = (r32 >> 2) & 1, sb = r32 & 3;
-  const int32_t sigma = 16 * (sa >> 1) + 8 * sh + 4 * (sa & 1) + sb;
 #pragma unroll
-  for (int si = 0; si < 8; ++si) L.koff[si] = sigma * 256 + (((2 * si + hl) ^ (sigma & 15)) << 4);
+  for (int b = 0; b < 2; ++b) {
+    const int32_t row = 8 * (c >> 2) + 4 * b + (c & 3);
 #pragma unroll
-  for (int cm = 0; cm < 4; ++cm) L.voff[cm] = r32 * 128 + (((2 * cm + hl) ^ ((r32 >> 1) & 7)) << 4);
+    for (int ds = 0; ds < 4; ++ds) L.koff[b][ds] = row * 256 + (((4 * ds + g) ^ kswz(row)) << 4);
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) L.voff[h] = c * 128 + (((4 * h + g) ^ ((c >> 1) & 7)) << 4);
   return L;
 }
 
-// Q^T operand of a 32-query block: lane holds Q[row][16 si + 8 hl .. +7],
+// Q^T operand of a 16-query block: lane holds Q[row][32 ds + 8 g .. +7],
 // pre-scaled to log2 units.  Rows past the node's end repeat its last row.
 __device__ __forceinline__ void load_q(const uint16_t* q, const AttnGeom& g, int32_t node, int32_t head,
-                                       int32_t qrow, int32_t hl, bf16x8 (&qreg)[8]) {
+                                       int32_t qrow, int32_t lg, bf16x8 (&qreg)[4]) {
   const int32_t qrow_c = qrow < g.nq ? qrow : g.nq - 1;
-  const uint16_t* qp = q + (((size_t)node * g.nq + qrow_c) * g.n_heads + head) * HDB + 8 * hl;
+  const uint16_t* qp = q + (((size_t)node * g.nq + qrow_c) * g.n_heads + head) * HDB + 8 * lg;
 #pragma unroll
-  for (int si = 0; si < 8; ++si) {
-    const bf16x8 raw = *reinterpret_cast<const bf16x8*>(qp + 16 * si);
+  for (int ds = 0; ds < 4; ++ds) {
+    const bf16x8 raw = *reinterpret_cast<const bf16x8*>(qp + 32 * ds);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) qreg[si][e] = static_cast<__bf16>(static_cast<float>(raw[e]) * g.scale_log2);
+    for (int e = 0; e < 8; ++e) qreg[ds][e] = static_cast<__bf16>(static_cast<float>(raw[e]) * g.scale_log2);
   }
 }
 
-// Maximum over one lane's 16 logits and its partner half (the other 16 keys
-// of the same query column).
-__device__ __forceinline__ float col_max16(const f32x16& s) {
-  float mx = fmaxf(s[0], s[1]);
-#pragma unroll
-  for (int i = 2; i < 16; ++i) mx = fmaxf(mx, s[i]);
-  return fmaxf(mx, __shfl_xor(mx, 32));
+// Logits of one 64-key tile for a wave's two 16-query blocks:
+// s[h][b][qb] holds, in lane (g, c) value r, key 32 h + 8 g + 4 b + r of the
+// tile for query c of block qb.
+typedef f32x4 STile[2][2][2];
+
+// Sum / maximum of one query's values over the four lane groups.
+__device__ __forceinline__ float group_sum(float x) {
+  x += __shfl_xor(x, 16);
+  return x + __shfl_xor(x, 32);
+}
+__device__ __forceinline__ float group_max(float x) {
+  x = fmaxf(x, __shfl_xor(x, 16));
+  return fmaxf(x, __shfl_xor(x, 32));
 }
 
-// Keys at or past the node's end get no weight: value i of a lane is key
-// key0 + 16 (i / 8) + 8 hl + i % 8 of the 32-key block starting at key0.
-__device__ __forceinline__ void mask32(f32x16& s, int32_t key0, int32_t nk, int32_t hl) {
+// Column maxima of a tile, per query block.
+__device__ __forceinline__ void tile_max(const STile& s, float (&mx)[2]) {
 #pragma unroll
-  for (int i = 0; i < 16; ++i)
-    if (key0 + 16 * (i >> 3) + 8 * hl + (i & 7) >= nk) s[i] = -INFINITY;
+  for (int qb = 0; qb < 2; ++qb) {
+    float m = s[0][0][qb][0];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) m = fmaxf(m, s[h][b][qb][r]);
+    mx[qb] = group_max(m);
+  }
 }
 
-// p = exp2(s) rounded to bf16 for one 32-key block (two B operands of the PV
-// MFMA) and the sum of the rounded values.
-__device__ __forceinline__ float probs32(const f32x16& s, bf16x8 (&pb)[2]) {
+// Keys at or past the node's end get no weight (t0: the tile's first key).
+__device__ __forceinline__ void mask_tile(STile& s, int32_t t0, int32_t nk, int32_t lg) {
 #pragma unroll
-  for (int mm = 0; mm < 2; ++mm)
+  for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) pb[mm][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(s[8 * mm + e]));
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (t0 + 32 * h + 8 * lg + 4 * b + r >= nk) s[h][b][qb][r] = -INFINITY;
+}
+
+// p = exp2(s) rounded to bf16: pb[h][qb] is the B operand of the PV MFMA for
+// the 32-key half h; returns this lane's sums of the rounded values per block.
+__device__ __forceinline__ void probs_tile(const STile& s, bf16x8 (&pb)[2][2], float (&lt)[2]) {
   const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
-  float l0 = 0.f, l1 = 0.f;
 #pragma unroll
-  for (int e = 0; e < 8; e += 2) {
-    l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[0][e], pb[0][e + 1]}, ones, l0, false);
-    l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[1][e], pb[1][e + 1]}, ones, l1, false);
+  for (int qb = 0; qb < 2; ++qb) {
+    float l0 = 0.f, l1 = 0.f;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        pb[h][qb][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(s[h][e >> 2][qb][e & 3]));
+#pragma unroll
+      for (int e = 0; e < 8; e += 4) {
+        l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[h][qb][e], pb[h][qb][e + 1]}, ones, l0, false);
+        l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[h][qb][e + 2], pb[h][qb][e + 3]}, ones, l1, false);
+      }
+    }
+    lt[qb] = l0 + l1;
   }
-  return l0 + l1;
 }
 
 // Direct global -> LDS copy of 16 bytes per lane (gfx950 LDS DMA): lane i
@@ -212,7 +261,7 @@ struct KvTiles {
   int32_t npages, nk, tpp, wave;
   uint32_t slot_bytes, khead, vhead, kbad;
   DivMagic tpp_div;
-  uint32_t kswz[KCP], vlane[VCP];
+  uint32_t klane[KCP], vlane[VCP];
   int32_t vkey[VCP], krow0;
 
   __device__ __forceinline__ KvTiles(const AttnPlan& plan, const AttnGeom& g, int32_t node, int32_t head,
@@ -235,7 +284,7 @@ struct KvTiles {
 #pragma unroll
     for (int j = 0; j < KCP; ++j) {
       const int32_t row = krow0 + 4 * j;
-      kswz[j] = (uint32_t)row * 256 + ((kp ^ (row & 15)) << 4);  // plus key t0 * 256
+      klane[j] = (uint32_t)row * 256 + ((kp ^ kswz(row)) << 4);  // plus key t0 * 256
     }
 #pragma unroll
     for (int j = 0; j < VCP; ++j) {
@@ -264,8 +313,8 @@ struct KvTiles {
 #pragma unroll
     for (int j = 0; j < KCP; ++j) {
       const int32_t rk = krow0 + 4 * j;  // tile-relative key
-      const uint32_t src = rk >= lim ? kbad + (kswz[j] - (uint32_t)rk * 256)
-                                     : (rk >= split ? hi : lo) + kswz[j];
+      const uint32_t src = rk >= lim ? kbad + (klane[j] - (uint32_t)rk * 256)
+                                     : (rk >= split ? hi : lo) + klane[j];
       dma16(lbase + src, kl + (4 * KCP * wave + 4 * j) * 256);
     }
   }
@@ -338,59 +387,80 @@ __device__ __forceinline__ AttnItem decode_item(const AttnPlan& plan, const Attn
   return it;
 }
 
-// The result of a work item for one 32-query block: the normalised output of
-// a whole unit, or a piece's unnormalised partial with its max and sum.
+// The result of a work item for one 16-query block: the normalised output
+// of a whole unit, or a piece's unnormalised partial with its max and sum.
+// oacc[db] holds, in lane (g, c) value r, O[query c][16 db + 4 g + r].
 template <int BQ>
 __device__ __forceinline__ void store_rows(const AttnItem& it, const AttnGeom& g, uint16_t* o,
-                                           const f32x16 (&oacc)[4], float m_run, float l_run,
-                                           int32_t lrow, int32_t hl) {
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+                                           const f32x4 (&oacc)[8], float m_run, float l_run,
+                                           int32_t lrow, int32_t lg) {
+  const float l_tot = group_sum(l_run);
   if (it.slot < 0) {
     const float inv = 1.f / l_tot;
     const int32_t qrow = it.qt * BQ + lrow;
     if (qrow < g.nq) {
-      uint16_t* op = o + (((size_t)it.node * g.nq + qrow) * g.n_heads + it.head) * HDB;
+      uint16_t* op = o + (((size_t)it.node * g.nq + qrow) * g.n_heads + it.head) * HDB + 4 * lg;
 #pragma unroll
-      for (int db = 0; db < 4; ++db)
-#pragma unroll
-        for (int gi = 0; gi < 4; ++gi) {
-          const int32_t d = 32 * db + 8 * gi + 4 * hl;
-          u32x2 v;
-          v.x = pack_bf16x2(oacc[db][4 * gi + 0] * inv, oacc[db][4 * gi + 1] * inv);
-          v.y = pack_bf16x2(oacc[db][4 * gi + 2] * inv, oacc[db][4 * gi + 3] * inv);
-          *reinterpret_cast<u32x2*>(op + d) = v;
-        }
+      for (int db = 0; db < 8; ++db) {
+        u32x2 v;
+        v.x = pack_bf16x2(oacc[db][0] * inv, oacc[db][1] * inv);
+        v.y = pack_bf16x2(oacc[db][2] * inv, oacc[db][3] * inv);
+        *reinterpret_cast<u32x2*>(op + 16 * db) = v;
+      }
     }
   } else {
-    float* po = g.part_o + ((size_t)it.slot * BQ + lrow) * HDB;
+    float* po = g.part_o + ((size_t)it.slot * BQ + lrow) * HDB + 4 * lg;
 #pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int gi = 0; gi < 4; ++gi) {
-        const int32_t d = 32 * db + 8 * gi + 4 * hl;
-        *reinterpret_cast<f32x4*>(po + d) =
-            f32x4{oacc[db][4 * gi + 0], oacc[db][4 * gi + 1], oacc[db][4 * gi + 2], oacc[db][4 * gi + 3]};
-      }
-    if (hl == 0) {
+    for (int db = 0; db < 8; ++db) *reinterpret_cast<f32x4*>(po + 16 * db) = oacc[db];
+    if (lg == 0) {
       g.part_ml[((size_t)it.slot * 2 + 0) * BQ + lrow] = m_run;
       g.part_ml[((size_t)it.slot * 2 + 1) * BQ + lrow] = l_tot;
     }
   }
 }
 
-// S^T blocks of one tile, s[kb] = K_kb Q^T - m for the two 32-key halves.
-__device__ __forceinline__ void qk_tile(const char* kl, const AttnLane& L, const bf16x8 (&qreg)[8],
-                                        f32x16 (&s)[2], float m) {
+// S^T of one 64-key tile, s[h][b][qb] = K_(h,b) Q_qb^T - m_qb: all eight
+// accumulators advance together.
+__device__ __forceinline__ void qk_tile(const char* kl, const AttnLane& L, const bf16x8 (&qreg)[2][4],
+                                        STile& s, const float (&m)[2]) {
+  f32x4 acc[2][2][2];
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
+  for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) s[kb][i] = -m;
+    for (int b = 0; b < 2; ++b)
 #pragma unroll
-    for (int si = 0; si < 8; ++si) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + L.koff[si] + kb * 8192);
-      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[si], s[kb], 0, 0, 0);
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[h][b][qb][r] = -m[qb];
+#pragma unroll
+  for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + L.koff[b][ds] + h * 8192);
+        acc[h][b][0] = mfma16(a, qreg[0][ds], acc[h][b][0]);
+        acc[h][b][1] = mfma16(a, qreg[1][ds], acc[h][b][1]);
+      }
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) s[h][b][qb] = acc[h][b][qb];
+}
+
+// O^T += V^T P^T for a 64-key tile whose V^T sits at vl.
+__device__ __forceinline__ void pv_tile(const char* vl, const AttnLane& L, const bf16x8 (&pb)[2][2],
+                                        f32x4 (&oacc)[2][8]) {
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(vl + L.voff[h] + db * 2048);
+      oacc[0][db] = mfma16(a, pb[h][0], oacc[0][db]);
+      oacc[1][db] = mfma16(a, pb[h][1], oacc[1][db]);
     }
-  }
 }
 
 // One step of the software-pipelined loop, for tile t: probabilities of
@@ -399,32 +469,26 @@ __device__ __forceinline__ void qk_tile(const char* kl, const AttnLane& L, const
 // check, then O^T += V(t)^T P(t).  K runs one tile ahead of V: K(t+1) sits
 // in K buffer KN, V(t) in V buffer VC.
 template <int KN, int VC, bool NEXT, bool MASK>
-__device__ __forceinline__ void attn_step(const char* smem, const AttnLane& L, const bf16x8 (&qreg)[8],
-                                          f32x16 (&oacc)[4], f32x16 (&s)[2], float& m_run,
-                                          float& l_run, bool& bad, int32_t t0, int32_t nk, int32_t hl) {
-  if constexpr (MASK) {
-    mask32(s[0], t0, nk, hl);
-    mask32(s[1], t0 + 32, nk, hl);
-  }
+__device__ __forceinline__ void attn_step(const char* smem, const AttnLane& L, const bf16x8 (&qreg)[2][4],
+                                          f32x4 (&oacc)[2][8], STile& s, const float (&m)[2],
+                                          float (&l)[2], bool& bad, int32_t t0, int32_t nk, int32_t lg) {
+  if constexpr (MASK) mask_tile(s, t0, nk, lg);
   bf16x8 pb[2][2];
-  const float l_tile = probs32(s[0], pb[0]) + probs32(s[1], pb[1]);
-  f32x16 sn[2];
-  if constexpr (NEXT) qk_tile(smem + KN * KT_BYTES, L, qreg, sn, m_run);
-  bad |= __builtin_amdgcn_ballot_w64(!(l_tile < P_GUARD)) != 0;  // also NaN / inf
-  l_run += l_tile;
-  const char* vl = smem + 2 * KT_BYTES + VC * VT_BYTES;
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int mm = 0; mm < 2; ++mm)
-#pragma unroll
-      for (int db = 0; db < 4; ++db) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(vl + L.voff[2 * kb + mm] + db * 4096);
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kb][mm], oacc[db], 0, 0, 0);
-      }
+  float lt[2];
+  probs_tile(s, pb, lt);
+  STile sn;
+  if constexpr (NEXT) qk_tile(smem + KN * KT_BYTES, L, qreg, sn, m);
+  bad |= __builtin_amdgcn_ballot_w64(!(lt[0] < P_GUARD && lt[1] < P_GUARD)) != 0;  // also NaN / inf
+  l[0] += lt[0];
+  l[1] += lt[1];
+  pv_tile(smem + 2 * KT_BYTES + VC * VT_BYTES, L, pb, oacc);
   if constexpr (NEXT) {
-    s[0] = sn[0];
-    s[1] = sn[1];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) s[h][b][qb] = sn[h][b][qb];
   }
 }
 
@@ -434,52 +498,53 @@ __device__ __forceinline__ void attn_step(const char* smem, const AttnLane& L, c
 // taken only for logits far above the first tile's maximum.
 template <int NW>
 __device__ __forceinline__ void attn_exact(char* smem, const KvTiles<NW>& kv, const AttnLane& L,
-                                           const bf16x8 (&qreg)[8], f32x16 (&oacc)[4], float& m_run,
-                                           float& l_run, int32_t ta, int32_t ntiles, int32_t hl) {
+                                           const bf16x8 (&qreg)[2][4], f32x4 (&oacc)[2][8], float (&m)[2],
+                                           float (&l)[2], int32_t ta, int32_t ntiles, int32_t lg) {
   char* const kl = smem;
   char* const vl = smem + 2 * KT_BYTES;
   const int32_t nk = kv.nk;
-  float mx = -INFINITY;
+  const float zero[2] = {0.f, 0.f};
+  float mx[2] = {-INFINITY, -INFINITY};
   for (int32_t t = ta; t < ntiles; ++t) {
     kv.copy_k(t * BK, kl, kv.slots(t * BK));
     landed();
-    f32x16 s[2];
-    qk_tile(kl, L, qreg, s, 0.f);
-    mask32(s[0], t * BK, nk, hl);
-    mask32(s[1], t * BK + 32, nk, hl);
-    mx = fmaxf(mx, fmaxf(col_max16(s[0]), col_max16(s[1])));
+    STile s;
+    qk_tile(kl, L, qreg, s, zero);
+    mask_tile(s, t * BK, nk, lg);
+    float tm[2];
+    tile_max(s, tm);
+    mx[0] = fmaxf(mx[0], tm[0]);
+    mx[1] = fmaxf(mx[1], tm[1]);
     __syncthreads();
   }
-  m_run = mx;
-  l_run = 0.f;
 #pragma unroll
-  for (int db = 0; db < 4; ++db) oacc[db] = f32x16{};
+  for (int qb = 0; qb < 2; ++qb) {
+    m[qb] = mx[qb];
+    l[qb] = 0.f;
+#pragma unroll
+    for (int db = 0; db < 8; ++db) oacc[qb][db] = f32x4{};
+  }
   for (int32_t t = ta; t < ntiles; ++t) {
     const typename KvTiles<NW>::Slots sl = kv.slots(t * BK);
     kv.copy_k(t * BK, kl, sl);
     kv.copy_v(t * BK, vl, sl);
     landed();
-    f32x16 s[2];
-    qk_tile(kl, L, qreg, s, m_run);
-    mask32(s[0], t * BK, nk, hl);
-    mask32(s[1], t * BK + 32, nk, hl);
+    STile s;
+    qk_tile(kl, L, qreg, s, m);
+    mask_tile(s, t * BK, nk, lg);
     bf16x8 pb[2][2];
-    l_run += probs32(s[0], pb[0]) + probs32(s[1], pb[1]);
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int mm = 0; mm < 2; ++mm)
-#pragma unroll
-        for (int db = 0; db < 4; ++db) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(vl + L.voff[2 * kb + mm] + db * 4096);
-          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kb][mm], oacc[db], 0, 0, 0);
-        }
+    float lt[2];
+    probs_tile(s, pb, lt);
+    l[0] += lt[0];
+    l[1] += lt[1];
+    pv_tile(vl, L, pb, oacc);
     __syncthreads();
   }
 }
 
 // NW = 8: 256 queries per work-group, one work-group per CU; NW = 4: 128
-// queries, two per CU.  Both keep two waves per SIMD.
+// queries, two per CU.  Both keep two waves per SIMD; each wave owns two
+// 16-query blocks.
 template <int NW>
 __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                                     uint16_t* __restrict__ o, AttnGeom g,
@@ -493,21 +558,24 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
   if (it.ta == it.tb) return;  // empty piece of a unit shorter than the split
   const int32_t ta = it.ta, ntiles = it.tb;  // this item's key tiles: [ta, ntiles)
   const int32_t tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int32_t hl = lane >> 5, r32 = lane & 31;
+  const int32_t lg = lane >> 4, c = lane & 15;
   if (tid == 0) any_bad = 0;
   const KvTiles<NW> kv(plan, g, it.node, it.head, wave, lane);
   const int32_t nk = kv.nk;
   const bool ragged = it.tb == it.ntiles && (nk % BK) != 0;
-  const int32_t lrow = wave * 32 + r32;
-  bf16x8 qreg[8];
-  load_q(q, g, it.node, it.head, it.qt * BQ + lrow, hl, qreg);
-  const AttnLane L = attn_lane(r32, hl);
-
-  f32x16 oacc[4];
+  bf16x8 qreg[2][4];
 #pragma unroll
-  for (int db = 0; db < 4; ++db) oacc[db] = f32x16{};
-  float m_run = 0.f, l_run = 0.f;
-  // prologue: K(ta), V(ta), K(ta+1) in flight; S(ta) = K(ta) Q^T; m = its exact max
+  for (int qb = 0; qb < 2; ++qb)
+    load_q(q, g, it.node, it.head, it.qt * BQ + wave * 32 + 16 * qb + c, lg, qreg[qb]);
+  const AttnLane L = attn_lane(c, lg);
+
+  f32x4 oacc[2][8];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+    for (int db = 0; db < 8; ++db) oacc[qb][db] = f32x4{};
+  float m[2] = {0.f, 0.f}, l[2] = {0.f, 0.f};
+  // prologue: K(ta), V(ta), K(ta+1) in flight; S(ta) = K(ta) Q^T; m = its exact column maxima
   {
     const typename KvTiles<NW>::Slots s0 = kv.slots(ta * BK);
     kv.copy_k(ta * BK, smem, s0);
@@ -515,17 +583,18 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
     if (ta + 1 < ntiles) kv.copy_k((ta + 1) * BK, smem + KT_BYTES, kv.slots((ta + 1) * BK));
   }
   landed();
-  f32x16 s[2];
-  qk_tile(smem, L, qreg, s, 0.f);
-  if (ta + 1 == ntiles && ragged) {
-    mask32(s[0], ta * BK, nk, hl);
-    mask32(s[1], ta * BK + 32, nk, hl);
-  }
-  m_run = fmaxf(col_max16(s[0]), col_max16(s[1]));
+  STile s;
+  qk_tile(smem, L, qreg, s, m);
+  if (ta + 1 == ntiles && ragged) mask_tile(s, ta * BK, nk, lg);
+  tile_max(s, m);
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
+  for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) s[kb][i] -= m_run;
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) s[h][b][qb][r] -= m[qb];
   __syncthreads();  // every wave has read K(ta) before K(ta+2) is copied over it
 
   // iteration t (buffer parity counted from ta): copy K(t+2) over K(t) and
@@ -538,34 +607,35 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
     kv.copy_v((t + 1) * BK, smem + 2 * KT_BYTES + VT_BYTES, sv);
     sk = kv.slots(min(t + 3, it.ntiles - 1) * BK);
     sv = kv.slots(min(t + 2, it.ntiles - 1) * BK);
-    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, bad, t * BK, nk, hl);
+    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m, l, bad, t * BK, nk, lg);
     landed();
     if (t + 3 < ntiles) kv.copy_k((t + 3) * BK, smem + KT_BYTES, sk);
     kv.copy_v((t + 2) * BK, smem + 2 * KT_BYTES, sv);
     sk = kv.slots(min(t + 4, it.ntiles - 1) * BK);
     sv = kv.slots(min(t + 3, it.ntiles - 1) * BK);
-    attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m_run, l_run, bad, (t + 1) * BK, nk, hl);
+    attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m, l, bad, (t + 1) * BK, nk, lg);
     landed();
   }
   if (t + 1 < ntiles) {  // two tiles left, parity 0
     kv.copy_v((t + 1) * BK, smem + 2 * KT_BYTES + VT_BYTES, sv);
-    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m_run, l_run, bad, t * BK, nk, hl);
+    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m, l, bad, t * BK, nk, lg);
     landed();
     ++t;
     if (ragged)
-      attn_step<0, 1, false, true>(smem, L, qreg, oacc, s, m_run, l_run, bad, t * BK, nk, hl);
+      attn_step<0, 1, false, true>(smem, L, qreg, oacc, s, m, l, bad, t * BK, nk, lg);
     else
-      attn_step<0, 1, false, false>(smem, L, qreg, oacc, s, m_run, l_run, bad, t * BK, nk, hl);
+      attn_step<0, 1, false, false>(smem, L, qreg, oacc, s, m, l, bad, t * BK, nk, lg);
   } else {               // one tile left, parity 0 (masking twice is harmless)
     if (ragged)
-      attn_step<1, 0, false, true>(smem, L, qreg, oacc, s, m_run, l_run, bad, t * BK, nk, hl);
+      attn_step<1, 0, false, true>(smem, L, qreg, oacc, s, m, l, bad, t * BK, nk, lg);
     else
-      attn_step<1, 0, false, false>(smem, L, qreg, oacc, s, m_run, l_run, bad, t * BK, nk, hl);
+      attn_step<1, 0, false, false>(smem, L, qreg, oacc, s, m, l, bad, t * BK, nk, lg);
   }
   if (bad && lane == 0) atomicOr(&any_bad, 1);
   __syncthreads();  // every wave is done with the ring; any_bad is final
-  if (any_bad) attn_exact(smem, kv, L, qreg, oacc, m_run, l_run, ta, ntiles, hl);
-  store_rows<BQ>(it, g, o, oacc, m_run, l_run, lrow, hl);
+  if (any_bad) attn_exact(smem, kv, L, qreg, oacc, m, l, ta, ntiles, lg);
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) store_rows<BQ>(it, g, o, oacc[qb], m[qb], l[qb], wave * 32 + 16 * qb + c, lg);
 }
 
 // Merges the pieces of each tail unit, in piece order: one work-group per
