@@ -37,8 +37,8 @@ METRIC = "steady-state latent frames/s per DiT block + attention TFLOP/s (% bf16
 # FETCH_SIZE and WRITE_SIZE per dispatch, scaled by what the same counters
 # read for a plain 256 MiB copy (x2.0 fetch, x1.0 write).  Valid only for the
 # kernel sources it was measured on (hash below); otherwise reported as null.
-ATTN_TRAFFIC = {"sources_sha1": "3f9547d3f89b8d7c6d4f937921e3d9d575d98cfd",
-                "fetch_bytes": 1.3590e+09, "write_bytes": 1.8268e+08}
+ATTN_TRAFFIC = {"sources_sha1": "5871aaf6f9c74106855e6809bc829aa2d33bc0f7",
+                "fetch_bytes": 1.3619e+09, "write_bytes": 1.8974e+08}
 
 
 def attn_traffic():
