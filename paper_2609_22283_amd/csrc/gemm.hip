@@ -1,6 +1,8 @@
 // bf16 GEMM for the DiT block's projections, D[f][t] = sum_k W[f][k] X[t][k]
-// (W in [out, in] layout, X token-major), fp32 accumulation on 32x32x16 bf16
-// MFMAs, with the block's elementwise work fused into the epilogue:
+// (W in [out, in] layout, X token-major), fp32 accumulation on 16x16x32 bf16
+// MFMAs (half the accumulator traffic per FLOP of the 32x32 shape, so a
+// higher clock under the power cap), with the block's elementwise work fused
+// into the epilogue:
 //   QKV      RoPE on q and k; q to a token-major buffer; k and v scattered
 //            into the pack nodes' page slots (k as [head][token][d], v as
 //            [head][d][token])
@@ -20,7 +22,6 @@ constexpr int GWM = 128;
 constexpr int G_NW = 8;               // waves per work-group, two per SIMD
 constexpr int G_THREADS = 64 * G_NW;
 constexpr int GWN = 2 * GBN / G_NW;   // tokens per wave tile
-constexpr int GNB = GWN / 32;         // 32-token MFMA blocks per wave
 constexpr int GROWS = GBM / G_NW;     // operand rows each wave copies per stage
 constexpr int G_TILE_BYTES = GBM * GBK * 2;  // 32 KB per operand per stage
 
@@ -61,7 +62,7 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   const int32_t f0 = tf * GBM, t0 = tt * GBN;
 
   const int32_t tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int32_t hl = lane >> 5, r32 = lane & 31;
+  const int32_t lg = lane >> 4, c16 = lane & 15;
   const int32_t wf = (wave & 1) * GWM, wt = (wave >> 1) * GWN;
 
   // copies: each wave moves rows [GROWS wave, GROWS wave + GROWS) of both
@@ -96,26 +97,29 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
     __syncthreads();
   };
 
-  // LDS read offsets of this lane's fragments (16-byte column 2 s + hl)
-  uint32_t aoff[4], boff[GNB];
+  // LDS read offsets of this lane's fragments (16-byte column 4 s + lg)
+  // 16x16x32 MFMAs: lane (lg, c16) supplies row c16 of each 16-row operand
+  // block with k values 8 lg .. 8 lg + 7 of a 32-k step
+  constexpr int FB = GWM / 16, TB = GWN / 16;
+  uint32_t aoff[FB], boff[TB];
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb) aoff[mb] = (uint32_t)(wf + 32 * mb + r32) * 128;
+  for (int fb = 0; fb < FB; ++fb) aoff[fb] = (uint32_t)(wf + 16 * fb + c16) * 128;
 #pragma unroll
-  for (int nb = 0; nb < GNB; ++nb) boff[nb] = (uint32_t)(wt + 32 * nb + r32) * 128;
-  const int32_t swz = (r32 >> 1) & 7;  // rows wf + 32 mb + r32 share (row >> 1) & 7
+  for (int tb = 0; tb < TB; ++tb) boff[tb] = (uint32_t)(wt + 16 * tb + c16) * 128;
+  const int32_t swz = (c16 >> 1) & 7;  // rows wf + 16 fb + c16 share (row >> 1) & 7
 
-  f32x16 acc[4][GNB];
+  f32x4 acc[FB][TB];
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb)
+  for (int fb = 0; fb < FB; ++fb)
 #pragma unroll
-    for (int nb = 0; nb < GNB; ++nb) acc[mb][nb] = f32x16{};
+    for (int tb = 0; tb < TB; ++tb) acc[fb][tb] = f32x4{};
 
-  auto frags = [&](const char* a, const char* b, int s, bf16x8 (&af)[4], bf16x8 (&bf)[GNB]) {
-    const uint32_t c = (uint32_t)(((2 * s + hl) ^ swz) << 4);
+  auto frags = [&](const char* a, const char* b, int s, bf16x8 (&af)[FB], bf16x8 (&bf)[TB]) {
+    const uint32_t c = (uint32_t)(((4 * s + lg) ^ swz) << 4);
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) af[mb] = *reinterpret_cast<const bf16x8*>(a + aoff[mb] + c);
+    for (int fb = 0; fb < FB; ++fb) af[fb] = *reinterpret_cast<const bf16x8*>(a + aoff[fb] + c);
 #pragma unroll
-    for (int nb = 0; nb < GNB; ++nb) bf[nb] = *reinterpret_cast<const bf16x8*>(b + boff[nb] + c);
+    for (int tb = 0; tb < TB; ++tb) bf[tb] = *reinterpret_cast<const bf16x8*>(b + boff[tb] + c);
   };
 
   const int32_t nk = Kd / GBK;
@@ -125,50 +129,48 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
     if (kt + 1 < nk) issue((kt + 1) * GBK, (kt + 1) & 1);
     const char* a = smem + (kt & 1) * 2 * G_TILE_BYTES;
     const char* b = a + G_TILE_BYTES;
-    bf16x8 af[2][4], bfr[2][GNB];
+    bf16x8 af[2][FB], bfr[2][TB];
     frags(a, b, 0, af[0], bfr[0]);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      if (s + 1 < 4) frags(a, b, s + 1, af[(s + 1) & 1], bfr[(s + 1) & 1]);
+    for (int s = 0; s < 2; ++s) {
+      if (s + 1 < 2) frags(a, b, s + 1, af[(s + 1) & 1], bfr[(s + 1) & 1]);
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
+      for (int fb = 0; fb < FB; ++fb)
 #pragma unroll
-        for (int nb = 0; nb < GNB; ++nb)
-          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s & 1][mb], bfr[s & 1][nb],
-                                                                acc[mb][nb], 0, 0, 0);
+        for (int tb = 0; tb < TB; ++tb)
+          acc[fb][tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[s & 1][fb], bfr[s & 1][tb],
+                                                                acc[fb][tb], 0, 0, 0);
     }
     landed();
   }
 
-  // epilogue: lane holds D[f][t] for t = t0 + wt + 32 nb + r32 and
-  // f = f0 + wf + 32 mb + 8 g + 4 hl + e (e = 0..3)
+  // epilogue: lane holds D[f][t] for t = t0 + wt + 16 tb + c16 and
+  // f = f0 + wf + 16 fb + 4 lg + e (e = 0..3)
   if constexpr (EPI == EPI_QKV) {
     // a 256-feature tile lies in one of q, k, v (hidden is a multiple of 256)
     // and each wave's 128 features in one head (head_dim 128)
     const int32_t sec = f0 / ep.hidden;
     const int32_t hf0 = f0 - sec * ep.hidden + wf;       // wave's first feature in its section
     const int32_t head = hf0 / ep.head_dim;
-    const int32_t dbase = hf0 - head * ep.head_dim + 4 * hl;
+    const int32_t dbase = hf0 - head * ep.head_dim + 4 * lg;
 #pragma unroll
-    for (int nb = 0; nb < GNB; ++nb) {
-      const int32_t t = t0 + wt + 32 * nb + r32;
+    for (int tb = 0; tb < TB; ++tb) {
+      const int32_t t = t0 + wt + 16 * tb + c16;
       if (t >= T) continue;
       const int32_t node = t / ep.nq, tok = t - node * ep.nq;
       const int32_t frame = tok / ep.tpp, n = tok - frame * ep.tpp;
       const int32_t pos_t = ep.node_chunk[node] * ep.ppc + frame;
       const int32_t pos_h = n / ep.grid_w, pos_w = n - pos_h * ep.grid_w;
       char* slot_base = ep.layer_base + (size_t)ep.node_slot[node * ep.ppc + frame] * ep.slot_bytes;
-      uint16_t* qrow = ep.q_out + (size_t)t * ep.hidden + hf0 + 4 * hl;
+      uint16_t* qrow = ep.q_out + (size_t)t * ep.hidden + hf0 + 4 * lg;
       uint16_t* krow = reinterpret_cast<uint16_t*>(slot_base) + ((size_t)head * ep.tpp + n) * ep.head_dim;
       uint16_t* vcol = reinterpret_cast<uint16_t*>(slot_base + ep.kv_half) +
                        (size_t)head * ep.head_dim * ep.tpp + n;
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int32_t d = dbase + 32 * mb + 8 * g;
-          float v0 = acc[mb][nb][4 * g + 0], v1 = acc[mb][nb][4 * g + 1];
-          float v2 = acc[mb][nb][4 * g + 2], v3 = acc[mb][nb][4 * g + 3];
+      for (int fb = 0; fb < FB; ++fb) {
+          const int32_t d = dbase + 16 * fb;
+          float v0 = acc[fb][tb][0], v1 = acc[fb][tb][1];
+          float v2 = acc[fb][tb][2], v3 = acc[fb][tb][3];
           if (sec < 2 && ep.rope_table) {
 #pragma unroll
             for (int pp = 0; pp < 2; ++pp) {
@@ -188,7 +190,7 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
           pk.x = pack_bf16x2(v0, v1);
           pk.y = pack_bf16x2(v2, v3);
           if (sec == 0) {
-            *reinterpret_cast<u32x2*>(qrow + 32 * mb + 8 * g) = pk;
+            *reinterpret_cast<u32x2*>(qrow + 16 * fb) = pk;
           } else if (sec == 1) {
             *reinterpret_cast<u32x2*>(krow + d) = pk;
           } else {
@@ -202,25 +204,23 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
     }
   } else {
 #pragma unroll
-    for (int nb = 0; nb < GNB; ++nb) {
-      const int32_t t = t0 + wt + 32 * nb + r32;
+    for (int tb = 0; tb < TB; ++tb) {
+      const int32_t t = t0 + wt + 16 * tb + c16;
       if (t >= T) continue;
-      uint16_t* orow = ep.out + (size_t)t * ep.ld_out + f0 + wf + 4 * hl;
+      uint16_t* orow = ep.out + (size_t)t * ep.ld_out + f0 + wf + 4 * lg;
       // noise-level gate of this token's node (residual epilogue only)
       const float* gate = nullptr;
       if (EPI == EPI_RESIDUAL && ep.mod)
-        gate = ep.mod + ((size_t)ep.node_level[t / ep.nq] * 6 + ep.gate_row) * F + f0 + wf + 4 * hl;
+        gate = ep.mod + ((size_t)ep.node_level[t / ep.nq] * 6 + ep.gate_row) * F + f0 + wf + 4 * lg;
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
+      for (int fb = 0; fb < FB; ++fb) {
           float v[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = acc[mb][nb][4 * g + e];
-          uint16_t* dst = orow + 32 * mb + 8 * g;
+          for (int e = 0; e < 4; ++e) v[e] = acc[fb][tb][e];
+          uint16_t* dst = orow + 16 * fb;
           if constexpr (EPI == EPI_RESIDUAL) {
             if (gate) {
-              const f32x4 gv = *reinterpret_cast<const f32x4*>(gate + 32 * mb + 8 * g);
+              const f32x4 gv = *reinterpret_cast<const f32x4*>(gate + 16 * fb);
 #pragma unroll
               for (int e = 0; e < 4; ++e) v[e] *= gv[e];
             }
