@@ -557,7 +557,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
   const AttnItem it = decode_item(plan, g, blockIdx.x);
   if (it.ta == it.tb) return;  // empty piece of a unit shorter than the split
   const int32_t ta = it.ta, ntiles = it.tb;  // this item's key tiles: [ta, ntiles)
-  const int32_t tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int32_t tid = threadIdx.x, lane = tid & 63;
+  const int32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: LDS copy addresses stay scalar
   const int32_t lg = lane >> 4, c = lane & 15;
   if (tid == 0) any_bad = 0;
   const KvTiles<NW> kv(plan, g, it.node, it.head, wave, lane);

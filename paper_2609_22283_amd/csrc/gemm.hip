@@ -61,7 +61,8 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   const int32_t tf = in_group / gt, tt = group * GT + in_group % gt;
   const int32_t f0 = tf * GBM, t0 = tt * GBN;
 
-  const int32_t tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int32_t tid = threadIdx.x, lane = tid & 63;
+  const int32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: LDS copy addresses stay scalar
   const int32_t lg = lane >> 4, c16 = lane & 15;
   const int32_t wf = (wave & 1) * GWM, wt = (wave >> 1) * GWN;
 
