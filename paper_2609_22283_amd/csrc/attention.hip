@@ -305,6 +305,10 @@ struct KvTiles {
     sl.hi = (uint32_t)page_slot[phi] * slot_bytes;
     return sl;
   }
+  // The 4 K rows of one copy instruction are tile rows 4 (KCP wave + j) ..
+  // +3; page boundaries and the node's end are multiples of 8 keys, so the
+  // page (or the out-of-range fallback) is one wave-uniform choice per
+  // instruction.
   __device__ __forceinline__ void copy_k(int32_t t0, char* kl, const Slots& sl) const {
     const int32_t bkey = (sl.plo + 1) * tpp;
     const uint32_t lo = sl.lo + khead + (uint32_t)(t0 - sl.plo * tpp) * 256;
@@ -312,17 +316,24 @@ struct KvTiles {
     const int32_t lim = nk - t0, split = bkey - t0;
 #pragma unroll
     for (int j = 0; j < KCP; ++j) {
-      const int32_t rk = krow0 + 4 * j;  // tile-relative key
-      const uint32_t src = rk >= lim ? kbad + (klane[j] - (uint32_t)rk * 256)
-                                     : (rk >= split ? hi : lo) + klane[j];
-      dma16(lbase + src, kl + (4 * KCP * wave + 4 * j) * 256);
+      const int32_t rg = 4 * KCP * wave + 4 * j;  // first tile row of this copy (wave-uniform)
+      const uint32_t src = rg >= lim ? kbad + (klane[j] & 255u) : (rg >= split ? hi : lo) + klane[j];
+      dma16(lbase + src, kl + rg * 256);
     }
   }
+  // A V^T row holds the tile's 64 keys; a page boundary or the node's end
+  // falls inside the tile for about one tile in a page, so the per-lane
+  // choice is taken only then (wave-uniform branch).
   __device__ __forceinline__ void copy_v(int32_t t0, char* vl, const Slots& sl) const {
     const int32_t bkey = (sl.plo + 1) * tpp;
     const uint32_t lo = sl.lo + vhead + (uint32_t)(t0 - sl.plo * tpp) * 2;
-    const uint32_t hi = sl.hi + vhead + (uint32_t)(t0 - bkey) * 2;
     const int32_t lim = nk - t0, split = bkey - t0;
+    if (split >= BK && lim >= BK) {
+#pragma unroll
+      for (int j = 0; j < VCP; ++j) dma16(lbase + (lo + vlane[j]), vl + (8 * VCP * wave + 8 * j) * 128);
+      return;
+    }
+    const uint32_t hi = sl.hi + vhead + (uint32_t)(t0 - bkey) * 2;
 #pragma unroll
     for (int j = 0; j < VCP; ++j) {
       const int32_t rk = vkey[j];
