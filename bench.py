@@ -37,8 +37,8 @@ METRIC = "steady-state latent frames/s per DiT block + attention TFLOP/s (% bf16
 # FETCH_SIZE and WRITE_SIZE per dispatch, scaled by what the same counters
 # read for a plain 256 MiB copy (x2.0 fetch, x1.0 write).  Valid only for the
 # kernel sources it was measured on (hash below); otherwise reported as null.
-ATTN_TRAFFIC = {"sources_sha1": "5871aaf6f9c74106855e6809bc829aa2d33bc0f7",
-                "fetch_bytes": 1.3619e+09, "write_bytes": 1.8974e+08}
+ATTN_TRAFFIC = {"sources_sha1": "f53c5ba5162a62d88eb241221bf10993b5421874",
+                "fetch_bytes": 1.3617e+09, "write_bytes": 2.0873e+08}
 
 
 def attn_traffic():
