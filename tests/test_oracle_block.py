@@ -225,3 +225,235 @@ def test_serial_and_pipelined_progressive_agree_bitwise():
     assert set(pipe) == set(ser) and len(pipe) == B * (K + 1)
     for node in pipe:
         assert np.array_equal(pipe[node], ser[node]), node
+
+
+# ---- qk-norm and cross-attention to the condition (Wan block form) ----
+
+def _pack_inputs(shp, seed, n=2):
+    xs = [normal((shp.tokens_per_chunk, shp.hidden), (seed, i)).astype(np.float64) for i in range(n)]
+    res = {(0, 0): tuple(normal((shp.tokens_per_chunk, 2, 16), (seed, t, 0)).astype(np.float64)
+                         for t in (2, 3))}
+    return xs, res
+
+
+def _gains(shp, seed):
+    return tuple(1.0 + normal((shp.hidden,), (seed, 40, s), 0.3).astype(np.float64) for s in range(2))
+
+
+def test_qk_norm_removes_projection_scale():
+    """With qk-norm the block no longer sees the scale of Wq and Wk (up to the
+    eps of the norm); without it, the same rescale changes the output."""
+    shp = _tiny_shape()
+    sel = select(policy("prog", 4, 2), [(1, 1), (2, 2)])
+    xs, res = _pack_inputs(shp, 7)
+    w = _weights(shp, 0)
+    ws = {k: v.copy() for k, v in w.items()}
+    ws["w_qkv"][:shp.hidden] *= 4.0
+    ws["w_qkv"][shp.hidden:2 * shp.hidden] *= 0.25
+    g = _gains(shp, 1)
+    a, kva = block_forward(sel, lambda i: xs[i], w, res.__getitem__, shp, qk_norm=g)
+    b, kvb = block_forward(sel, lambda i: xs[i], ws, res.__getitem__, shp, qk_norm=g)
+    c, _ = block_forward(sel, lambda i: xs[i], w, res.__getitem__, shp)
+    d, _ = block_forward(sel, lambda i: xs[i], ws, res.__getitem__, shp)
+    for i in range(2):
+        # eps / (mean square of the projection, about 1.3 here) bounds the change
+        np.testing.assert_allclose(b[i], a[i], rtol=0, atol=1e-4)
+        np.testing.assert_allclose(kvb[i][0], kva[i][0], rtol=0, atol=1e-4)
+        assert np.max(np.abs(d[i] - c[i])) > 1e-2
+        assert np.max(np.abs(a[i] - c[i])) > 1e-2
+
+
+def test_qk_norm_gains_enter_as_a_product():
+    """Gains constant over each RoPE pair commute with the rotation, so only
+    g_q * g_k reaches the logits: (s g, g / s) equals (g, g) up to rounding,
+    when the resident history's keys carry the same 1 / s."""
+    shp = _tiny_shape()
+    sel = select(policy("prog", 4, 2), [(1, 1), (2, 2)])
+    xs, res = _pack_inputs(shp, 8)
+    k0, v0 = res[(0, 0)]
+    res_s = {(0, 0): (k0 / 3.0, v0)}
+    w = _weights(shp, 0)
+    g = np.repeat(1.0 + normal((shp.hidden // 2,), (9, 41), 0.3).astype(np.float64), 2)
+    a, _ = block_forward(sel, lambda i: xs[i], w, res.__getitem__, shp, qk_norm=(g, g))
+    b, _ = block_forward(sel, lambda i: xs[i], w, res_s.__getitem__, shp,
+                         qk_norm=(3.0 * g, g / 3.0))
+    for i in range(2):
+        np.testing.assert_allclose(b[i], a[i], rtol=1e-12, atol=1e-12)
+
+
+def test_qk_norm_cached_keys_have_unit_rms_over_the_width():
+    """With unit gains each cached key has mean square 1 over the whole hidden
+    width (RoPE keeps lengths); the per-head mean squares differ, so the norm
+    does not act head by head."""
+    shp = _tiny_shape()
+    sel = select(policy("prog", 4, 2), [(0, 4)])
+    xs, _ = _pack_inputs(shp, 9, n=1)
+    one = np.ones(shp.hidden)
+    _, kv = block_forward(sel, lambda i: xs[i], _weights(shp, 0), None, shp, qk_norm=(one, one))
+    k = kv[0][0]
+    ms = np.mean(k.reshape(k.shape[0], -1) ** 2, axis=1)
+    np.testing.assert_allclose(ms, 1.0, rtol=1e-5)
+    per_head = np.mean(k ** 2, axis=2)
+    assert np.max(np.abs(per_head - 1.0)) > 1e-2
+
+
+def _cross(shp, L, seed, g_q=None, g_k=None):
+    from oracle.block import condition_kv
+    D = shp.hidden
+    ctx = normal((L, D), (seed, 50)).astype(np.float64)
+    wk, wv = (normal((D, D), (seed, 51 + s), 0.2).astype(np.float64) for s in range(2))
+    k, v = condition_kv(ctx, wk, wv, shp, g_k)
+    return {"k": k, "v": v, "g_q": g_q,
+            "w_q": normal((D, D), (seed, 53), 0.2).astype(np.float64),
+            "w_o": normal((D, D), (seed, 54), 0.2).astype(np.float64)}
+
+
+def test_cross_attention_with_zero_output_projection_is_the_plain_block():
+    shp = _tiny_shape()
+    sel = select(policy("prog", 4, 2), [(1, 1), (2, 2)])
+    xs, res = _pack_inputs(shp, 10)
+    cr = _cross(shp, 5, 0)
+    cr["w_o"][:] = 0.0
+    a, _ = block_forward(sel, lambda i: xs[i], _weights(shp, 0), res.__getitem__, shp)
+    b, _ = block_forward(sel, lambda i: xs[i], _weights(shp, 0), res.__getitem__, shp, cross=cr)
+    for i in range(2):
+        np.testing.assert_array_equal(b[i], a[i])
+
+
+def _no_mlp(shp):
+    w = _weights(shp, 0)
+    w["w_down"][:] = 0.0
+    return w
+
+
+def test_cross_attention_single_and_constant_keys():
+    """One condition token: every row adds v W_co^T.  Identical keys: every
+    row adds mean(V) W_co^T (uniform weights).  The MLP is switched off so the
+    block output is x' + cross term."""
+    shp = _tiny_shape()
+    sel = select(policy("prog", 4, 2), [(1, 1), (2, 2)])
+    xs, res = _pack_inputs(shp, 11)
+    w = _no_mlp(shp)
+    base, _ = block_forward(sel, lambda i: xs[i], w, res.__getitem__, shp)
+    one = _cross(shp, 1, 1)
+    y1, _ = block_forward(sel, lambda i: xs[i], w, res.__getitem__, shp, cross=one)
+    add1 = one["v"].reshape(1, -1) @ one["w_o"].T
+    flat = _cross(shp, 6, 2)
+    flat["k"] = np.repeat(flat["k"][:1], 6, axis=0)
+    yc, _ = block_forward(sel, lambda i: xs[i], w, res.__getitem__, shp, cross=flat)
+    addc = flat["v"].reshape(6, -1).mean(axis=0, keepdims=True) @ flat["w_o"].T
+    for i in range(2):
+        np.testing.assert_allclose(y1[i] - base[i], np.repeat(add1, len(xs[i]), 0), atol=1e-12)
+        np.testing.assert_allclose(yc[i] - base[i], np.repeat(addc, len(xs[i]), 0), atol=1e-12)
+
+
+def test_cross_attention_two_tokens_logistic_weights():
+    """Two condition tokens: the weight of the first is the logistic function
+    of the scaled logit difference, per head.  The cross query reads the
+    self-attention residual x' (the plain block without MLP gives x')."""
+    shp = _tiny_shape()
+    sel = select(policy("prog", 4, 2), [(0, 4)])
+    xs, _ = _pack_inputs(shp, 12, n=1)
+    w = _no_mlp(shp)
+    cr = _cross(shp, 2, 3)
+    y, _ = block_forward(sel, lambda i: xs[i], w, None, shp, cross=cr)
+    x1, _ = block_forward(sel, lambda i: xs[i], w, None, shp)
+    assert np.max(np.abs(x1[0] - xs[0])) > 1e-2
+    q = (rmsnorm(x1[0]) @ cr["w_q"].T).reshape(-1, 2, 16)
+    k, v = cr["k"], cr["v"]
+    o = np.zeros_like(q)
+    for h in range(2):
+        dl = (q[:, h] @ (k[0, h] - k[1, h])) / 4.0        # 1/sqrt(16)
+        p0 = 1.0 / (1.0 + np.exp(-dl))
+        o[:, h] = p0[:, None] * v[0, h] + (1.0 - p0)[:, None] * v[1, h]
+    np.testing.assert_allclose(y[0] - x1[0], o.reshape(len(q), -1) @ cr["w_o"].T, atol=1e-12)
+
+
+def test_cross_attention_feeds_the_mlp():
+    """Self-attention off (W_o = 0) and one condition token: the cross term is
+    the constant a = v W_co^T, so the block on x equals the plain block on
+    x + a (the MLP reads x + a)."""
+    shp = _tiny_shape()
+    sel = select(policy("prog", 4, 2), [(0, 4)])
+    xs, _ = _pack_inputs(shp, 15, n=1)
+    w = _weights(shp, 0)
+    w["w_o"][:] = 0.0
+    one = _cross(shp, 1, 8)
+    a = one["v"].reshape(1, -1) @ one["w_o"].T
+    y, _ = block_forward(sel, lambda i: xs[i], w, None, shp, cross=one)
+    ref, _ = block_forward(sel, lambda i: xs[i] + a, w, None, shp)
+    np.testing.assert_allclose(y[0], ref[0], rtol=1e-12, atol=1e-12)
+
+
+def test_cross_attention_zero_query_gain_is_uniform():
+    """g_cq = 0 zeroes every cross logit: each row adds mean(V) W_co^T."""
+    shp = _tiny_shape()
+    sel = select(policy("prog", 4, 2), [(1, 1), (2, 2)])
+    xs, res = _pack_inputs(shp, 16)
+    w = _no_mlp(shp)
+    base, _ = block_forward(sel, lambda i: xs[i], w, res.__getitem__, shp)
+    cr = _cross(shp, 5, 9, g_q=np.zeros(shp.hidden), g_k=_gains(shp, 2)[1])
+    y, _ = block_forward(sel, lambda i: xs[i], w, res.__getitem__, shp, cross=cr)
+    add = cr["v"].reshape(5, -1).mean(axis=0, keepdims=True) @ cr["w_o"].T
+    for i in range(2):
+        np.testing.assert_allclose(y[i] - base[i], np.repeat(add, len(xs[i]), 0), atol=1e-12)
+
+
+def test_cross_attention_ignores_condition_order_and_query_scale():
+    """The condition has no positions: permuting its tokens leaves the block
+    unchanged.  With the query norm (g_cq) the scale of W_cq drops out, and
+    only g_cq * g_ck reaches the logits."""
+    shp = _tiny_shape()
+    sel = select(policy("prog", 4, 2), [(1, 1), (2, 2)])
+    xs, res = _pack_inputs(shp, 13)
+    w = _weights(shp, 0)
+    g_q, g_k = _gains(shp, 4)
+    cr = _cross(shp, 7, 5, g_q=g_q, g_k=g_k)
+    perm = np.random.default_rng(0).permutation(7)
+    cp = dict(cr, k=cr["k"][perm], v=cr["v"][perm])
+    cs = dict(cr, w_q=cr["w_q"] * 5.0)
+    cg = _cross(shp, 7, 5, g_q=g_q * 4.0, g_k=g_k / 4.0)
+    a, _ = block_forward(sel, lambda i: xs[i], w, res.__getitem__, shp, cross=cr)
+    b, _ = block_forward(sel, lambda i: xs[i], w, res.__getitem__, shp, cross=cp)
+    c, _ = block_forward(sel, lambda i: xs[i], w, res.__getitem__, shp, cross=cs)
+    d, _ = block_forward(sel, lambda i: xs[i], w, res.__getitem__, shp, cross=cg)
+    for i in range(2):
+        np.testing.assert_allclose(b[i], a[i], rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(c[i], a[i], rtol=0, atol=1e-5)
+        np.testing.assert_allclose(d[i], a[i], rtol=1e-12, atol=1e-12)
+
+
+def test_cross_and_qk_norm_rows_subset_matches_full():
+    shp = _tiny_shape()
+    sel = select(policy("prog", 4, 2), [(1, 1), (2, 2)])
+    xs, res = _pack_inputs(shp, 14)
+    g = _gains(shp, 6)
+    cr = _cross(shp, 4, 7, g_q=g[0], g_k=g[1])
+    full, _ = block_forward(sel, lambda i: xs[i], _weights(shp, 0), res.__getitem__, shp,
+                           qk_norm=g, cross=cr)
+    rows = [1, 4, 10]
+    part, _ = block_forward(sel, lambda i: xs[i], _weights(shp, 0), res.__getitem__, shp,
+                            rows=rows, qk_norm=g, cross=cr)
+    for i in range(2):
+        np.testing.assert_array_equal(part[i], full[i][rows])
+
+
+def test_condition_kv_is_linear_and_key_norm_is_scale_free():
+    """V_c (and K_c without its norm) is linear in the condition; with the
+    norm, K_c ignores the condition's scale (up to eps)."""
+    from oracle.block import condition_kv
+    shp = _tiny_shape()
+    D = shp.hidden
+    c1, c2 = (normal((4, D), (17, s)).astype(np.float64) for s in range(2))
+    wk, wv = (normal((D, D), (17, 2 + s), 0.2).astype(np.float64) for s in range(2))
+    k1, v1 = condition_kv(c1, wk, wv, shp)
+    k2, v2 = condition_kv(c2, wk, wv, shp)
+    k3, v3 = condition_kv(2.0 * c1 - 0.5 * c2, wk, wv, shp)
+    np.testing.assert_allclose(v3, 2.0 * v1 - 0.5 * v2, atol=1e-12)
+    np.testing.assert_allclose(k3, 2.0 * k1 - 0.5 * k2, atol=1e-12)
+    g = _gains(shp, 3)[1]
+    kn, vn = condition_kv(c1, wk, wv, shp, g)
+    kb, vb = condition_kv(8.0 * c1, wk, wv, shp, g)
+    np.testing.assert_allclose(kb, kn, rtol=2e-6)       # eps / mean square, halved
+    np.testing.assert_allclose(vb, 8.0 * vn, atol=1e-12)
+    np.testing.assert_array_equal(vn, v1)
