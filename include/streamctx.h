@@ -32,7 +32,7 @@
 extern "C" {
 #endif
 
-#define SC_ABI_VERSION 4
+#define SC_ABI_VERSION 5
 
 enum {
   SC_OK = 0,
@@ -178,6 +178,17 @@ int sc_plan_get(const sc_plan* plan, int32_t* n_nodes, int32_t* n_pages,
                 const int32_t** page_tokens, const int32_t** page_frame);
 void sc_plan_free(sc_plan* plan);
 
+/* Plan over a condition cache: the condition c of Eq. 1 (e.g. text tokens)
+ * is read by every query of a node, with no visibility mask and no position.
+ * Node i of a pack reads all pages of the cached state conditions[i]
+ * (several nodes may name one state), with nq query rows per node -- the
+ * nq of the pack's own plan.  Each state must hold slots in the cache
+ * (written by sc_condition_append or sc_cache_append); whether a layer has
+ * been written is checked when the plan is used.  Errors: SC_EINVAL (null
+ * argument, n < 1 or nq < 1), SC_ENOTFOUND (a state not in the cache). */
+int sc_plan_condition(sc_cache* cache, const sc_node* conditions, int32_t n, int32_t nq,
+                      sc_plan** out);
+
 /* ---- Packed block-causal attention (Eq. 6 over the plan) ---------------
  * For every pack node i and head h:
  *   O_i = softmax(Q_i K_i^T * scale) V_i
@@ -197,6 +208,24 @@ void sc_plan_free(sc_plan* plan);
 size_t sc_attention_workspace_bytes(const sc_plan* plan, const sc_cache* cache);
 int sc_attention(const sc_plan* plan, const sc_cache* cache, int32_t layer, const void* q,
                  void* o, float scale, void* ws, size_t ws_bytes, sc_stream stream);
+
+/* ---- Condition K/V (the condition c of Eq. 1) ---------------------------
+ * Projects a condition sequence once per layer and caches it:
+ *   K_c = ctx Wk^T (then RMSNorm over the hidden width times k_norm, when
+ *         k_norm != NULL), V_c = ctx Wv^T, no RoPE,
+ * written into the pages of `state` in a condition cache whose geometry
+ * holds one condition per state (n_tokens = tokens_per_page *
+ * pages_per_chunk; hidden = n_heads * head_dim, a multiple of 256, head_dim
+ * 128, bf16).  ctx: device bf16 [n_tokens, hidden]; w_k, w_v: device bf16
+ * [hidden, hidden] in [out, in] layout; k_norm: device fp32 [hidden],
+ * 16-byte aligned, or NULL.  ws: device workspace of at least
+ * sc_condition_workspace_bytes(cache) bytes, 16-byte aligned.  Slots are
+ * allocated as by sc_cache_append.  Errors: SC_EEXIST (layer already
+ * written), SC_ECAPACITY, SC_EINVAL, SC_EUNSUPPORTED, SC_EDEVICE. */
+size_t sc_condition_workspace_bytes(const sc_cache* cache);
+int sc_condition_append(sc_cache* cache, int32_t layer, sc_node state, const void* ctx,
+                        const void* w_k, const void* w_v, const float* k_norm, void* ws,
+                        size_t ws_bytes, sc_stream stream);
 
 /* ---- One DiT block over the pack ----------------------------------------
  * The network F_theta of Eq. 1 for the packed nodes, one block (bf16 only):
@@ -219,7 +248,31 @@ int sc_attention(const sc_plan* plan, const sc_cache* cache, int32_t layer, cons
  *   x' = x + gate_a[j] * (o Wo^T)
  *   h2 = RMSNorm(x') * (1 + scale_m[j]) + shift_m[j]
  *   x  = x' + gate_m[j] * (GELU_tanh(h2 Wup^T) Wdown^T)
- * (elementwise over hidden).  mod == NULL is the unconditioned form above. */
+ * (elementwise over hidden).  mod == NULL is the unconditioned form above.
+ *
+ * qk-norm (optional, qk_norm != NULL): q and k are RMS-normalised over the
+ * whole hidden width and multiplied by the gains before RoPE:
+ *   q = RMSNorm(h Wq^T) * qk_norm[0:hidden], k = RMSNorm(h Wk^T) * qk_norm[hidden:2*hidden]
+ * (device fp32 [2][hidden], 16-byte aligned; the cached keys are the
+ * normalised ones).
+ *
+ * Cross-attention to the condition (optional, cross != NULL), after the
+ * self-attention residual and before the MLP, which then reads its result:
+ *   qc = RMSNorm(x') Wcq^T  [then RMSNorm(qc) * q_norm when q_norm != NULL]
+ *   x' = x' + Attn(qc, K_c, V_c) Wco^T       (scale 1/sqrt(head_dim))
+ * K_c, V_c are read through cross->plan (sc_plan_condition over
+ * cross->cache, one node per pack node, the pack plan's nq) at this layer;
+ * the condition cache has the block's head geometry.  The block forms are
+ * the Wan-shaped reading of F_theta (the paper does not define the network;
+ * c of Eq. 1 is read by cross-attention). */
+typedef struct {
+  const void* w_q;        /* [hidden, hidden] bf16 */
+  const void* w_o;        /* [hidden, hidden] bf16 */
+  const float* q_norm;    /* [hidden] fp32 gain, 16-byte aligned, or NULL */
+  const sc_cache* cache;  /* condition cache (bf16)                       */
+  const sc_plan* plan;    /* sc_plan_condition over that cache            */
+} sc_cross_attn;
+
 typedef struct {
   int32_t hidden, n_heads, head_dim, mlp;
   const void* w_qkv;  /* [3*hidden, hidden] */
@@ -228,6 +281,8 @@ typedef struct {
   const void* w_down; /* [hidden, mlp]      */
   const float* mod;   /* [mod_levels][6][hidden] fp32, or NULL */
   int32_t mod_levels;
+  const float* qk_norm;        /* [2][hidden] fp32 gains, or NULL */
+  const sc_cross_attn* cross;  /* or NULL */
 } sc_block_weights;
 size_t sc_block_workspace_bytes(const sc_block_weights* w, int32_t n_tokens);
 int sc_block_forward(const sc_block_weights* w, sc_cache* cache, int32_t layer,
@@ -279,7 +334,10 @@ int sc_stack_forward(const sc_block_weights* layers, int32_t n_layers, sc_cache*
  * summed elapsed milliseconds since the timer was last enabled.  Kinds:
  * "attention", "gemm_qkv", "gemm_out", "gemm_up", "gemm_down", "rmsnorm",
  * "append", "sampler", "attention_combine" (the merge of split key ranges;
- * "attention" is the main kernel alone).  Enabling clears earlier records.  Events are created
+ * "attention" is the main kernel alone), "qk_norm" (the per-token scaling of
+ * qk-norm and of the normalised condition queries and keys),
+ * "cross_attention", "gemm_cross_q", "gemm_cross_out", "gemm_condition"
+ * (the projections of sc_condition_append).  Enabling clears earlier records.  Events are created
  * lazily and reused; the cost is two event records per launch. */
 int sc_timer_enable(int on);
 int sc_timer_read(const char* kind, int32_t* launches, double* total_ms);

@@ -21,7 +21,8 @@ __all__ = [
     "sc_rope_table_bytes", "sc_rope_table_build", "sc_plan_build", "sc_attention",
     "sc_attention_workspace_bytes", "sc_block_workspace_bytes", "sc_block_forward", "sc_sampler_step",
     "sc_timer_enable", "sc_timer_read", "sc_probe_mfma_out_bytes", "sc_probe_mfma",
-    "Selection", "Cache", "Plan", "Rope", "BlockWeights",
+    "Selection", "Cache", "Plan", "Rope", "BlockWeights", "CrossAttn",
+    "sc_plan_condition", "sc_condition_workspace_bytes", "sc_condition_append",
     "sc_pipeline_rounds", "sc_pipeline_round_nodes", "sc_cache_release_unread", "sc_stack_forward",
 ]
 
@@ -38,7 +39,8 @@ EXPORTED_SYMBOLS = [
     "sc_cache_pool_bytes", "sc_cache_create", "sc_cache_free", "sc_cache_contains",
     "sc_cache_slots", "sc_cache_free_slot_count", "sc_cache_release", "sc_cache_append",
     "sc_rope_table_bytes", "sc_rope_table_build",
-    "sc_plan_build", "sc_plan_get", "sc_plan_free",
+    "sc_plan_build", "sc_plan_get", "sc_plan_free", "sc_plan_condition",
+    "sc_condition_workspace_bytes", "sc_condition_append",
     "sc_attention_workspace_bytes", "sc_attention",
     "sc_block_workspace_bytes", "sc_block_forward", "sc_sampler_step",
     "sc_timer_enable", "sc_timer_read", "sc_probe_mfma_out_bytes", "sc_probe_mfma",
@@ -94,11 +96,17 @@ class sc_rope(C.Structure):
     _fields_ = [("desc", sc_rope_desc), ("dev_table", C.c_void_p)]
 
 
+class sc_cross_attn(C.Structure):
+    _fields_ = [("w_q", C.c_void_p), ("w_o", C.c_void_p), ("q_norm", C.c_void_p),
+                ("cache", C.c_void_p), ("plan", C.c_void_p)]
+
+
 class sc_block_weights(C.Structure):
     _fields_ = [("hidden", C.c_int32), ("n_heads", C.c_int32), ("head_dim", C.c_int32),
                 ("mlp", C.c_int32), ("w_qkv", C.c_void_p), ("w_o", C.c_void_p),
                 ("w_up", C.c_void_p), ("w_down", C.c_void_p), ("mod", C.c_void_p),
-                ("mod_levels", C.c_int32)]
+                ("mod_levels", C.c_int32), ("qk_norm", C.c_void_p),
+                ("cross", C.POINTER(sc_cross_attn))]
 
 
 _P = C.c_void_p
@@ -125,6 +133,9 @@ _SIG = {
     "sc_plan_build": (C.c_int, [_P, _P, C.POINTER(_P)]),
     "sc_plan_get": (C.c_int, [_P, _I32P, _I32P] + [C.POINTER(_I32P)] * 4),
     "sc_plan_free": (None, [_P]),
+    "sc_plan_condition": (C.c_int, [_P, C.POINTER(sc_node), C.c_int32, C.c_int32, C.POINTER(_P)]),
+    "sc_condition_workspace_bytes": (C.c_size_t, [_P]),
+    "sc_condition_append": (C.c_int, [_P, C.c_int32, sc_node, _P, _P, _P, _P, _P, C.c_size_t, _P]),
     "sc_attention_workspace_bytes": (C.c_size_t, [_P, _P]),
     "sc_attention": (C.c_int, [_P, _P, C.c_int32, _P, _P, C.c_float, _P, C.c_size_t, _P]),
     "sc_block_workspace_bytes": (C.c_size_t, [C.POINTER(sc_block_weights), C.c_int32]),
@@ -144,7 +155,7 @@ _SIG = {
                                    C.POINTER(sc_rope), _P, C.c_size_t, _P]),
 }
 # ABI version this binding marshals for (SC_ABI_VERSION of the header)
-ABI_VERSION = 4
+ABI_VERSION = 5
 if not hasattr(lib, "sc_abi_version") or lib.sc_abi_version() != ABI_VERSION:
     raise ImportError(f"{library_path} does not implement ABI version {ABI_VERSION}; rebuild it "
                       "(__graft_entry__.build())")
@@ -364,6 +375,25 @@ def sc_plan_build(sel: Selection, cache: Cache) -> Plan:
     return Plan(out.value, cache)
 
 
+def sc_plan_condition(cache: Cache, conditions, nq: int) -> Plan:
+    """Plan in which pack node i reads every page of the cached condition
+    state conditions[i], with nq query rows per node."""
+    arr = (sc_node * max(1, len(conditions)))(*[sc_node(int(c), int(j)) for c, j in conditions])
+    out = C.c_void_p()
+    _check(lib.sc_plan_condition(cache.handle, arr, len(conditions), nq, C.byref(out)))
+    return Plan(out.value, cache)
+
+
+def sc_condition_workspace_bytes(cache: Cache) -> int:
+    return lib.sc_condition_workspace_bytes(cache.handle)
+
+
+def sc_condition_append(cache: Cache, layer: int, state, ctx, w_k, w_v, k_norm, ws, ws_bytes: int,
+                        stream=None) -> None:
+    _check(lib.sc_condition_append(cache.handle, layer, sc_node(*state), _ptr(ctx), _ptr(w_k),
+                                   _ptr(w_v), _ptr(k_norm), _ptr(ws), ws_bytes, _stream(stream)))
+
+
 def sc_attention_workspace_bytes(plan: Plan, cache: Cache) -> int:
     return lib.sc_attention_workspace_bytes(plan.handle, cache.handle)
 
@@ -375,15 +405,30 @@ def sc_attention(plan: Plan, cache: Cache, layer: int, q, o, scale: float, ws=No
 
 
 # ---------------------------------------------------------------------- block
+class CrossAttn:
+    """Cross-attention of a block to a condition cache: device weights w_q,
+    w_o, optional fp32 query gain q_norm, the condition cache and its plan
+    (sc_plan_condition)."""
+
+    def __init__(self, w_q, w_o, cache: "Cache", plan: "Plan", q_norm=None):
+        self.refs = (w_q, w_o, q_norm, cache, plan)
+        self.struct = sc_cross_attn(_ptr(w_q), _ptr(w_o), _ptr(q_norm), cache.handle.value,
+                                    plan.handle.value)
+
+
 class BlockWeights:
     """Device weights of one block; ``mod`` is the optional fp32 per-level
-    modulation table [levels][6][hidden] (noise-level conditioning)."""
+    modulation table [levels][6][hidden] (noise-level conditioning),
+    ``qk_norm`` the optional fp32 gains [2][hidden] of q and k, ``cross``
+    the optional CrossAttn."""
 
-    def __init__(self, hidden, n_heads, head_dim, mlp, w_qkv, w_o, w_up, w_down, mod=None):
-        self.tensors = (w_qkv, w_o, w_up, w_down, mod)
+    def __init__(self, hidden, n_heads, head_dim, mlp, w_qkv, w_o, w_up, w_down, mod=None,
+                 qk_norm=None, cross: Optional[CrossAttn] = None):
+        self.tensors = (w_qkv, w_o, w_up, w_down, mod, qk_norm, cross)
         levels = 0 if mod is None else int(mod.shape[0])
+        cp = C.pointer(cross.struct) if cross is not None else None
         self.struct = sc_block_weights(hidden, n_heads, head_dim, mlp, _ptr(w_qkv), _ptr(w_o),
-                                       _ptr(w_up), _ptr(w_down), _ptr(mod), levels)
+                                       _ptr(w_up), _ptr(w_down), _ptr(mod), levels, _ptr(qk_norm), cp)
 
 
 def sc_block_workspace_bytes(w: BlockWeights, n_tokens: int) -> int:

@@ -754,13 +754,28 @@ size_t attention_workspace_bytes(const sc_plan* p, const sc_cache* c) {
 
 size_t attention_workspace_bound() { return (size_t)kAttnMaxPieces * BQ_MAX * (HDB + 2) * sizeof(float); }
 
-int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const void* q, void* o,
-                     float scale, void* ws, size_t ws_bytes, hipStream_t stream) {
+int attention_check(const sc_plan* p, const sc_cache* c) {
   const sc_cache_desc& d = c->d;
   const int32_t n = (int32_t)p->nodes.size();
   if (n > kMaxNodes) return fail(SC_EUNSUPPORTED, "pack of %d nodes exceeds %d", n, kMaxNodes);
   if ((int32_t)p->page_slot.size() > kMaxPages)
     return fail(SC_EUNSUPPORTED, "plan of %zu pages exceeds %d", p->page_slot.size(), kMaxPages);
+  if (d.dtype == SC_DTYPE_F32) return SC_OK;
+  if (d.head_dim != HDB) return fail(SC_EUNSUPPORTED, "bf16 attention needs head_dim 128");
+  if (d.tokens_per_page < BK)
+    return fail(SC_EUNSUPPORTED, "bf16 attention needs pages of >= %d tokens (got %d)", BK,
+                d.tokens_per_page);
+  if ((uint64_t)d.n_slots * c->slot_bytes > 0xffffffffull)
+    return fail(SC_EUNSUPPORTED, "bf16 attention needs one layer of the pool within 4 GB");
+  return SC_OK;
+}
+
+int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const void* q, void* o,
+                     float scale, void* ws, size_t ws_bytes, hipStream_t stream) {
+  const sc_cache_desc& d = c->d;
+  const int32_t n = (int32_t)p->nodes.size();
+  const int rc = attention_check(p, c);
+  if (rc != SC_OK) return rc;
   AttnPlan plan;
   for (int32_t i = 0; i <= n; ++i) plan.page_off[i] = p->page_off[i];
   for (size_t i = 0; i < p->page_slot.size(); ++i) plan.page_slot[i] = p->page_slot[i];
@@ -790,12 +805,6 @@ int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const v
     SC_HIP(hipGetLastError());
     return SC_OK;
   }
-  if (d.head_dim != HDB) return fail(SC_EUNSUPPORTED, "bf16 attention needs head_dim 128");
-  if (d.tokens_per_page < BK)
-    return fail(SC_EUNSUPPORTED, "bf16 attention needs pages of >= %d tokens (got %d)", BK,
-                d.tokens_per_page);
-  if ((uint64_t)d.n_slots * c->slot_bytes > 0xffffffffull)
-    return fail(SC_EUNSUPPORTED, "bf16 attention needs one layer of the pool within 4 GB");
   const size_t need = attention_workspace_bytes(p, c);
   if (ws_bytes < need || (need && !ws))
     return fail(SC_EINVAL, "attention workspace of %zu bytes, need %zu", ws_bytes, need);

@@ -1,9 +1,12 @@
 // One DiT block over a pack of nodes: launch sequence and argument checks.
-// RMSNorm -> QKV GEMM (+RoPE, q out, k/v into the pack's page slots) ->
-// packed attention -> out-projection (+residual) -> RMSNorm -> MLP up (+GELU)
-// -> MLP down (+residual).  Stream order makes "append before attend" hold,
-// which is what lets a node read the K/V an older pack node computes in the
-// same forward (the joint causal forward of Sec. 3.3).
+// RMSNorm -> QKV GEMM (+RoPE, q out, k/v into the pack's page slots)
+// [-> qk-norm scaling] -> packed attention -> out-projection (+residual)
+// [-> RMSNorm -> condition query GEMM [-> its norm] -> attention over the
+// condition cache -> condition out-projection (+residual)] -> RMSNorm ->
+// MLP up (+GELU) -> MLP down (+residual).  Stream order makes "append before
+// attend" hold, which is what lets a node read the K/V an older pack node
+// computes in the same forward (the joint causal forward of Sec. 3.3).
+// Also the condition's K/V projection (sc_condition_append).
 #include <cstring>
 
 #include "gemm.h"
@@ -13,10 +16,35 @@ using namespace sc;
 
 static size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
 
+constexpr float kNormEps = 1e-6f;
+
+// workspace: normalised input | q | attention output | MLP hidden |
+// attention partials | qk-norm partial sums of squares
 extern "C" size_t sc_block_workspace_bytes(const sc_block_weights* w, int32_t n_tokens) {
   if (!w || n_tokens <= 0) return 0;
   const size_t T = (size_t)n_tokens;
-  return align256(T * w->hidden * 2) * 3 + align256(T * w->mlp * 2) + attention_workspace_bound();
+  return align256(T * w->hidden * 2) * 3 + align256(T * w->mlp * 2) + attention_workspace_bound() +
+         align256(T * (2 * w->hidden / 128) * 4);
+}
+
+static bool misaligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) & 15; }
+
+// Checks of the optional cross-attention against the block's pack plan.
+static int cross_check(const sc_cross_attn* cr, const sc_cache* c, const sc_plan* p, int32_t layer) {
+  if (!cr->w_q || !cr->w_o || !cr->cache || !cr->plan)
+    return fail(SC_EINVAL, "cross-attention needs w_q, w_o, a condition cache and its plan");
+  const sc_cache_desc& e = cr->cache->d;
+  if (e.dtype != SC_DTYPE_BF16 || e.n_heads != c->d.n_heads || e.head_dim != c->d.head_dim)
+    return fail(SC_EINVAL, "condition cache (%d heads x %d, dtype %d) does not match the block",
+                e.n_heads, e.head_dim, e.dtype);
+  if (cr->plan->nodes.size() != p->nodes.size() || cr->plan->nq != p->nq)
+    return fail(SC_EINVAL, "condition plan has %zu nodes of %d queries, the pack %zu of %d",
+                cr->plan->nodes.size(), cr->plan->nq, p->nodes.size(), p->nq);
+  if (cr->q_norm && misaligned16(cr->q_norm))
+    return fail(SC_EINVAL, "condition query gain must be 16-byte aligned");
+  int rc = plan_check(cr->plan, cr->cache, layer);
+  if (rc != SC_OK) return rc;
+  return attention_check(cr->plan, cr->cache);
 }
 
 extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t layer,
@@ -52,6 +80,11 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
   nm_m.which = 1;
   if (ws_bytes < sc_block_workspace_bytes(w, T))
     return fail(SC_EINVAL, "workspace of %zu bytes, need %zu", ws_bytes, sc_block_workspace_bytes(w, T));
+  if (misaligned16(ws)) return fail(SC_EINVAL, "workspace must be 16-byte aligned");
+  if (w->qk_norm && misaligned16(w->qk_norm)) return fail(SC_EINVAL, "qk-norm gains must be 16-byte aligned");
+  int rc = attention_check(p, c);
+  if (rc != SC_OK) return rc;
+  if (w->cross && (rc = cross_check(w->cross, c, p, layer)) != SC_OK) return rc;
   if (rope) {
     const sc_rope_desc& r = rope->desc;
     if (!rope->dev_table || r.grid_h * r.grid_w != d.tokens_per_page ||
@@ -94,6 +127,7 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
   uint16_t* ob = reinterpret_cast<uint16_t*>(wsb + 2 * align256((size_t)T * w->hidden * 2));
   uint16_t* ub = reinterpret_cast<uint16_t*>(wsb + 3 * align256((size_t)T * w->hidden * 2));
   char* attn_ws = wsb + 3 * align256((size_t)T * w->hidden * 2) + align256((size_t)T * w->mlp * 2);
+  float* ssb = reinterpret_cast<float*>(attn_ws + attention_workspace_bound());
   uint16_t* xb = static_cast<uint16_t*>(x);
   const int32_t D = w->hidden;
 
@@ -119,10 +153,33 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
     ep.grid_w = 1;
   }
 
-  int rc;
+  if (w->qk_norm) {
+    ep.ss_part = ssb;
+    ep.n_part = 2 * D / 128;
+    ep.qk_gain = w->qk_norm;
+  }
+
   if ((rc = launch_rmsnorm(xb, hn, T, D, nm_a, stream)) != SC_OK) return rc;
   if ((rc = launch_gemm(EPI_QKV, TK_GEMM_QKV, static_cast<const uint16_t*>(w->w_qkv), hn, 3 * D, T, D, ep, stream)) != SC_OK)
     return rc;
+  if (w->qk_norm) {  // 1 / rms of q (token-major) and of k (in the page slots)
+    NormScale ns;
+    std::memset(&ns, 0, sizeof ns);
+    ns.part = ssb;
+    ns.n_part = 2 * D / 128;
+    ns.D = D;
+    ns.eps = kNormEps;
+    ns.rows = qb;
+    ns.ld = D;
+    ns.layer_base = ep.layer_base;
+    ns.slot_bytes = ep.slot_bytes;
+    ns.nq = p->nq;
+    ns.tpp = d.tokens_per_page;
+    ns.ppc = d.pages_per_chunk;
+    ns.head_dim = d.head_dim;
+    std::memcpy(ns.node_slot, ep.node_slot, sizeof ns.node_slot);
+    if ((rc = launch_norm_scale(T, ns, stream)) != SC_OK) return rc;
+  }
   for (int32_t i = 0; i < n; ++i)
     c->states.at(StateKey(p->nodes[i].chunk, p->nodes[i].level)).written[layer] = 1;
   if ((rc = launch_attention(p, c, layer, qb, ob, 1.0f / std::sqrt((float)d.head_dim), attn_ws,
@@ -138,6 +195,47 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
   for (int32_t i = 0; i < n; ++i) e2.node_level[i] = p->nodes[i].level;
   if ((rc = launch_gemm(EPI_RESIDUAL, TK_GEMM_OUT, static_cast<const uint16_t*>(w->w_o), ob, D, T, D, e2, stream)) != SC_OK)
     return rc;
+  if (const sc_cross_attn* cr = w->cross) {
+    NormMod plain;
+    std::memset(&plain, 0, sizeof plain);
+    plain.nq = p->nq;
+    if ((rc = launch_rmsnorm(xb, hn, T, D, plain, stream)) != SC_OK) return rc;
+    GemmEpilogue ec;
+    std::memset(&ec, 0, sizeof ec);
+    ec.out = qb;
+    ec.ld_out = D;
+    if (cr->q_norm) {
+      ec.ss_part = ssb;
+      ec.n_part = D / 128;
+    }
+    if ((rc = launch_gemm(EPI_STORE, TK_GEMM_CROSS_Q, static_cast<const uint16_t*>(cr->w_q), hn, D, T, D, ec, stream)) != SC_OK)
+      return rc;
+    if (cr->q_norm) {
+      NormScale ns;
+      std::memset(&ns, 0, sizeof ns);
+      ns.part = ssb;
+      ns.n_part = D / 128;
+      ns.D = D;
+      ns.eps = kNormEps;
+      ns.rows = qb;
+      ns.ld = D;
+      ns.gain = cr->q_norm;
+      if ((rc = launch_norm_scale(T, ns, stream)) != SC_OK) return rc;
+    }
+    {
+      TimerAlias alias(TK_ATTENTION, TK_CROSS_ATTENTION);
+      if ((rc = launch_attention(cr->plan, cr->cache, layer, qb, ob, 1.0f / std::sqrt((float)d.head_dim),
+                                 attn_ws, attention_workspace_bound(), stream)) != SC_OK)
+        return rc;
+    }
+    GemmEpilogue eo;
+    std::memset(&eo, 0, sizeof eo);
+    eo.out = xb;
+    eo.ld_out = D;
+    eo.nq = p->nq;
+    if ((rc = launch_gemm(EPI_RESIDUAL, TK_GEMM_CROSS_OUT, static_cast<const uint16_t*>(cr->w_o), ob, D, T, D, eo, stream)) != SC_OK)
+      return rc;
+  }
   if ((rc = launch_rmsnorm(xb, hn, T, D, nm_m, stream)) != SC_OK) return rc;
   GemmEpilogue e3;
   std::memset(&e3, 0, sizeof e3);
@@ -150,4 +248,68 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
   if ((rc = launch_gemm(EPI_RESIDUAL, TK_GEMM_DOWN, static_cast<const uint16_t*>(w->w_down), ub, D, T, w->mlp, e4, stream)) != SC_OK)
     return rc;
   return SC_OK;
+}
+
+extern "C" size_t sc_condition_workspace_bytes(const sc_cache* c) {
+  if (!c) return 0;
+  const size_t L = (size_t)c->d.tokens_per_page * c->d.pages_per_chunk;
+  const size_t D = (size_t)c->d.n_heads * c->d.head_dim;
+  return 2 * align256(L * D * 2) + align256(L * (D / 128) * 4);
+}
+
+extern "C" int sc_condition_append(sc_cache* c, int32_t layer, sc_node st, const void* ctx,
+                                   const void* w_k, const void* w_v, const float* k_norm, void* ws,
+                                   size_t ws_bytes, sc_stream stream_) {
+  if (!c || !ctx || !w_k || !w_v || !ws) return fail(SC_EINVAL, "null argument");
+  const sc_cache_desc& d = c->d;
+  if (d.dtype != SC_DTYPE_BF16) return fail(SC_EUNSUPPORTED, "condition projection is bf16 only");
+  const int32_t D = d.n_heads * d.head_dim;
+  const int32_t L = d.tokens_per_page * d.pages_per_chunk;
+  if (d.head_dim != 128 || D % 256)
+    return fail(SC_EUNSUPPORTED, "condition projection needs head_dim 128 and hidden %% 256 == 0");
+  if (layer < 0 || layer >= d.n_layers) return fail(SC_EINVAL, "layer %d out of range", layer);
+  if (st.chunk < 0 || st.level < 0) return fail(SC_EINVAL, "bad state (%d,%d)", st.chunk, st.level);
+  auto it = c->states.find(StateKey(st.chunk, st.level));
+  if (it != c->states.end() && it->second.written[layer])
+    return fail(SC_EEXIST, "state (%d,%d) layer %d already written", st.chunk, st.level, layer);
+  if (it == c->states.end() && sc_cache_free_slot_count(c) < d.pages_per_chunk)
+    return fail(SC_ECAPACITY, "no free slots for condition (%d,%d)", st.chunk, st.level);
+  if (ws_bytes < sc_condition_workspace_bytes(c))
+    return fail(SC_EINVAL, "workspace of %zu bytes, need %zu", ws_bytes, sc_condition_workspace_bytes(c));
+  if (misaligned16(ws) || (k_norm && misaligned16(k_norm)))
+    return fail(SC_EINVAL, "workspace and key gain must be 16-byte aligned");
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  char* wsb = static_cast<char*>(ws);
+  uint16_t* kb = reinterpret_cast<uint16_t*>(wsb);
+  uint16_t* vb = reinterpret_cast<uint16_t*>(wsb + align256((size_t)L * D * 2));
+  float* ssb = reinterpret_cast<float*>(wsb + 2 * align256((size_t)L * D * 2));
+  const uint16_t* xb = static_cast<const uint16_t*>(ctx);
+  GemmEpilogue e;
+  std::memset(&e, 0, sizeof e);
+  e.out = kb;
+  e.ld_out = D;
+  if (k_norm) {
+    e.ss_part = ssb;
+    e.n_part = D / 128;
+  }
+  int rc;
+  if ((rc = launch_gemm(EPI_STORE, TK_GEMM_CONDITION, static_cast<const uint16_t*>(w_k), xb, D, L, D, e, stream)) != SC_OK)
+    return rc;
+  if (k_norm) {
+    NormScale ns;
+    std::memset(&ns, 0, sizeof ns);
+    ns.part = ssb;
+    ns.n_part = D / 128;
+    ns.D = D;
+    ns.eps = kNormEps;
+    ns.rows = kb;
+    ns.ld = D;
+    ns.gain = k_norm;
+    if ((rc = launch_norm_scale(L, ns, stream)) != SC_OK) return rc;
+  }
+  e.out = vb;
+  e.ss_part = nullptr;
+  if ((rc = launch_gemm(EPI_STORE, TK_GEMM_CONDITION, static_cast<const uint16_t*>(w_v), xb, D, L, D, e, stream)) != SC_OK)
+    return rc;
+  return sc_cache_append(c, layer, st, kb, vb, nullptr, stream_);
 }

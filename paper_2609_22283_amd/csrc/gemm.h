@@ -30,6 +30,32 @@ struct GemmEpilogue {
   const float* mod;
   int32_t gate_row;
   int32_t node_level[kGemmMaxNodes];
+  // Sums of squares for a later RMSNorm over features (qk-norm), STORE and
+  // QKV (q and k sections): ss_part[t * n_part + f / 128] = sum of D[f'][t]^2
+  // over the 128 features f' of f's wave tile, before any gain or RoPE.
+  // NULL: none.  QKV with ss_part also multiplies q and k by qk_gain
+  // ([2][hidden], the gains of q then k) before RoPE.
+  float* ss_part;
+  int32_t n_part;
+  const float* qk_gain;
+};
+
+// Second half of an RMSNorm whose sums of squares came from a GEMM epilogue:
+// for each token t, inv = 1 / sqrt(sum_p part[t * n_part + p0 + p] / D + eps)
+// over the D / 128 partials of one tensor, then
+//   rows[t][:] *= inv (* gain[:] when gain != NULL)   (token-major, q)
+//   the token's k rows in its node's page slot *= inv  (k of the QKV pass)
+struct NormScale {
+  const float* part;
+  int32_t n_part, D;
+  float eps;
+  uint16_t* rows;          // token-major [T][ld] rows (part offset 0), or NULL
+  int32_t ld;
+  const float* gain;       // [D] fp32 for rows, or NULL
+  char* layer_base;        // page-slot keys (part offset D / 128), or NULL
+  uint64_t slot_bytes;
+  int32_t nq, tpp, ppc, head_dim;
+  int32_t node_slot[kGemmMaxNodePages];
 };
 
 // Per-level shift/scale after RMSNorm (noise-level conditioning): row r of
@@ -43,6 +69,7 @@ struct NormMod {
 
 int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, int32_t F, int32_t T,
                 int32_t Kd, const GemmEpilogue& ep, hipStream_t stream);
+int launch_norm_scale(int32_t T, const NormScale& ns, hipStream_t stream);
 int launch_rmsnorm(const uint16_t* x, uint16_t* y, int32_t rows, int32_t D, const NormMod& nm,
                    hipStream_t stream);
 

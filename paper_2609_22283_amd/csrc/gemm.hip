@@ -8,6 +8,10 @@
 //            [head][d][token])
 //   GELU     out[t][f] = GELU_tanh(D)
 //   RESIDUAL x[t][f] += D   (in place)
+//   STORE    out[t][f] = D
+// QKV and STORE can also emit per-token sums of squares over each wave's 128
+// features, the first half of an RMSNorm over the feature axis (qk-norm);
+// norm_scale_kernel finishes it.
 // Work-group tile 256 (features) x 256 (tokens) x 64 (k), eight waves of
 // 128 x 64, operands double-buffered in LDS with an XOR swizzle.  Each lane
 // holds four consecutive features of one token, so RoPE pairs stay in-lane.
@@ -40,6 +44,27 @@ __device__ __forceinline__ void gdma16(const char* src, char* lds_wave_base) {
                                    reinterpret_cast<__attribute__((address_space(3))) void*>(
                                        reinterpret_cast<uintptr_t>(lds_wave_base)),
                                    16, 0, 0);
+}
+
+// Per-token sum of squares of a wave's 128 x 64 accumulator tile: lane
+// (lg, c16) holds 32 features of token c16 of each 16-token block; the four
+// lg lanes of a token are summed with two butterflies and lane lg = 0 stores.
+template <int FB, int TB>
+__device__ __forceinline__ void store_sum_squares(const f32x4 (&acc)[FB][TB], float* ss,
+                                                  int32_t n_part, int32_t part, int32_t tw0,
+                                                  int32_t T, int32_t lg, int32_t c16) {
+#pragma unroll
+  for (int tb = 0; tb < TB; ++tb) {
+    float s = 0.f;
+#pragma unroll
+    for (int fb = 0; fb < FB; ++fb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s = fmaf(acc[fb][tb][e], acc[fb][tb][e], s);
+    s += __shfl_xor(s, 16);
+    s += __shfl_xor(s, 32);
+    const int32_t t = tw0 + 16 * tb + c16;
+    if (lg == 0 && t < T) ss[(size_t)t * n_part + part] = s;
+  }
 }
 
 template <int EPI>
@@ -154,6 +179,20 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
     const int32_t hf0 = f0 - sec * ep.hidden + wf;       // wave's first feature in its section
     const int32_t head = hf0 / ep.head_dim;
     const int32_t dbase = hf0 - head * ep.head_dim + 4 * lg;
+    if (ep.ss_part && sec < 2) {
+      // qk-norm: sums of squares of the raw q or k, then the gain (before
+      // RoPE); the 1 / rms factor is applied by norm_scale_kernel
+      store_sum_squares(acc, ep.ss_part, ep.n_part, (f0 + wf) / GWM, t0 + wt, T, lg, c16);
+      const float* g = ep.qk_gain + f0 + wf + 4 * lg;
+#pragma unroll
+      for (int fb = 0; fb < FB; ++fb) {
+        const f32x4 gv = *reinterpret_cast<const f32x4*>(g + 16 * fb);
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[fb][tb][e] *= gv[e];
+      }
+    }
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
       const int32_t t = t0 + wt + 16 * tb + c16;
@@ -204,6 +243,8 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
         }
     }
   } else {
+    if (EPI == EPI_STORE && ep.ss_part)
+      store_sum_squares(acc, ep.ss_part, ep.n_part, (f0 + wf) / GWM, t0 + wt, T, lg, c16);
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
       const int32_t t = t0 + wt + 16 * tb + c16;
@@ -329,6 +370,73 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
     for (int k = 0; k < 4; ++k) r[k] = pack_bf16x2(f[2 * k], f[2 * k + 1]);
     yr[v] = r;
   }
+}
+
+// ------------------------------------------------------- RMSNorm, second half
+// One wave per token: the token's 1 / rms from the GEMM's partial sums of
+// squares (summed in a fixed order), applied in place to its q row
+// (token-major, with the optional gain) and to its k rows in the page slot.
+__global__ __launch_bounds__(256) void norm_scale_kernel(int32_t T, NormScale ns) {
+  const int32_t t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int32_t lane = threadIdx.x & 63;
+  if (t >= T) return;
+  const int32_t np = ns.D / 128, nv = ns.D / 8;
+  const float* pr = ns.part + (size_t)t * ns.n_part;
+  auto scale8 = [&](u32x4* p, float inv, const float* gain) {
+    const u32x4 a = *p;
+    float f[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      f[2 * k] = __uint_as_float(a[k] << 16) * inv;
+      f[2 * k + 1] = __uint_as_float(a[k] & 0xffff0000u) * inv;
+    }
+    if (gain) {
+      const f32x4 g0 = *reinterpret_cast<const f32x4*>(gain);
+      const f32x4 g1 = *reinterpret_cast<const f32x4*>(gain + 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        f[e] *= g0[e];
+        f[4 + e] *= g1[e];
+      }
+    }
+    u32x4 r;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) r[k] = pack_bf16x2(f[2 * k], f[2 * k + 1]);
+    *p = r;
+  };
+  if (ns.rows) {
+    float s = 0.f;
+    for (int32_t p = 0; p < np; ++p) s += pr[p];
+    const float inv = rsqrtf(s / (float)ns.D + ns.eps);
+    u32x4* row = reinterpret_cast<u32x4*>(ns.rows + (size_t)t * ns.ld);
+    for (int32_t v = lane; v < nv; v += 64) scale8(row + v, inv, ns.gain ? ns.gain + 8 * v : nullptr);
+  }
+  if (ns.layer_base) {
+    float s = 0.f;
+    for (int32_t p = 0; p < np; ++p) s += pr[np + p];
+    const float inv = rsqrtf(s / (float)ns.D + ns.eps);
+    const int32_t node = t / ns.nq, tok = t - node * ns.nq;
+    const int32_t frame = tok / ns.tpp, n = tok - frame * ns.tpp;
+    uint16_t* kb = reinterpret_cast<uint16_t*>(
+        ns.layer_base + (size_t)ns.node_slot[node * ns.ppc + frame] * ns.slot_bytes);
+    const int32_t vph = ns.head_dim / 8;  // 16-byte vectors per head row
+    for (int32_t v = lane; v < nv; v += 64) {
+      const int32_t head = v / vph, c = v - head * vph;
+      scale8(reinterpret_cast<u32x4*>(kb + ((size_t)head * ns.tpp + n) * ns.head_dim + 8 * c), inv,
+             nullptr);
+    }
+  }
+}
+
+int launch_norm_scale(int32_t T, const NormScale& ns, hipStream_t stream) {
+  if (ns.D % 128 || (ns.layer_base && ns.head_dim % 8))
+    return fail(SC_EUNSUPPORTED, "qk-norm needs hidden %% 128 == 0 (got %d)", ns.D);
+  if (T <= 0) return SC_OK;
+  timer_begin(TK_QK_NORM, stream);
+  hipLaunchKernelGGL(norm_scale_kernel, dim3((T + 3) / 4), dim3(256), 0, stream, T, ns);
+  timer_end(TK_QK_NORM, stream);
+  SC_HIP(hipGetLastError());
+  return SC_OK;
 }
 
 int launch_rmsnorm(const uint16_t* x, uint16_t* y, int32_t rows, int32_t D, const NormMod& nm,

@@ -386,6 +386,37 @@ int sc_plan_get(const sc_plan* p, int32_t* n_nodes, int32_t* n_pages, const int3
 
 void sc_plan_free(sc_plan* p) { delete p; }
 
+int sc_plan_condition(sc_cache* c, const sc_node* conds, int32_t n, int32_t nq, sc_plan** out) {
+  if (!c || !conds || !out) return fail(SC_EINVAL, "null argument");
+  *out = nullptr;
+  if (n < 1 || nq < 1) return fail(SC_EINVAL, "need n >= 1 and nq >= 1 (n=%d nq=%d)", n, nq);
+  for (int32_t i = 0; i < n; ++i)
+    if (!c->states.count(StateKey(conds[i].chunk, conds[i].level)))
+      return fail(SC_ENOTFOUND, "condition state (%d,%d) not in the cache", conds[i].chunk,
+                  conds[i].level);
+  sc_plan* p = new (std::nothrow) sc_plan;
+  if (!p) return fail(SC_EINVAL, "out of host memory");
+  p->nodes.assign(conds, conds + n);
+  p->cache = c;
+  p->nq = nq;
+  p->page_off.push_back(0);
+  const int32_t ppc = c->d.pages_per_chunk;
+  for (int32_t i = 0; i < n; ++i) {
+    const StateKey key(conds[i].chunk, conds[i].level);
+    const StateEntry& e = c->states.at(key);
+    for (int32_t f = 0; f < ppc; ++f) {
+      p->page_slot.push_back(e.slots[f]);
+      p->page_tokens.push_back(c->d.tokens_per_page);
+      p->page_frame.push_back(f);
+      p->page_gen.push_back(c->gen[e.slots[f]]);
+      p->page_state.push_back(key);
+    }
+    p->page_off.push_back((int32_t)p->page_slot.size());
+  }
+  *out = p;
+  return SC_OK;
+}
+
 // ---------------------------------------------------------------- attention
 
 size_t sc_attention_workspace_bytes(const sc_plan* p, const sc_cache* c) {

@@ -75,6 +75,9 @@ bool policy_selects(const sc_policy* p, int32_t c, int32_t j, int32_t r);
 int32_t policy_level(const sc_policy* p, int32_t c, int32_t j, int32_t r);
 
 // Kernel launchers (device code lives in the .hip files).
+// Whether launch_attention supports the plan's shape (pack and plan sizes,
+// head_dim and page size of the dtype's kernel): SC_OK or SC_EUNSUPPORTED.
+int attention_check(const sc_plan* plan, const sc_cache* cache);
 int launch_attention(const sc_plan* plan, const sc_cache* cache, int32_t layer,
                      const void* q, void* o, float scale, void* ws, size_t ws_bytes,
                      hipStream_t stream);
@@ -93,10 +96,18 @@ int launch_rope_table(const sc_rope_desc* d, void* table, hipStream_t stream);
 // Kernel timer: launchers bracket their kernel with timer_begin/timer_end.
 enum TimerKind {
   TK_ATTENTION = 0, TK_GEMM_QKV, TK_GEMM_OUT, TK_GEMM_UP, TK_GEMM_DOWN, TK_RMSNORM, TK_APPEND,
-  TK_SAMPLER, TK_ATTN_COMBINE, TK_COUNT
+  TK_SAMPLER, TK_ATTN_COMBINE, TK_QK_NORM, TK_CROSS_ATTENTION, TK_GEMM_CROSS_Q,
+  TK_GEMM_CROSS_OUT, TK_GEMM_CONDITION, TK_COUNT
 };
 void timer_begin(int kind, hipStream_t stream);
 void timer_end(int kind, hipStream_t stream);
+// While alive, launches recorded under kind `from` are recorded under `to`
+// (the cross-attention reuses the attention launcher).
+struct TimerAlias {
+  TimerAlias(int from, int to);
+  ~TimerAlias();
+  int from, prev;
+};
 
 // Offsets of the three axis tables inside a RoPE table, in float2 units.
 struct RopeLayout {

@@ -9,7 +9,8 @@ namespace {
 
 const char* const kNames[TK_COUNT] = {"attention", "gemm_qkv", "gemm_out", "gemm_up",
                                       "gemm_down", "rmsnorm", "append", "sampler",
-                                      "attention_combine"};
+                                      "attention_combine", "qk_norm", "cross_attention",
+                                      "gemm_cross_q", "gemm_cross_out", "gemm_condition"};
 
 struct Record {
   int kind;
@@ -25,6 +26,7 @@ struct Timer {
 };
 
 Timer g_timer;
+int g_alias[TK_COUNT] = {};  // 0: no alias, else kind + 1 to record under
 
 hipEvent_t take_event() {
   if (!g_timer.pool.empty()) {
@@ -47,8 +49,14 @@ void recycle_all() {
 
 }  // namespace
 
+TimerAlias::TimerAlias(int from_, int to) : from(from_), prev(g_alias[from_]) { g_alias[from] = to + 1; }
+TimerAlias::~TimerAlias() { g_alias[from] = prev; }
+
+static int aliased(int kind) { return g_alias[kind] ? g_alias[kind] - 1 : kind; }
+
 void timer_begin(int kind, hipStream_t stream) {
   if (!g_timer.on) return;
+  kind = aliased(kind);
   hipEvent_t e = take_event();
   if (!e) return;
   if (hipEventRecord(e, stream) != hipSuccess) {  // an unrecorded launch is not timed
@@ -60,6 +68,7 @@ void timer_begin(int kind, hipStream_t stream) {
 }
 
 void timer_end(int kind, hipStream_t stream) {
+  kind = aliased(kind);
   if (!g_timer.on || g_timer.open_kind != kind || !g_timer.open_start) return;
   hipEvent_t e = take_event();
   if (!e) return;

@@ -31,6 +31,12 @@ TAG_W_O = 11
 TAG_W_UP = 12
 TAG_W_DOWN = 13
 TAG_NOISE = 20
+TAG_CTX = 40       # condition sequence (e.g. text tokens)
+TAG_W_CQ = 41      # cross-attention projections
+TAG_W_CK = 42
+TAG_W_CV = 43
+TAG_W_CO = 44
+TAG_GAIN = 45      # RMSNorm gains (qk-norm)
 
 
 def normal(shape, key, scale: float = 1.0) -> np.ndarray:

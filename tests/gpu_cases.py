@@ -137,3 +137,59 @@ def bf16_gates(got: np.ndarray, want: np.ndarray, what: str):
         rel = np.linalg.norm(got[:, h] - want[:, h]) / np.linalg.norm(want[:, h])
         assert rel <= BF16_REL_FROB, f"{what}: head {h} relative error {rel:.3g}"
     return float(d.max()), float(d.mean())
+
+
+def gains(hidden: int, key) -> np.ndarray:
+    """RMSNorm gains around 1 (fp32 [hidden])."""
+    return (1.0 + normal((hidden,), key, 0.3)).astype(np.float32)
+
+
+class ConditionCase:
+    """A condition cache of n_cond sequences of L tokens (one page each, one
+    layer), filled through sc_condition_append, with the oracle's K_c/V_c
+    (condition_kv on the same bf16 inputs) and the cross-attention weights.
+    Weights are N(0, 1/hidden), so projections of unit-variance inputs have
+    unit variance and the cross logits are O(1)."""
+
+    def __init__(self, geo, L, seed, n_cond=1, q_norm=False, k_norm=False):
+        from oracle.block import BlockShape, condition_kv
+        from synth import TAG_CTX, TAG_GAIN, TAG_W_CK, TAG_W_CO, TAG_W_CQ, TAG_W_CV
+        torch = torch_mod()
+        D = geo.hidden
+        self.geo, self.L, self.n_cond = geo, L, n_cond
+        nbytes = sc.sc_cache_pool_bytes(1, geo.heads, geo.head_dim, L, 1, n_cond)
+        self.pool = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+        self.cache = sc.sc_cache_create(self.pool, 1, geo.heads, geo.head_dim, L, 1, n_cond)
+        self.w_dev, self.w = {}, {}
+        s = 1.0 / math.sqrt(D)
+        for name, tag in (("w_q", TAG_W_CQ), ("w_k", TAG_W_CK), ("w_v", TAG_W_CV), ("w_o", TAG_W_CO)):
+            self.w_dev[name], self.w[name] = to_device(normal((D, D), (seed, tag), s), sc.SC_DTYPE_BF16)
+        self.g_q = gains(D, (seed, TAG_GAIN, 2)) if q_norm else None
+        self.g_k = gains(D, (seed, TAG_GAIN, 3)) if k_norm else None
+        self.g_q_dev = None if self.g_q is None else torch.from_numpy(self.g_q).cuda()
+        g_k_dev = None if self.g_k is None else torch.from_numpy(self.g_k).cuda()
+        shp = BlockShape(D, geo.heads, geo.head_dim, geo.mlp)
+        ws_bytes = sc.sc_condition_workspace_bytes(self.cache)
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+        self.kv, keep = [], []
+        for i in range(n_cond):
+            ctx_dev, ctx = to_device(normal((L, D), (seed, TAG_CTX, i)), sc.SC_DTYPE_BF16)
+            sc.sc_condition_append(self.cache, 0, (i, 0), ctx_dev, self.w_dev["w_k"], self.w_dev["w_v"],
+                                   g_k_dev, ws, ws_bytes)
+            g_k = None if self.g_k is None else self.g_k.astype(np.float64)
+            self.kv.append(condition_kv(ctx, self.w["w_k"], self.w["w_v"], shp, g_k))
+            keep.append(ctx_dev)
+        torch.cuda.synchronize()
+        self.g_k_dev, self.ws, self.ws_bytes = g_k_dev, ws, ws_bytes
+
+    def plan(self, conds, nq):
+        return sc.sc_plan_condition(self.cache, [(c, 0) for c in conds], nq)
+
+    def cross_attn(self, n_nodes, nq, cond=0):
+        self._plan = self.plan([cond] * n_nodes, nq)
+        return sc.CrossAttn(self.w_dev["w_q"], self.w_dev["w_o"], self.cache, self._plan,
+                            q_norm=self.g_q_dev)
+
+    def oracle_dict(self, cond=0):
+        return {"k": self.kv[cond][0], "v": self.kv[cond][1], "w_q": self.w["w_q"],
+                "w_o": self.w["w_o"], "g_q": None if self.g_q is None else self.g_q.astype(np.float64)}

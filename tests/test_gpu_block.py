@@ -106,9 +106,14 @@ def _mod_table(geo, seed):
 
 
 class BlockCase:
-    def __init__(self, geo, kind, pack, resident, seed=0, mod=None):
+    """One block over a pack.  Options: ``mod`` (host fp32 modulation table),
+    ``qk`` (host fp32 qk-norm gains [2][hidden]), ``cross`` (a ConditionCase
+    whose condition 0 every node reads)."""
+
+    def __init__(self, geo, kind, pack, resident, seed=0, mod=None, qk=None, cross=None):
         torch = torch_mod()
         self.mod = mod                                   # host fp32 table or None
+        self.qk, self.cross = qk, cross
         self.geo, self.kind, self.pack = geo, kind, pack
         ppc, tpp = geo.frames_per_chunk, geo.tokens_per_page
         n_slots = (len(resident) + len(pack) + 2) * ppc
@@ -138,9 +143,11 @@ class BlockCase:
         self.x = [xv[i * n:(i + 1) * n] for i in range(len(pack))]
         self.w_dev, self.w = _weights(geo, 0, seed)
         self.mod_dev = None if mod is None else torch.from_numpy(mod).cuda()
+        self.qk_dev = None if qk is None else torch.from_numpy(np.ascontiguousarray(qk)).cuda()
+        ca = None if cross is None else cross.cross_attn(len(pack), geo.tokens_per_chunk)
         self.bw = sc.BlockWeights(geo.hidden, geo.heads, geo.head_dim, geo.mlp, self.w_dev["w_qkv"],
                                   self.w_dev["w_o"], self.w_dev["w_up"], self.w_dev["w_down"],
-                                  mod=self.mod_dev)
+                                  mod=self.mod_dev, qk_norm=self.qk_dev, cross=ca)
         T = len(pack) * n
         self.ws_bytes = sc.sc_block_workspace_bytes(self.bw, T)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device="cuda")
@@ -158,8 +165,10 @@ class BlockCase:
 
     def oracle(self, rows=None):
         sel = select(oracle_policy(self.kind, self.geo.K, self.geo.W), self.pack)
+        qk = None if self.qk is None else tuple(self.qk.astype(np.float64))
+        cross = None if self.cross is None else self.cross.oracle_dict(0)
         return block_forward(sel, lambda i: self.x[i], self.w, self.res_kv.__getitem__, self.shape,
-                             rows=rows, mod=self.mod)
+                             rows=rows, mod=self.mod, qk_norm=qk, cross=cross)
 
 
 def block_gate(got, want, what):

@@ -25,7 +25,7 @@ def test_header_symbols_exported():
     assert declared == set(sc.EXPORTED_SYMBOLS)
     for name in declared:
         assert hasattr(sc.lib, name), name
-    assert sc.sc_abi_version() == sc.ABI_VERSION == 4
+    assert sc.sc_abi_version() == sc.ABI_VERSION == 5
 
 
 def _random_pack(rnd, K, max_chunk=9, max_n=6):
@@ -250,3 +250,75 @@ def test_position_dependent_selection_bit_exact():
     with pytest.raises(sc.ScError) as e:
         sc.sc_selection_build("prog", K, W, [(0, 1)], n_chunks=-1)
     assert e.value.code == sc.SC_EINVAL
+
+
+def test_condition_plan_tables_and_errors():
+    """sc_plan_condition: node i reads every page of its condition state (one
+    state may serve several nodes); unknown states and empty or query-less
+    packs are refused."""
+    cond = sc.sc_cache_create(0x100000, 2, 2, 128, 64, 2, 6)
+    sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(0, 0), (1, 0)]), cond)  # reserve
+    s0, s1 = cond.slots((0, 0)), cond.slots((1, 0))
+    plan = sc.sc_plan_condition(cond, [(1, 0), (0, 0), (1, 0)], 4680)
+    off, slot, tok, frame = plan.tables()
+    assert off == [0, 2, 4, 6] and slot == s1 + s0 + s1
+    assert tok == [64] * 6 and frame == [0, 1] * 3
+    for conds, nq, code in [([(2, 0)], 8, sc.SC_ENOTFOUND), ([], 8, sc.SC_EINVAL),
+                            ([(0, 0)], 0, sc.SC_EINVAL)]:
+        with pytest.raises(sc.ScError) as e:
+            sc.sc_plan_condition(cond, conds, nq)
+        assert e.value.code == code
+    # a condition reserved but never written is refused when read
+    with pytest.raises(sc.ScError) as e:
+        sc.sc_attention(plan, cond, 0, 0x1000, 0x2000, 0.125)
+    assert e.value.code == sc.SC_EUNAVAILABLE
+
+
+def test_condition_append_and_cross_block_checks_without_device():
+    """Argument checks of the condition projection and of the block's
+    cross-attention and qk-norm options, all taken before any launch."""
+    cond = sc.sc_cache_create(0x100000, 1, 2, 128, 64, 1, 1)
+    need = sc.sc_condition_workspace_bytes(cond)
+    L, D = 64, 256
+    assert need == 2 * L * D * 2 + L * (D // 128) * 4
+    args = dict(ctx=0x1000, w_k=0x2000, w_v=0x3000, k_norm=None, ws=0x4000)
+    for layer, ws_bytes, extra, code in [(1, need, {}, sc.SC_EINVAL),         # layer out of range
+                                         (0, need - 1, {}, sc.SC_EINVAL),     # workspace too small
+                                         (0, need, {"k_norm": 0x5004}, sc.SC_EINVAL)]:  # misaligned gain
+        a = dict(args, **extra)
+        with pytest.raises(sc.ScError) as e:
+            sc.sc_condition_append(cond, layer, (0, 0), a["ctx"], a["w_k"], a["w_v"], a["k_norm"],
+                                   a["ws"], ws_bytes)
+        assert e.value.code == code
+    sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(5, 0)]), cond)     # fills the pool
+    with pytest.raises(sc.ScError) as e:
+        sc.sc_condition_append(cond, 0, (0, 0), 0x1000, 0x2000, 0x3000, None, 0x4000, need)
+    assert e.value.code == sc.SC_ECAPACITY
+
+    # block with cross-attention: the condition plan must match the pack
+    cache = sc.sc_cache_create(0x100000, 1, 2, 128, 64, 1, 8)
+    plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(0, 4), (1, 4)]), cache)
+    cond2 = sc.sc_cache_create(0x200000, 1, 2, 128, 64, 1, 2)
+    sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(0, 0)]), cond2)
+    good = sc.sc_plan_condition(cond2, [(0, 0), (0, 0)], 64)
+    wrong_n = sc.sc_plan_condition(cond2, [(0, 0)], 64)
+    wrong_nq = sc.sc_plan_condition(cond2, [(0, 0), (0, 0)], 32)
+    mism = sc.sc_cache_create(0x300000, 1, 4, 128, 64, 1, 2)                  # 4 heads
+    sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(0, 0)]), mism)
+    mism_plan = sc.sc_plan_condition(mism, [(0, 0), (0, 0)], 64)
+    bw0 = sc.BlockWeights(D, 2, 128, 512, 0x1000, 0x2000, 0x3000, 0x4000)
+    ws_bytes = sc.sc_block_workspace_bytes(bw0, 128)
+    cases = [(sc.CrossAttn(0x1000, 0x2000, cond2, wrong_n), None, sc.SC_EINVAL),
+             (sc.CrossAttn(0x1000, 0x2000, cond2, wrong_nq), None, sc.SC_EINVAL),
+             (sc.CrossAttn(0x1000, 0x2000, mism, mism_plan), None, sc.SC_EINVAL),
+             (sc.CrossAttn(0x1000, 0x2000, cond2, good, q_norm=0x5008), None, sc.SC_EINVAL),
+             (sc.CrossAttn(0x1000, 0x2000, cond2, good), None, sc.SC_EUNAVAILABLE),  # not written
+             (None, 0x5004, sc.SC_EINVAL)]                                       # misaligned gains
+    for cross, qk, code in cases:
+        bw = sc.BlockWeights(D, 2, 128, 512, 0x1000, 0x2000, 0x3000, 0x4000, qk_norm=qk,
+                             cross=cross)
+        assert sc.sc_block_workspace_bytes(bw, 128) == ws_bytes
+        with pytest.raises(sc.ScError) as e:
+            sc.sc_block_forward(bw, cache, 0, plan, 0x6000, None, 0x7000, ws_bytes)
+        assert e.value.code == code, (cross, qk)
+    assert not cache.contains((0, 4), 0)                  # nothing was written
