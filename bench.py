@@ -16,6 +16,11 @@ weights), all resident in HBM before timing.
 
 Prints one JSON line.  ``value`` is latent frames/s per DiT block:
 3 latent frames per chunk, K + 1 = 5 node forwards per chunk.
+
+``full_block`` in the same line times the fuller Wan block form on the same
+pack: per-level modulation (adaLN table), qk-norm, and cross-attention to a
+512-token condition whose K/V were projected and cached once beforehand
+(they depend on the condition only, not on the step).
 """
 from __future__ import annotations
 
@@ -37,8 +42,8 @@ METRIC = "steady-state latent frames/s per DiT block + attention TFLOP/s (% bf16
 # FETCH_SIZE and WRITE_SIZE per dispatch, scaled by what the same counters
 # read for a plain 256 MiB copy (x2.0 fetch, x1.0 write).  Valid only for the
 # kernel sources it was measured on (hash below); otherwise reported as null.
-ATTN_TRAFFIC = {"sources_sha1": "f53c5ba5162a62d88eb241221bf10993b5421874",
-                "fetch_bytes": 1.3617e+09, "write_bytes": 2.0873e+08}
+ATTN_TRAFFIC = {"sources_sha1": "8d679dc6a3538a5a340e1a85f7db33f69b3efc81",
+                "fetch_bytes": 1.3626e+09, "write_bytes": 2.0873e+08}
 
 
 def attn_traffic():
@@ -62,16 +67,22 @@ def workload(name):
             "cfg2": cfg2_clean(4)}[name]
 
 
-class Setup:
-    """Device-resident inputs of one packed block step."""
+COND_TOKENS = 512    # condition (text) tokens of the full block form
+FULL_FORM = f"level modulation, qk-norm, cross-attention to {COND_TOKENS} condition tokens"
 
-    def __init__(self, wl, seed=0):
+
+class Setup:
+    """Device-resident inputs of one packed block step; ``full`` adds the
+    modulation table, qk-norm gains and a cached 512-token condition."""
+
+    def __init__(self, wl, seed=0, full=False):
         import numpy as np
         import torch
 
         import paper_2609_22283_amd as sc
-        from synth import (TAG_K, TAG_NOISE, TAG_V, TAG_W_DOWN, TAG_W_O, TAG_W_QKV, TAG_W_UP, TAG_X,
-                           bf16_bits, normal_parallel)
+        from synth import (TAG_CTX, TAG_GAIN, TAG_K, TAG_NOISE, TAG_V, TAG_W_CK, TAG_W_CO, TAG_W_CQ,
+                           TAG_W_CV, TAG_W_DOWN, TAG_W_O, TAG_W_QKV, TAG_W_UP, TAG_X, bf16_bits,
+                           normal, normal_parallel)
         from synth.configs import WAN as g
 
         self.sc, self.torch, self.g, self.wl = sc, torch, g, wl
@@ -98,20 +109,55 @@ class Setup:
         self.w = [dev(normal_parallel(s, (seed, tag, 0), 0.02)) for s, tag in
                   [((3 * D, D), TAG_W_QKV), ((D, D), TAG_W_O), ((M, D), TAG_W_UP), ((D, M), TAG_W_DOWN)]]
         self.bw = sc.BlockWeights(D, g.heads, g.head_dim, M, *self.w)
+        self.full = full
+        if full:
+            def f32(x):
+                return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda()
+            mod = np.stack([np.stack([normal((D,), (seed, 30, j, r), 0.2) for r in range(6)])
+                            for j in range(g.K + 1)])
+            mod[:, 2] += 1.0
+            mod[:, 5] += 1.0
+            self.mod = f32(mod)
+            self.qk = f32(1.0 + np.stack([normal((D,), (seed, TAG_GAIN, s), 0.3) for s in range(4)]))
+            self.wc = {k: dev(normal_parallel((D, D), (seed, tag), 0.02)) for k, tag in
+                       [("w_q", TAG_W_CQ), ("w_k", TAG_W_CK), ("w_v", TAG_W_CV), ("w_o", TAG_W_CO)]}
+            L = COND_TOKENS
+            cb = sc.sc_cache_pool_bytes(1, g.heads, g.head_dim, L, 1, 1)
+            self.cond_pool = torch.empty(cb, dtype=torch.uint8, device="cuda")
+            self.cond = sc.sc_cache_create(self.cond_pool, 1, g.heads, g.head_dim, L, 1, 1)
+            cws = sc.sc_condition_workspace_bytes(self.cond)
+            ws = torch.empty(cws, dtype=torch.uint8, device="cuda")
+            ctx = dev(normal_parallel((L, D), (seed, TAG_CTX, 0)))
+            sc.sc_condition_append(self.cond, 0, (0, 0), ctx, self.wc["w_k"], self.wc["w_v"],
+                                   self.qk[3], ws, cws)
+            torch.cuda.synchronize()
+            del ws, ctx
         T = len(wl.pack) * n
         self.x = dev(np.concatenate([normal_parallel((n, D), (seed, TAG_X) + st) for st in wl.pack]))
         self.noise = dev(np.concatenate([normal_parallel((n, D), (seed, TAG_NOISE) + st)
                                          for st in wl.pack]))
-        self.ws_bytes = sc.sc_block_workspace_bytes(self.bw, T)
+        self.ws_bytes = sc.sc_block_workspace_bytes(self.block_weights(len(wl.pack)), T)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device="cuda")
         self.t_sched = (0.0, 5.0 / 8.0, 5.0 / 6.0, 15.0 / 16.0, 1.0)
         torch.cuda.synchronize()
+
+    def block_weights(self, n_nodes):
+        """The block's weights for a pack of n_nodes (the full form also plans
+        the pack's reads of the condition)."""
+        if not self.full:
+            return self.bw
+        sc, g = self.sc, self.g
+        plan_c = sc.sc_plan_condition(self.cond, [(0, 0)] * n_nodes, g.tokens_per_chunk)
+        cross = sc.CrossAttn(self.wc["w_q"], self.wc["w_o"], self.cond, plan_c, q_norm=self.qk[2])
+        return sc.BlockWeights(g.hidden, g.heads, g.head_dim, g.mlp, *self.w, mod=self.mod,
+                               qk_norm=self.qk[0:2], cross=cross)
 
     def packed_step(self):
         sc, g, wl = self.sc, self.g, self.wl
         sel = sc.sc_selection_build(wl.policy, g.K, g.W, wl.pack)
         plan = sc.sc_plan_build(sel, self.cache)
-        sc.sc_block_forward(self.bw, self.cache, 0, plan, self.x, self.rope, self.ws, self.ws_bytes)
+        sc.sc_block_forward(self.block_weights(len(wl.pack)), self.cache, 0, plan, self.x, self.rope,
+                            self.ws, self.ws_bytes)
         sc.sc_sampler_step(wl.pack, self.t_sched, g.K, self.x, self.x, self.noise,
                            self.n * g.hidden)
         for st in wl.pack:
@@ -128,7 +174,8 @@ class Setup:
             sel = sc.sc_selection_build(wl.policy, g.K, g.W, [node])
             plan = sc.sc_plan_build(sel, self.cache)
             xi = self.x[i * self.n:(i + 1) * self.n]
-            sc.sc_block_forward(self.bw, self.cache, 0, plan, xi, self.rope, self.ws, self.ws_bytes)
+            sc.sc_block_forward(self.block_weights(1), self.cache, 0, plan, xi, self.rope, self.ws,
+                                self.ws_bytes)
             sc.sc_sampler_step([node], self.t_sched, g.K, xi, xi,
                                self.noise[i * self.n:(i + 1) * self.n], self.n * D)
         for st in wl.pack:
@@ -155,7 +202,8 @@ def time_steps(setup, fn, steps, warmup, timer=False):
     kernels = {}
     if timer:
         for kind in ("attention", "attention_combine", "gemm_qkv", "gemm_out", "gemm_up",
-                     "gemm_down", "rmsnorm", "sampler"):
+                     "gemm_down", "rmsnorm", "sampler", "qk_norm", "cross_attention",
+                     "gemm_cross_q", "gemm_cross_out"):
             n, tot = sc.sc_timer_read(kind)
             if n:
                 kernels[kind] = (n, tot / n)
@@ -443,6 +491,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sequential", action="store_true")
     ap.add_argument("--no-probe", action="store_true", help="skip the matrix-core ceiling probe")
+    ap.add_argument("--form", default="plain", choices=["plain", "full"],
+                    help="block form of the main measurement: plain (RMSNorm, RoPE, attention, "
+                         "MLP) or full (plus level modulation, qk-norm, cross-attention)")
+    ap.add_argument("--no-full-block", action="store_true",
+                    help="with --form plain: skip the extra timing of the full block form")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only copy a 256 MiB device buffer 4 times (calibrates the HBM byte "
                          "counters of a profiler run) and exit")
@@ -511,7 +564,7 @@ def main():
         return
     wl = workload(args.workload)
     log(f"[bench] workload {wl.name}: pack {wl.pack}, resident {len(wl.resident)} states")
-    setup = Setup(wl)
+    setup = Setup(wl, full=args.form == "full")
     g = setup.g
     ms, wall_ms, kernels = time_steps(setup, setup.packed_step, args.steps, args.warmup, timer=True)
     log(f"[bench] packed: {ms:.3f} ms/step (host wall {wall_ms:.3f})")
@@ -547,6 +600,7 @@ def main():
                    "keys_per_node": [s * g.tokens_per_chunk for s in segment_counts(wl, g)],
                    "hidden": g.hidden, "heads": g.heads,
                    "head_dim": g.head_dim, "mlp": g.mlp, "page_tokens": g.tokens_per_page,
+                   "block_form": FULL_FORM if args.form == "full" else "plain",
                    "parallelism": "single GPU"},
         "attention_tflops": round(attn_tflops, 1),
         "attention_pct_peak": round(100.0 * attn_tflops / PEAK_BF16_TFLOPS, 2),
@@ -562,6 +616,25 @@ def main():
                      "kernel": "attn_bf16_kernel",
                      "algorithmic_per_launch": f"{a_flops:.4e} FLOP"},
     }
+    if args.form == "plain" and not args.no_full_block:
+        del setup
+        full = Setup(wl, full=True)
+        fms, _, fk = time_steps(full, full.packed_step, args.steps, args.warmup, timer=True)
+        log(f"[bench] full block form: {fms:.3f} ms/step")
+        fseq = None
+        if not args.no_sequential:
+            fseq, _, _ = time_steps(full, full.sequential_step, max(3, args.steps // 2), 1)
+            log(f"[bench] full block form, sequential: {fseq:.3f} ms/step")
+        del full
+        result["full_block"] = {
+            "form": FULL_FORM,
+            "ms_per_step": round(fms, 4),
+            "value": round(3.0 * n_nodes / (fms * 1e-3) / (g.K + 1), 3),
+            "unit": "latent frames/s per DiT block",
+            "sequential_ms_per_step": round(fseq, 4) if fseq else None,
+            "packed_vs_sequential": round(fseq / fms, 3) if fseq else None,
+            "kernel_avg_ms": {k: round(v[1], 4) for k, v in fk.items()},
+        }
     if not args.no_probe:
         ceil = mfma_ceiling()
         log(f"[bench] matrix-core probe: {ceil} TFLOP/s")
