@@ -42,8 +42,8 @@ METRIC = "steady-state latent frames/s per DiT block + attention TFLOP/s (% bf16
 # FETCH_SIZE and WRITE_SIZE per dispatch, scaled by what the same counters
 # read for a plain 256 MiB copy (x2.0 fetch, x1.0 write).  Valid only for the
 # kernel sources it was measured on (hash below); otherwise reported as null.
-ATTN_TRAFFIC = {"sources_sha1": "8d679dc6a3538a5a340e1a85f7db33f69b3efc81",
-                "fetch_bytes": 1.3626e+09, "write_bytes": 2.0873e+08}
+ATTN_TRAFFIC = {"sources_sha1": "d8fa52bde07910861a869cca1434f65f163a1748",
+                "fetch_bytes": 1.3902e+09, "write_bytes": 2.4717e+08}
 
 
 def attn_traffic():

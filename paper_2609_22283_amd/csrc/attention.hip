@@ -111,6 +111,10 @@ constexpr int BQ_SMALL = 128, BQ_MAX = 256;  // queries per work-group of the tw
 // reaches the guard (logits more than 64 log2 units above the first tile's
 // maximum) redoes its item exactly in two passes (attn_exact).  Rescaling in
 // place would keep the accumulators and the recomputation live in the loop.
+// The row sums come from the matrix cores: one more 16-row block of V^T whose
+// first row is all ones turns O^T += V^T P^T into l += sum_k p as well, so
+// the sum sees the same bf16 p as the numerator.  Since p >= 0 the final sum
+// bounds every partial one, and the guard is checked once, on it.
 constexpr float P_GUARD = 18446744073709551616.0f;  // 2^64
 
 // Matrix-core shape: v_mfma_f32_16x16x32_bf16.  Lane l (g = l / 16,
@@ -179,6 +183,16 @@ __device__ __forceinline__ float group_max(float x) {
   return fmaxf(x, __shfl_xor(x, 32));
 }
 
+// A operand of the row-sum MFMA: row 0 all ones, rows 1..15 zero (lane c
+// supplies row c).  D[0][query] = sum over the 32 keys of p.
+__device__ __forceinline__ bf16x8 ones_row(int32_t c) {
+  bf16x8 a;
+  const __bf16 v = static_cast<__bf16>(c == 0 ? 1.0f : 0.0f);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) a[e] = v;
+  return a;
+}
+
 // Column maxima of a tile, per query block.
 __device__ __forceinline__ void tile_max(const STile& s, float (&mx)[2]) {
 #pragma unroll
@@ -208,7 +222,19 @@ __device__ __forceinline__ void mask_tile(STile& s, int32_t t0, int32_t nk, int3
 }
 
 // p = exp2(s) rounded to bf16: pb[h][qb] is the B operand of the PV MFMA for
-// the 32-key half h; returns this lane's sums of the rounded values per block.
+// the 32-key half h.
+__device__ __forceinline__ void probs(const STile& s, bf16x8 (&pb)[2][2]) {
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        pb[h][qb][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(s[h][e >> 2][qb][e & 3]));
+}
+
+// The same, also returning this lane's sums of the rounded values per block
+// (the exact redo path).
 __device__ __forceinline__ void probs_tile(const STile& s, bf16x8 (&pb)[2][2], float (&lt)[2]) {
   const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 #pragma unroll
@@ -476,23 +502,25 @@ __device__ __forceinline__ void pv_tile(const char* vl, const AttnLane& L, const
 
 // One step of the software-pipelined loop, for tile t: probabilities of
 // S(t) (held in s), the next tile's S(t+1) = K(t+1) Q^T - m on the matrix
-// cores while the exponentials of tile t run on the vector ALUs, the guard
-// check, then O^T += V(t)^T P(t).  K runs one tile ahead of V: K(t+1) sits
-// in K buffer KN, V(t) in V buffer VC.
+// cores while the exponentials of tile t run on the vector ALUs, then
+// O^T += V(t)^T P(t) and the row sums lsum += 1^T P(t).  K runs one tile
+// ahead of V: K(t+1) sits in K buffer KN, V(t) in V buffer VC.
 template <int KN, int VC, bool NEXT, bool MASK>
 __device__ __forceinline__ void attn_step(const char* smem, const AttnLane& L, const bf16x8 (&qreg)[2][4],
                                           f32x4 (&oacc)[2][8], STile& s, const float (&m)[2],
-                                          float (&l)[2], bool& bad, int32_t t0, int32_t nk, int32_t lg) {
+                                          f32x4 (&lsum)[2], const bf16x8& ones, int32_t t0, int32_t nk,
+                                          int32_t lg) {
   if constexpr (MASK) mask_tile(s, t0, nk, lg);
   bf16x8 pb[2][2];
-  float lt[2];
-  probs_tile(s, pb, lt);
+  probs(s, pb);
   STile sn;
   if constexpr (NEXT) qk_tile(smem + KN * KT_BYTES, L, qreg, sn, m);
-  bad |= __builtin_amdgcn_ballot_w64(!(lt[0] < P_GUARD && lt[1] < P_GUARD)) != 0;  // also NaN / inf
-  l[0] += lt[0];
-  l[1] += lt[1];
   pv_tile(smem + 2 * KT_BYTES + VC * VT_BYTES, L, pb, oacc);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    lsum[0] = mfma16(ones, pb[h][0], lsum[0]);
+    lsum[1] = mfma16(ones, pb[h][1], lsum[1]);
+  }
   if constexpr (NEXT) {
 #pragma unroll
     for (int h = 0; h < 2; ++h)
@@ -564,7 +592,6 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
   // K buffers 0, 1 then V^T buffers 0, 1 (16 KB each)
   __shared__ __attribute__((aligned(1024))) char smem[SMEM_BYTES];
   __shared__ int32_t any_bad;
-  bool bad = false;
   const AttnItem it = decode_item(plan, g, blockIdx.x);
   if (it.ta == it.tb) return;  // empty piece of a unit shorter than the split
   const int32_t ta = it.ta, ntiles = it.tb;  // this item's key tiles: [ta, ntiles)
@@ -586,7 +613,9 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
   for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
     for (int db = 0; db < 8; ++db) oacc[qb][db] = f32x4{};
-  float m[2] = {0.f, 0.f}, l[2] = {0.f, 0.f};
+  float m[2] = {0.f, 0.f}, l[2];
+  f32x4 lsum[2] = {f32x4{}, f32x4{}};  // value 0 of lanes 0..15: row sums of the two blocks
+  const bf16x8 ones = ones_row(c);
   // prologue: K(ta), V(ta), K(ta+1) in flight; S(ta) = K(ta) Q^T; m = its exact column maxima
   {
     const typename KvTiles<NW>::Slots s0 = kv.slots(ta * BK);
@@ -619,30 +648,34 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
     kv.copy_v((t + 1) * BK, smem + 2 * KT_BYTES + VT_BYTES, sv);
     sk = kv.slots(min(t + 3, it.ntiles - 1) * BK);
     sv = kv.slots(min(t + 2, it.ntiles - 1) * BK);
-    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m, l, bad, t * BK, nk, lg);
+    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
     landed();
     if (t + 3 < ntiles) kv.copy_k((t + 3) * BK, smem + KT_BYTES, sk);
     kv.copy_v((t + 2) * BK, smem + 2 * KT_BYTES, sv);
     sk = kv.slots(min(t + 4, it.ntiles - 1) * BK);
     sv = kv.slots(min(t + 3, it.ntiles - 1) * BK);
-    attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m, l, bad, (t + 1) * BK, nk, lg);
+    attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, (t + 1) * BK, nk, lg);
     landed();
   }
   if (t + 1 < ntiles) {  // two tiles left, parity 0
     kv.copy_v((t + 1) * BK, smem + 2 * KT_BYTES + VT_BYTES, sv);
-    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m, l, bad, t * BK, nk, lg);
+    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
     landed();
     ++t;
     if (ragged)
-      attn_step<0, 1, false, true>(smem, L, qreg, oacc, s, m, l, bad, t * BK, nk, lg);
+      attn_step<0, 1, false, true>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
     else
-      attn_step<0, 1, false, false>(smem, L, qreg, oacc, s, m, l, bad, t * BK, nk, lg);
+      attn_step<0, 1, false, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
   } else {               // one tile left, parity 0 (masking twice is harmless)
     if (ragged)
-      attn_step<1, 0, false, true>(smem, L, qreg, oacc, s, m, l, bad, t * BK, nk, lg);
+      attn_step<1, 0, false, true>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
     else
-      attn_step<1, 0, false, false>(smem, L, qreg, oacc, s, m, l, bad, t * BK, nk, lg);
+      attn_step<1, 0, false, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
   }
+  // the guard, on the final sums (also NaN / inf)
+  const bool bad = __builtin_amdgcn_ballot_w64(!(lsum[0][0] < P_GUARD && lsum[1][0] < P_GUARD)) != 0;
+  l[0] = lsum[0][0];  // zero outside lanes 0..15, so the group sum is the row sum
+  l[1] = lsum[1][0];
   if (bad && lane == 0) atomicOr(&any_bad, 1);
   __syncthreads();  // every wave is done with the ring; any_bad is final
   if (any_bad) attn_exact(smem, kv, L, qreg, oacc, m, l, ta, ntiles, lg);
