@@ -308,20 +308,27 @@ def cpu_baseline(wl, seed=0, row_stride=16):
                        f"x{n / len(rows):.2f}; estimated {est:.1f} s per step")}
 
 
-def stack_weights(n_layers, seed=0):
-    """bf16 device weights of an n-layer Wan-shaped stack (N(0, 0.02))."""
+def stack_weights(n_layers, seed=0, full=False):
+    """bf16 device weights of an n-layer Wan-shaped stack (N(0, 0.02)).  With
+    ``full``: per-layer modulation tables, qk-norm gains and cross-attention
+    weights, and a condition cache holding a 512-token condition's K/V for
+    every layer; returns (layers, keep, condition dict or None)."""
     import concurrent.futures as cf
 
     import numpy as np
     import torch
 
     import paper_2609_22283_amd as sc
-    from synth import TAG_W_DOWN, TAG_W_O, TAG_W_QKV, TAG_W_UP, bf16_bits, normal
+    from synth import (TAG_CTX, TAG_GAIN, TAG_W_CK, TAG_W_CO, TAG_W_CQ, TAG_W_CV, TAG_W_DOWN, TAG_W_O,
+                       TAG_W_QKV, TAG_W_UP, bf16_bits, normal)
     from synth.configs import WAN as g
 
     D, M = g.hidden, g.mlp
     shapes = [("w_qkv", (3 * D, D), TAG_W_QKV), ("w_o", (D, D), TAG_W_O),
               ("w_up", (M, D), TAG_W_UP), ("w_down", (D, M), TAG_W_DOWN)]
+    if full:
+        shapes += [("w_cq", (D, D), TAG_W_CQ), ("w_ck", (D, D), TAG_W_CK), ("w_cv", (D, D), TAG_W_CV),
+                   ("w_co", (D, D), TAG_W_CO)]
     jobs = [(l, name, shp, tag) for l in range(n_layers) for name, shp, tag in shapes]
 
     def make(job):
@@ -332,9 +339,35 @@ def stack_weights(n_layers, seed=0):
     with cf.ThreadPoolExecutor(min(16, len(os.sched_getaffinity(0)))) as ex:
         for (l, name, _, _), bits in ex.map(make, jobs):
             dev[(l, name)] = torch.from_numpy(bits.view(np.int16)).cuda().view(torch.bfloat16)
-    layers = [sc.BlockWeights(D, g.heads, g.head_dim, M, dev[(l, "w_qkv")], dev[(l, "w_o")],
-                              dev[(l, "w_up")], dev[(l, "w_down")]) for l in range(n_layers)]
-    return layers, dev
+    if not full:
+        layers = [sc.BlockWeights(D, g.heads, g.head_dim, M, dev[(l, "w_qkv")], dev[(l, "w_o")],
+                                  dev[(l, "w_up")], dev[(l, "w_down")]) for l in range(n_layers)]
+        return layers, dev, None
+
+    def f32(x):
+        return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda()
+    layers, cross = [], []
+    L = COND_TOKENS
+    cb = sc.sc_cache_pool_bytes(n_layers, g.heads, g.head_dim, L, 1, 1)
+    dev["cond_pool"] = torch.empty(cb, dtype=torch.uint8, device="cuda")
+    cond = sc.sc_cache_create(dev["cond_pool"], n_layers, g.heads, g.head_dim, L, 1, 1)
+    cws = sc.sc_condition_workspace_bytes(cond)
+    ws = torch.empty(cws, dtype=torch.uint8, device="cuda")
+    ctx = torch.from_numpy(bf16_bits(normal((L, D), (seed, TAG_CTX, 0))).view(np.int16)).cuda().view(torch.bfloat16)
+    for l in range(n_layers):
+        mod = np.stack([np.stack([normal((D,), (seed, 30, l, j, r), 0.2) for r in range(6)])
+                        for j in range(g.K + 1)])
+        mod[:, 2] += 1.0
+        mod[:, 5] += 1.0
+        gains = f32(1.0 + np.stack([normal((D,), (seed, TAG_GAIN, l, k), 0.3) for k in range(4)]))
+        dev[(l, "mod")], dev[(l, "gains")] = f32(mod), gains
+        layers.append(sc.BlockWeights(D, g.heads, g.head_dim, M, dev[(l, "w_qkv")], dev[(l, "w_o")],
+                                      dev[(l, "w_up")], dev[(l, "w_down")], mod=dev[(l, "mod")],
+                                      qk_norm=gains[0:2]))
+        cross.append((dev[(l, "w_cq")], dev[(l, "w_co")], gains[2]))
+        sc.sc_condition_append(cond, l, (0, 0), ctx, dev[(l, "w_ck")], dev[(l, "w_cv")], gains[3], ws, cws)
+    torch.cuda.synchronize()
+    return layers, dev, {"cache": cond, "cross": cross}
 
 
 def bench_kv_stream(args):
@@ -427,7 +460,7 @@ def bench_stack(args):
     L, B, K, W = args.layers, args.chunks, g.K, g.W
     n, D = g.tokens_per_chunk, g.hidden
     t0 = time.perf_counter()
-    layers, keep = stack_weights(L)
+    layers, keep, condition = stack_weights(L, full=args.form == "full")
     noise = torch.empty((B, K + 2, n, D), dtype=torch.bfloat16, device="cuda")
     import concurrent.futures as cf
 
@@ -454,7 +487,7 @@ def bench_stack(args):
         xs = noise[:, K + 1].clone()
         return StackPipeline(layers=layers, cache=cache, rope=rope, xs=xs, noise=noise,
                              policy=policy, K=K, W=W, B=B, t_sched=(0.0, 5 / 8, 5 / 6, 15 / 16, 1.0),
-                             refresh=True)
+                             refresh=True, condition=condition)
 
     steady = [r for r in range(K + B) if r - K >= W and r < B]      # full pack, full window
     res = {}
@@ -544,7 +577,9 @@ def main():
             "data": "synthetic (seeded noise, N(0,0.02) weights)",
             "config": {"workload": f"cfg5: {args.layers}-block Wan-shaped stack, progressive "
                                    f"pipeline, {args.chunks} chunks x 3 latent frames, K=4, W=6, refresh",
-                       "layers": args.layers, "chunks": args.chunks, "parallelism": "single GPU"},
+                       "layers": args.layers, "chunks": args.chunks,
+                       "block_form": FULL_FORM if args.form == "full" else "plain",
+                       "parallelism": "single GPU"},
             "stack_latent_frames_per_s": round(3.0 / (r["packed"] * 1e-3), 3),
             "sequential_ms_per_round": round(r["sequential"], 3),
             "same_level_packed_ms_per_round": round(r["same_packed"], 3),

@@ -67,7 +67,8 @@ def sampler_step(y: np.ndarray, xi: np.ndarray, t_prev: float) -> np.ndarray:
 
 def run_stack(packs: List[List[Tuple[int, int]]], pol: Policy, n_layers: int,
               weights_of: Callable[[int], Dict[str, np.ndarray]], noise_of: Callable[[int, int], np.ndarray],
-              shp, t_sched=T_SCHEDULE_K4, release: bool = True, n_slots: int = 4096):
+              shp, t_sched=T_SCHEDULE_K4, release: bool = True, n_slots: int = 4096,
+              options_of: Callable[[int], Dict] = None):
     """Run the packs in order through an ``n_layers`` block stack.
 
     Each pack is one forward: every node reads its selected states through
@@ -76,6 +77,8 @@ def run_stack(packs: List[List[Tuple[int, int]]], pol: Policy, n_layers: int,
     Under ``release`` the states that no later pack reads are dropped after
     each pack: levels >= 1 of the pack, and clean chunks older than the next
     pack's window (prog policy; other policies keep everything).
+    ``options_of(layer)`` gives that layer's optional block_forward keywords
+    (mod, qk_norm, cross).
     """
     K = pol.K
     x_state: Dict[Tuple[int, int], np.ndarray] = {}
@@ -93,7 +96,8 @@ def run_stack(packs: List[List[Tuple[int, int]]], pol: Policy, n_layers: int,
             xs.append(x_state[(c, j)])
         for layer in range(n_layers):
             y, new_kv = block_forward(sel, lambda i: xs[i], weights_of(layer),
-                                      lambda st, l=layer: kv[(st, l)], shp)
+                                      lambda st, l=layer: kv[(st, l)], shp,
+                                      **(options_of(layer) if options_of else {}))
             for i, node in enumerate(pack):
                 kv[(node, layer)] = new_kv[i]
                 cache.append(layer, node)

@@ -427,8 +427,16 @@ class BlockWeights:
         self.tensors = (w_qkv, w_o, w_up, w_down, mod, qk_norm, cross)
         levels = 0 if mod is None else int(mod.shape[0])
         cp = C.pointer(cross.struct) if cross is not None else None
+        self.args = (hidden, n_heads, head_dim, mlp, w_qkv, w_o, w_up, w_down, mod, qk_norm)
         self.struct = sc_block_weights(hidden, n_heads, head_dim, mlp, _ptr(w_qkv), _ptr(w_o),
                                        _ptr(w_up), _ptr(w_down), _ptr(mod), levels, _ptr(qk_norm), cp)
+
+    def with_cross(self, cross: Optional[CrossAttn]) -> "BlockWeights":
+        """The same block reading the condition through ``cross`` (a plan
+        per pack: the condition plan names the pack's nodes)."""
+        hidden, n_heads, head_dim, mlp, w_qkv, w_o, w_up, w_down, mod, qk_norm = self.args
+        return BlockWeights(hidden, n_heads, head_dim, mlp, w_qkv, w_o, w_up, w_down, mod=mod,
+                            qk_norm=qk_norm, cross=cross)
 
 
 def sc_block_workspace_bytes(w: BlockWeights, n_tokens: int) -> int:

@@ -12,6 +12,11 @@ After every round the states no later node reads are released
   sequential  the same rounds, one forward per node, oldest chunk first
   serial      Eq. 2 order, one forward per node, chunk by chunk
 
+With ``condition`` set, every block also cross-attends to a cached
+condition sequence (the condition c of Eq. 1): per forward, a condition plan
+maps each pack node to the condition its chunk reads (``condition_of``), and
+each layer's weights are bound to that plan.
+
 Every computation runs in the library; this module sequences calls and moves
 device buffers.
 """
@@ -25,13 +30,18 @@ from . import binding as sc
 class StackPipeline:
     def __init__(self, *, layers: Sequence["sc.BlockWeights"], cache: "sc.Cache", rope: "sc.Rope",
                  xs, noise, policy: str, K: int, W: int, B: int, t_sched: Sequence[float],
-                 refresh: bool = True, stream=None):
+                 refresh: bool = True, stream=None, condition=None):
+        """``condition``: optional dict with ``cache`` (an sc.Cache holding the
+        condition K/V of every layer), ``cross`` (per layer: (w_q, w_o,
+        q_norm or None)) and ``condition_of`` (chunk -> cached condition
+        state; default (0, 0))."""
         import torch
         self.torch = torch
         self.layers, self.cache, self.rope = list(layers), cache, rope
         self.xs, self.noise = xs, noise            # [B, n, hidden], [B, K + 2, n, hidden]
         self.policy, self.K, self.W, self.B = policy, K, W, B
         self.t_sched, self.refresh, self.stream = tuple(t_sched), refresh, stream
+        self.condition = condition
         self.n_tok, self.hidden = xs.shape[1], xs.shape[2]
         max_pack = K + 1
         self.stage = torch.empty((max_pack * self.n_tok, self.hidden), dtype=xs.dtype, device=xs.device)
@@ -56,7 +66,14 @@ class StackPipeline:
         for i, (c, _) in enumerate(nodes):
             self.stage[i * n:(i + 1) * n].copy_(self.xs[c])
         x = self.stage[:len(nodes) * n]
-        sc.sc_stack_forward(self.layers, self.cache, plan, x, self.rope, self.ws, self.ws_bytes,
+        layers = self.layers
+        if self.condition is not None:
+            cond = self.condition
+            of = cond.get("condition_of") or (lambda c: (0, 0))
+            plan_c = sc.sc_plan_condition(cond["cache"], [of(c) for c, _ in nodes], n)
+            layers = [w.with_cross(sc.CrossAttn(wq, wo, cond["cache"], plan_c, q_norm=qn))
+                      for w, (wq, wo, qn) in zip(self.layers, cond["cross"])]
+        sc.sc_stack_forward(layers, self.cache, plan, x, self.rope, self.ws, self.ws_bytes,
                             self.stream)
         for i, (c, j) in enumerate(nodes):
             if j >= 1:
@@ -98,7 +115,7 @@ class StackPipeline:
                 times.append((e0, e1))
             if kernel_timer_rounds and g == kernel_timer_rounds[1]:
                 for kind in ("attention", "attention_combine", "gemm_qkv", "gemm_out", "gemm_up",
-                             "gemm_down"):
+                             "gemm_down", "qk_norm", "cross_attention", "gemm_cross_q", "gemm_cross_out"):
                     self.kernel_times[kind] = sc.sc_timer_read(kind)
                 sc.sc_timer_enable(False)
         if time_rounds:

@@ -30,12 +30,57 @@ pytestmark = pytest.mark.gpu
 T_SCHED = (0.0, 5.0 / 8.0, 5.0 / 6.0, 15.0 / 16.0, 1.0)
 
 
-def _setup(geo, L, B, W, kind, seed, n_slots):
+def _full_form(geo, L, seed, n_cond_tokens=64):
+    """Per-layer modulation tables, qk-norm gains and cross-attention to one
+    cached condition (device side and the oracle's block options)."""
+    from oracle.block import condition_kv
+    from synth import TAG_CTX, TAG_GAIN, TAG_W_CK, TAG_W_CO, TAG_W_CQ, TAG_W_CV
+    from gpu_cases import gains
+    torch = torch_mod()
+    D = geo.hidden
+    shp = BlockShape(D, geo.heads, geo.head_dim, geo.mlp)
+    nb = sc.sc_cache_pool_bytes(L, geo.heads, geo.head_dim, n_cond_tokens, 1, 1)
+    pool = torch.zeros(nb, dtype=torch.uint8, device="cuda")
+    cond = sc.sc_cache_create(pool, L, geo.heads, geo.head_dim, n_cond_tokens, 1, 1)
+    ws_bytes = sc.sc_condition_workspace_bytes(cond)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    ctx_dev, ctx = to_device(normal((n_cond_tokens, D), (seed, TAG_CTX, 0)), sc.SC_DTYPE_BF16)
+    s = 1.0 / np.sqrt(D)
+    mods, qks, cross, opts, keep = [], [], [], [], [pool, ws, ctx_dev]
+    for l in range(L):
+        w = {}
+        for name, tag in (("w_q", TAG_W_CQ), ("w_k", TAG_W_CK), ("w_v", TAG_W_CV), ("w_o", TAG_W_CO)):
+            w[name] = to_device(normal((D, D), (seed, tag, l), s), sc.SC_DTYPE_BF16)
+        g = [gains(D, (seed, TAG_GAIN, l, k)) for k in range(4)]
+        gd = torch.from_numpy(np.stack(g)).cuda()
+        mod = np.stack([np.stack([normal((D,), (seed, 30, l, j, r), 0.2) for r in range(6)])
+                        for j in range(geo.K + 1)]).astype(np.float32)
+        mod[:, 2] += 1.0
+        mod[:, 5] += 1.0
+        md = torch.from_numpy(mod).cuda()
+        sc.sc_condition_append(cond, l, (0, 0), ctx_dev, w["w_k"][0], w["w_v"][0], gd[3], ws, ws_bytes)
+        k, v = condition_kv(ctx, w["w_k"][1], w["w_v"][1], shp, g[3].astype(np.float64))
+        mods.append(md)
+        qks.append(gd[0:2])
+        cross.append((w["w_q"][0], w["w_o"][0], gd[2]))
+        opts.append({"mod": mod, "qk_norm": (g[0].astype(np.float64), g[1].astype(np.float64)),
+                     "cross": {"k": k, "v": v, "w_q": w["w_q"][1], "w_o": w["w_o"][1],
+                               "g_q": g[2].astype(np.float64)}})
+        keep += [w, gd, md]
+    torch.cuda.synchronize()
+    return mods, qks, {"cache": cond, "cross": cross}, opts, keep
+
+
+def _setup(geo, L, B, W, kind, seed, n_slots, full=False):
     torch = torch_mod()
     n, D, M = geo.tokens_per_chunk, geo.hidden, geo.mlp
     big = n * D > 1 << 20
     gen = normal_parallel if big else normal
     weights_dev, weights_np, keep = [], [], []
+    mods = qks = condition = opts = None
+    if full:
+        mods, qks, condition, opts, fkeep = _full_form(geo, L, seed)
+        keep.append(fkeep)
     for l in range(L):
         w = {"w_qkv": gen((3 * D, D), (seed, TAG_W_QKV, l), 0.02),
              "w_o": gen((D, D), (seed, TAG_W_O, l), 0.02),
@@ -47,7 +92,8 @@ def _setup(geo, L, B, W, kind, seed, n_slots):
         keep.append(dev)
         weights_np.append(exact)
         weights_dev.append(sc.BlockWeights(D, geo.heads, geo.head_dim, M, dev["w_qkv"], dev["w_o"],
-                                           dev["w_up"], dev["w_down"]))
+                                           dev["w_up"], dev["w_down"],
+                                           mod=mods[l] if full else None, qk_norm=qks[l] if full else None))
     K = geo.K
     noise_np = np.stack([np.stack([gen((n, D), (seed, TAG_NOISE, c, j)) for j in range(K + 2)])
                          for c in range(B)])
@@ -65,7 +111,10 @@ def _setup(geo, L, B, W, kind, seed, n_slots):
                                    geo.frames_per_chunk, n_slots)
         xs = noise_dev[:, K + 1].clone()
         return StackPipeline(layers=weights_dev, cache=cache, rope=rope, xs=xs, noise=noise_dev,
-                             policy=mode_kind, K=K, W=W, B=B, t_sched=T_SCHED, refresh=True)
+                             policy=mode_kind, K=K, W=W, B=B, t_sched=T_SCHED, refresh=True,
+                             condition=condition)
+    if full:
+        return make, weights_np, noise_exact.reshape(B, K + 2, n, D), keep, opts
     return make, weights_np, noise_exact.reshape(B, K + 2, n, D), keep
 
 
@@ -109,6 +158,30 @@ def test_small_same_level_pipeline_matches_oracle():
                      geo.grid_h, geo.grid_w, geo.rope_dims, geo.theta)
     outs, _, _ = run_stack(pipeline_rounds(B, geo.K, True), policy("same", geo.K, W), L,
                            lambda l: w_np[l], lambda c, j: noise_np[c, j], shp, t_sched=T_SCHED)
+    for mode, got in runs.items():
+        for c in range(B):
+            _stack_gate(got[c], outs[(c, 1)], L, (mode, c))
+
+
+def test_small_full_form_pipeline_matches_oracle():
+    """The pipelined schedule with the full block form in every layer: level
+    modulation, qk-norm and cross-attention to a cached 64-token condition
+    (projected once per layer by sc_condition_append).  Packed and serial
+    execution against the oracle's run_stack with the same block options."""
+    geo, L, B, W = SMALL, 2, 6, 2
+    make, w_np, noise_np, keep, opts = _setup(geo, L, B, W, "prog", seed=24, n_slots=60, full=True)
+    torch = torch_mod()
+    runs = {}
+    for mode in ("packed", "serial"):
+        p = make()
+        p.run(mode)
+        torch.cuda.synchronize()
+        runs[mode] = from_device(p.xs)
+    shp = BlockShape(geo.hidden, geo.heads, geo.head_dim, geo.mlp, geo.frames_per_chunk,
+                     geo.grid_h, geo.grid_w, geo.rope_dims, geo.theta)
+    outs, _, _ = run_stack(pipeline_rounds(B, geo.K, True), policy("prog", geo.K, W), L,
+                           lambda l: w_np[l], lambda c, j: noise_np[c, j], shp, t_sched=T_SCHED,
+                           options_of=lambda l: opts[l])
     for mode, got in runs.items():
         for c in range(B):
             _stack_gate(got[c], outs[(c, 1)], L, (mode, c))
