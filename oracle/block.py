@@ -162,7 +162,8 @@ def block_forward(sel, x_of: Callable[[int], np.ndarray], weights: Dict[str, np.
     rows are still computed, since every row reads all of them).  ``mod``
     is the optional per-level modulation table [levels][6][hidden];
     ``qk_norm`` the optional gains (g_q, g_k); ``cross`` the optional
-    cross-attention (see cross_attention).
+    cross-attention (see cross_attention), one for every node or a function
+    of the node (c, j) (nodes of one pack may read different conditions).
     Returns ({i: y_i}, {i: (k_i, v_i)}).
     """
     def mod_row(j):
@@ -191,7 +192,7 @@ def block_forward(sel, x_of: Callable[[int], np.ndarray], weights: Dict[str, np.
         a = o @ np.asarray(weights["w_o"], dtype=np.float64).T
         x1 = x + (a if m is None else m[2] * a)
         if cross is not None:
-            x1 = x1 + cross_attention(x1, cross, shp)
+            x1 = x1 + cross_attention(x1, cross((c, j)) if callable(cross) else cross, shp)
         u = modulated_norm(x1, m, 1) @ np.asarray(weights["w_up"], dtype=np.float64).T
         f = gelu_tanh(u) @ np.asarray(weights["w_down"], dtype=np.float64).T
         out[i] = x1 + (f if m is None else m[5] * f)

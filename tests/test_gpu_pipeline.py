@@ -30,23 +30,25 @@ pytestmark = pytest.mark.gpu
 T_SCHED = (0.0, 5.0 / 8.0, 5.0 / 6.0, 15.0 / 16.0, 1.0)
 
 
-def _full_form(geo, L, seed, n_cond_tokens=64):
-    """Per-layer modulation tables, qk-norm gains and cross-attention to one
-    cached condition (device side and the oracle's block options)."""
+def _full_form(geo, L, seed, n_cond_tokens=64, n_cond=1, cond_of=None):
+    """Per-layer modulation tables, qk-norm gains and cross-attention to
+    cached conditions (device side and the oracle's block options); chunk c
+    reads condition cond_of(c) (default 0)."""
+    cond_of = cond_of or (lambda c: 0)
     from oracle.block import condition_kv
     from synth import TAG_CTX, TAG_GAIN, TAG_W_CK, TAG_W_CO, TAG_W_CQ, TAG_W_CV
     from gpu_cases import gains
     torch = torch_mod()
     D = geo.hidden
     shp = BlockShape(D, geo.heads, geo.head_dim, geo.mlp)
-    nb = sc.sc_cache_pool_bytes(L, geo.heads, geo.head_dim, n_cond_tokens, 1, 1)
+    nb = sc.sc_cache_pool_bytes(L, geo.heads, geo.head_dim, n_cond_tokens, 1, n_cond)
     pool = torch.zeros(nb, dtype=torch.uint8, device="cuda")
-    cond = sc.sc_cache_create(pool, L, geo.heads, geo.head_dim, n_cond_tokens, 1, 1)
+    cond = sc.sc_cache_create(pool, L, geo.heads, geo.head_dim, n_cond_tokens, 1, n_cond)
     ws_bytes = sc.sc_condition_workspace_bytes(cond)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
-    ctx_dev, ctx = to_device(normal((n_cond_tokens, D), (seed, TAG_CTX, 0)), sc.SC_DTYPE_BF16)
+    ctxs = [to_device(normal((n_cond_tokens, D), (seed, TAG_CTX, i)), sc.SC_DTYPE_BF16) for i in range(n_cond)]
     s = 1.0 / np.sqrt(D)
-    mods, qks, cross, opts, keep = [], [], [], [], [pool, ws, ctx_dev]
+    mods, qks, cross, opts, keep = [], [], [], [], [pool, ws, ctxs]
     for l in range(L):
         w = {}
         for name, tag in (("w_q", TAG_W_CQ), ("w_k", TAG_W_CK), ("w_v", TAG_W_CV), ("w_o", TAG_W_CO)):
@@ -58,20 +60,23 @@ def _full_form(geo, L, seed, n_cond_tokens=64):
         mod[:, 2] += 1.0
         mod[:, 5] += 1.0
         md = torch.from_numpy(mod).cuda()
-        sc.sc_condition_append(cond, l, (0, 0), ctx_dev, w["w_k"][0], w["w_v"][0], gd[3], ws, ws_bytes)
-        k, v = condition_kv(ctx, w["w_k"][1], w["w_v"][1], shp, g[3].astype(np.float64))
+        per_cond = []
+        for i, (ctx_dev, ctx) in enumerate(ctxs):
+            sc.sc_condition_append(cond, l, (i, 0), ctx_dev, w["w_k"][0], w["w_v"][0], gd[3], ws, ws_bytes)
+            k, v = condition_kv(ctx, w["w_k"][1], w["w_v"][1], shp, g[3].astype(np.float64))
+            per_cond.append({"k": k, "v": v, "w_q": w["w_q"][1], "w_o": w["w_o"][1],
+                             "g_q": g[2].astype(np.float64)})
         mods.append(md)
         qks.append(gd[0:2])
         cross.append((w["w_q"][0], w["w_o"][0], gd[2]))
         opts.append({"mod": mod, "qk_norm": (g[0].astype(np.float64), g[1].astype(np.float64)),
-                     "cross": {"k": k, "v": v, "w_q": w["w_q"][1], "w_o": w["w_o"][1],
-                               "g_q": g[2].astype(np.float64)}})
+                     "cross": (lambda node, pc=per_cond: pc[cond_of(node[0])])})
         keep += [w, gd, md]
     torch.cuda.synchronize()
-    return mods, qks, {"cache": cond, "cross": cross}, opts, keep
+    return mods, qks, {"cache": cond, "cross": cross, "condition_of": lambda c: (cond_of(c), 0)}, opts, keep
 
 
-def _setup(geo, L, B, W, kind, seed, n_slots, full=False):
+def _setup(geo, L, B, W, kind, seed, n_slots, full=False, n_cond=1, cond_of=None):
     torch = torch_mod()
     n, D, M = geo.tokens_per_chunk, geo.hidden, geo.mlp
     big = n * D > 1 << 20
@@ -79,7 +84,7 @@ def _setup(geo, L, B, W, kind, seed, n_slots, full=False):
     weights_dev, weights_np, keep = [], [], []
     mods = qks = condition = opts = None
     if full:
-        mods, qks, condition, opts, fkeep = _full_form(geo, L, seed)
+        mods, qks, condition, opts, fkeep = _full_form(geo, L, seed, n_cond=n_cond, cond_of=cond_of)
         keep.append(fkeep)
     for l in range(L):
         w = {"w_qkv": gen((3 * D, D), (seed, TAG_W_QKV, l), 0.02),
@@ -185,6 +190,28 @@ def test_small_full_form_pipeline_matches_oracle():
     for mode, got in runs.items():
         for c in range(B):
             _stack_gate(got[c], outs[(c, 1)], L, (mode, c))
+
+
+def test_small_pipeline_condition_switch():
+    """Chunks 0-2 read one condition and chunks 3-5 another (a prompt change
+    in the stream): rounds whose packs straddle the switch give their nodes
+    different conditions through one condition plan."""
+    geo, L, B, W = SMALL, 2, 6, 2
+    switch = lambda c: 0 if c < 3 else 1
+    make, w_np, noise_np, keep, opts = _setup(geo, L, B, W, "prog", seed=25, n_slots=60, full=True,
+                                              n_cond=2, cond_of=switch)
+    torch = torch_mod()
+    p = make()
+    p.run("packed")
+    torch.cuda.synchronize()
+    got = from_device(p.xs)
+    shp = BlockShape(geo.hidden, geo.heads, geo.head_dim, geo.mlp, geo.frames_per_chunk,
+                     geo.grid_h, geo.grid_w, geo.rope_dims, geo.theta)
+    outs, _, _ = run_stack(pipeline_rounds(B, geo.K, True), policy("prog", geo.K, W), L,
+                           lambda l: w_np[l], lambda c, j: noise_np[c, j], shp, t_sched=T_SCHED,
+                           options_of=lambda l: opts[l])
+    for c in range(B):
+        _stack_gate(got[c], outs[(c, 1)], L, ("switch", c))
 
 
 def _stack_gate(got, want, L, what, runs=1):

@@ -457,3 +457,21 @@ def test_condition_kv_is_linear_and_key_norm_is_scale_free():
     np.testing.assert_allclose(kb, kn, rtol=2e-6)       # eps / mean square, halved
     np.testing.assert_allclose(vb, 8.0 * vn, atol=1e-12)
     np.testing.assert_array_equal(vn, v1)
+
+
+def test_cross_attention_per_node_condition():
+    """A per-node condition function gives each node the block it would get
+    alone with that condition."""
+    shp = _tiny_shape()
+    pack = [(1, 1), (2, 2)]
+    sel = select(policy("prog", 4, 2), pack)
+    xs, res = _pack_inputs(shp, 18)
+    w = _weights(shp, 0)
+    crs = [_cross(shp, 5, 20), _cross(shp, 3, 21)]
+    mixed, _ = block_forward(sel, lambda i: xs[i], w, res.__getitem__, shp,
+                             cross=lambda node: crs[node[0] - 1])
+    for i in range(2):
+        alone, _ = block_forward(sel, lambda k: xs[k], w, res.__getitem__, shp, cross=crs[i])
+        np.testing.assert_array_equal(mixed[i], alone[i])
+    one, _ = block_forward(sel, lambda k: xs[k], w, res.__getitem__, shp, cross=crs[0])
+    assert np.max(np.abs(one[1] - mixed[1])) > 1e-3
