@@ -42,9 +42,9 @@ static int cross_check(const sc_cross_attn* cr, const sc_cache* c, const sc_plan
                 cr->plan->nodes.size(), cr->plan->nq, p->nodes.size(), p->nq);
   if (cr->q_norm && misaligned16(cr->q_norm))
     return fail(SC_EINVAL, "condition query gain must be 16-byte aligned");
-  int rc = plan_check(cr->plan, cr->cache, layer);
+  int rc = attention_check(cr->plan, cr->cache);  // shape support first, then state
   if (rc != SC_OK) return rc;
-  return attention_check(cr->plan, cr->cache);
+  return plan_check(cr->plan, cr->cache, layer);
 }
 
 extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t layer,

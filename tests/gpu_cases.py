@@ -151,15 +151,16 @@ class ConditionCase:
     Weights are N(0, 1/hidden), so projections of unit-variance inputs have
     unit variance and the cross logits are O(1)."""
 
-    def __init__(self, geo, L, seed, n_cond=1, q_norm=False, k_norm=False):
+    def __init__(self, geo, L, seed, n_cond=1, q_norm=False, k_norm=False, pages=1):
         from oracle.block import BlockShape, condition_kv
         from synth import TAG_CTX, TAG_GAIN, TAG_W_CK, TAG_W_CO, TAG_W_CQ, TAG_W_CV
         torch = torch_mod()
         D = geo.hidden
         self.geo, self.L, self.n_cond = geo, L, n_cond
-        nbytes = sc.sc_cache_pool_bytes(1, geo.heads, geo.head_dim, L, 1, n_cond)
+        tpp = L // pages                                  # a condition spans `pages` page slots
+        nbytes = sc.sc_cache_pool_bytes(1, geo.heads, geo.head_dim, tpp, pages, n_cond * pages)
         self.pool = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
-        self.cache = sc.sc_cache_create(self.pool, 1, geo.heads, geo.head_dim, L, 1, n_cond)
+        self.cache = sc.sc_cache_create(self.pool, 1, geo.heads, geo.head_dim, tpp, pages, n_cond * pages)
         self.w_dev, self.w = {}, {}
         s = 1.0 / math.sqrt(D)
         for name, tag in (("w_q", TAG_W_CQ), ("w_k", TAG_W_CK), ("w_v", TAG_W_CV), ("w_o", TAG_W_CO)):

@@ -52,13 +52,14 @@ def test_condition_append_matches_oracle(k_norm):
     assert e.value.code == sc.SC_EEXIST
 
 
-@pytest.mark.parametrize("nq", [300, 96], ids=["256-query", "128-query"])
-def test_attention_over_condition_plan(nq):
+@pytest.mark.parametrize("nq,L,pages", [(300, 200, 1), (96, 200, 1), (300, 256, 2)],
+                         ids=["256-query", "128-query", "two-page-condition"])
+def test_attention_over_condition_plan(nq, L, pages):
     """Each pack node reads its own condition (two nodes share one), every
-    query sees all L tokens; ragged L and ragged query counts."""
+    query sees all L tokens; ragged L and ragged query counts; a condition
+    spread over two page slots."""
     torch = torch_mod()
-    L = 200
-    cc = ConditionCase(SMALL, L, seed=22, n_cond=3, k_norm=True)
+    cc = ConditionCase(SMALL, L, seed=22, n_cond=3, k_norm=True, pages=pages)
     conds = [0, 2, 1, 0]
     plan = cc.plan(conds, nq)
     H, d = SMALL.heads, SMALL.head_dim

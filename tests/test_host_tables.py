@@ -322,3 +322,17 @@ def test_condition_append_and_cross_block_checks_without_device():
             sc.sc_block_forward(bw, cache, 0, plan, 0x6000, None, 0x7000, ws_bytes)
         assert e.value.code == code, (cross, qk)
     assert not cache.contains((0, 4), 0)                  # nothing was written
+    # a condition shorter than one 64-key tile has no bf16 kernel
+    short = sc.sc_cache_create(0x400000, 1, 2, 128, 32, 1, 1)
+    sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(0, 0)]), short)
+    sp = sc.sc_plan_condition(short, [(0, 0), (0, 0)], 64)
+    bw = sc.BlockWeights(D, 2, 128, 512, 0x1000, 0x2000, 0x3000, 0x4000,
+                         cross=sc.CrossAttn(0x1000, 0x2000, short, sp))
+    with pytest.raises(sc.ScError) as e:
+        sc.sc_block_forward(bw, cache, 0, plan, 0x6000, None, 0x7000, ws_bytes)
+    assert e.value.code == sc.SC_EUNSUPPORTED
+    # the condition projection is bf16 only
+    f32 = sc.sc_cache_create(0x500000, 1, 2, 128, 64, 1, 1, sc.SC_DTYPE_F32)
+    with pytest.raises(sc.ScError) as e:
+        sc.sc_condition_append(f32, 0, (0, 0), 0x1000, 0x2000, 0x3000, None, 0x4000, 1 << 30)
+    assert e.value.code == sc.SC_EUNSUPPORTED
