@@ -253,7 +253,7 @@ def gemm_flops(n_tokens, g):
     return 2.0 * n_tokens * (D * 3 * D + D * D + D * M + M * D)
 
 
-def cpu_baseline(wl, seed=0, row_stride=16):
+def cpu_baseline(wl, seed=0, row_stride=4):
     """The oracle's block on this workload, timed on the host's cores.
 
     Bounded sample: K/V projections for every token of every pack node (every
