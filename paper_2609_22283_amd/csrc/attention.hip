@@ -683,17 +683,20 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
   for (int qb = 0; qb < 2; ++qb) store_rows<BQ>(it, g, o, oacc[qb], m[qb], l[qb], wave * 32 + 16 * qb + c, lg);
 }
 
-// Merges the pieces of each tail unit, in piece order: one work-group per
-// tail unit, one thread per query row.  With m = max m_p:
+// Merges the pieces of each tail unit, in piece order.  A work-group takes 8
+// query rows of one tail unit; 32 lanes share a row, each holding 4 of its
+// 128 outputs, so every partial row is read as one contiguous 512-byte run.
+// With m = max m_p:
 //   O = sum_p 2^(m_p - m) O_p / sum_p 2^(m_p - m) l_p.
 template <int BQ>
-__global__ __launch_bounds__(BQ) void attn_combine_kernel(uint16_t* __restrict__ o, AttnGeom g, AttnPlan plan) {
+__global__ __launch_bounds__(256) void attn_combine_kernel(uint16_t* __restrict__ o, AttnGeom g, AttnPlan plan) {
   const int32_t tu = blockIdx.x;
   const int32_t unit = g.whole_units + tu;
   const int32_t qt = unit % g.n_qtiles;
   const int32_t node = (unit / g.n_qtiles) % g.n_nodes;
   const int32_t head = unit / (g.n_qtiles * g.n_nodes);
-  const int32_t lrow = threadIdx.x;
+  const int32_t lrow = blockIdx.y * 8 + (threadIdx.x >> 5);
+  const int32_t dl = threadIdx.x & 31;
   const int32_t qrow = qt * BQ + lrow;
   if (qrow >= g.nq) return;
   const int32_t nt = node_tiles(plan, g, node);
@@ -701,34 +704,22 @@ __global__ __launch_bounds__(BQ) void attn_combine_kernel(uint16_t* __restrict__
   float m = -INFINITY;
   for (int32_t p = 0; p < g.tail_split; ++p)
     if (nonempty(p)) m = fmaxf(m, g.part_ml[((size_t)(p * g.tail_units + tu) * 2 + 0) * BQ + lrow]);
-  float acc[HDB];
-#pragma unroll
-  for (int d = 0; d < HDB; ++d) acc[d] = 0.f;
+  f32x4 acc = {};
   float l = 0.f;
   for (int32_t p = 0; p < g.tail_split; ++p) {
     if (!nonempty(p)) continue;
     const size_t slot = (size_t)p * g.tail_units + tu;
     const float a = __builtin_amdgcn_exp2f(g.part_ml[(slot * 2 + 0) * BQ + lrow] - m);
     l += a * g.part_ml[(slot * 2 + 1) * BQ + lrow];
-    const f32x4* po = reinterpret_cast<const f32x4*>(g.part_o + (slot * BQ + lrow) * HDB);
+    const f32x4 v = *reinterpret_cast<const f32x4*>(g.part_o + (slot * BQ + lrow) * HDB + 4 * dl);
 #pragma unroll
-    for (int d4 = 0; d4 < HDB / 4; ++d4) {
-      const f32x4 v = po[d4];
-      acc[4 * d4 + 0] += a * v[0];
-      acc[4 * d4 + 1] += a * v[1];
-      acc[4 * d4 + 2] += a * v[2];
-      acc[4 * d4 + 3] += a * v[3];
-    }
+    for (int e = 0; e < 4; ++e) acc[e] += a * v[e];
   }
   const float inv = 1.f / l;
-  uint16_t* op = o + (((size_t)node * g.nq + qrow) * g.n_heads + head) * HDB;
-#pragma unroll
-  for (int d8 = 0; d8 < HDB / 8; ++d8) {
-    u32x4 v;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) v[k] = pack_bf16x2(acc[8 * d8 + 2 * k] * inv, acc[8 * d8 + 2 * k + 1] * inv);
-    *reinterpret_cast<u32x4*>(op + 8 * d8) = v;
-  }
+  u32x2 r;
+  r.x = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+  r.y = pack_bf16x2(acc[2] * inv, acc[3] * inv);
+  *reinterpret_cast<u32x2*>(o + (((size_t)node * g.nq + qrow) * g.n_heads + head) * HDB + 4 * dl) = r;
 }
 
 // Tail split for a plan: units = heads x nodes x query tiles; the last
@@ -866,11 +857,11 @@ int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const v
   if (g.tail_units) {
     timer_begin(TK_ATTN_COMBINE, stream);
     if (bq == BQ_SMALL)
-      hipLaunchKernelGGL(attn_combine_kernel<BQ_SMALL>, dim3((uint32_t)g.tail_units), dim3(BQ_SMALL), 0, stream,
-                         ob, g, plan);
+      hipLaunchKernelGGL(attn_combine_kernel<BQ_SMALL>, dim3((uint32_t)g.tail_units, BQ_SMALL / 8), dim3(256),
+                         0, stream, ob, g, plan);
     else
-      hipLaunchKernelGGL(attn_combine_kernel<BQ_MAX>, dim3((uint32_t)g.tail_units), dim3(BQ_MAX), 0, stream,
-                         ob, g, plan);
+      hipLaunchKernelGGL(attn_combine_kernel<BQ_MAX>, dim3((uint32_t)g.tail_units, BQ_MAX / 8), dim3(256), 0,
+                         stream, ob, g, plan);
     timer_end(TK_ATTN_COMBINE, stream);
   }
   SC_HIP(hipGetLastError());
