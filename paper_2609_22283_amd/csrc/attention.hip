@@ -616,62 +616,78 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
   float m[2] = {0.f, 0.f}, l[2];
   f32x4 lsum[2] = {f32x4{}, f32x4{}};  // value 0 of lanes 0..15: row sums of the two blocks
   const bf16x8 ones = ones_row(c);
-  // prologue: K(ta), V(ta), K(ta+1) in flight; S(ta) = K(ta) Q^T; m = its exact column maxima
-  {
-    const typename KvTiles<NW>::Slots s0 = kv.slots(ta * BK);
-    kv.copy_k(ta * BK, smem, s0);
-    kv.copy_v(ta * BK, smem + 2 * KT_BYTES, s0);
-    if (ta + 1 < ntiles) kv.copy_k((ta + 1) * BK, smem + KT_BYTES, kv.slots((ta + 1) * BK));
-  }
-  landed();
+  // A wave whose 32 queries all lie past the node's end (in a node's last
+  // query tile) still copies its share of every tile and meets every
+  // barrier, but skips the matrix and softmax work.
+  const bool active = it.qt * BQ + wave * 32 < g.nq;
   STile s;
-  qk_tile(smem, L, qreg, s, m);
-  if (ta + 1 == ntiles && ragged) mask_tile(s, ta * BK, nk, lg);
-  tile_max(s, m);
+  auto run = [&](auto act) __attribute__((always_inline)) {
+    constexpr bool ACT = decltype(act)::value;
+    // prologue: K(ta), V(ta), K(ta+1) in flight; S(ta) = K(ta) Q^T; m = its exact column maxima
+    {
+      const typename KvTiles<NW>::Slots s0 = kv.slots(ta * BK);
+      kv.copy_k(ta * BK, smem, s0);
+      kv.copy_v(ta * BK, smem + 2 * KT_BYTES, s0);
+      if (ta + 1 < ntiles) kv.copy_k((ta + 1) * BK, smem + KT_BYTES, kv.slots((ta + 1) * BK));
+    }
+    landed();
+    if constexpr (ACT) {
+      qk_tile(smem, L, qreg, s, m);
+      if (ta + 1 == ntiles && ragged) mask_tile(s, ta * BK, nk, lg);
+      tile_max(s, m);
 #pragma unroll
-  for (int h = 0; h < 2; ++h)
+      for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
+          for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) s[h][b][qb][r] -= m[qb];
-  __syncthreads();  // every wave has read K(ta) before K(ta+2) is copied over it
+            for (int r = 0; r < 4; ++r) s[h][b][qb][r] -= m[qb];
+    }
+    __syncthreads();  // every wave has read K(ta) before K(ta+2) is copied over it
 
-  // iteration t (buffer parity counted from ta): copy K(t+2) over K(t) and
-  // V(t+1) over V(t-1), then step t
-  int32_t t = ta;
-  typename KvTiles<NW>::Slots sk = kv.slots(min(ta + 2, it.ntiles - 1) * BK);
-  typename KvTiles<NW>::Slots sv = kv.slots(min(ta + 1, it.ntiles - 1) * BK);
-  for (; t + 2 < ntiles; t += 2) {
-    kv.copy_k((t + 2) * BK, smem, sk);
-    kv.copy_v((t + 1) * BK, smem + 2 * KT_BYTES + VT_BYTES, sv);
-    sk = kv.slots(min(t + 3, it.ntiles - 1) * BK);
-    sv = kv.slots(min(t + 2, it.ntiles - 1) * BK);
-    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
-    landed();
-    if (t + 3 < ntiles) kv.copy_k((t + 3) * BK, smem + KT_BYTES, sk);
-    kv.copy_v((t + 2) * BK, smem + 2 * KT_BYTES, sv);
-    sk = kv.slots(min(t + 4, it.ntiles - 1) * BK);
-    sv = kv.slots(min(t + 3, it.ntiles - 1) * BK);
-    attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, (t + 1) * BK, nk, lg);
-    landed();
-  }
-  if (t + 1 < ntiles) {  // two tiles left, parity 0
-    kv.copy_v((t + 1) * BK, smem + 2 * KT_BYTES + VT_BYTES, sv);
-    attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
-    landed();
-    ++t;
-    if (ragged)
-      attn_step<0, 1, false, true>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
-    else
-      attn_step<0, 1, false, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
-  } else {               // one tile left, parity 0 (masking twice is harmless)
-    if (ragged)
-      attn_step<1, 0, false, true>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
-    else
-      attn_step<1, 0, false, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
-  }
+    // iteration t (buffer parity counted from ta): copy K(t+2) over K(t) and
+    // V(t+1) over V(t-1), then step t
+    int32_t t = ta;
+    typename KvTiles<NW>::Slots sk = kv.slots(min(ta + 2, it.ntiles - 1) * BK);
+    typename KvTiles<NW>::Slots sv = kv.slots(min(ta + 1, it.ntiles - 1) * BK);
+    for (; t + 2 < ntiles; t += 2) {
+      kv.copy_k((t + 2) * BK, smem, sk);
+      kv.copy_v((t + 1) * BK, smem + 2 * KT_BYTES + VT_BYTES, sv);
+      sk = kv.slots(min(t + 3, it.ntiles - 1) * BK);
+      sv = kv.slots(min(t + 2, it.ntiles - 1) * BK);
+      if constexpr (ACT) attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
+      landed();
+      if (t + 3 < ntiles) kv.copy_k((t + 3) * BK, smem + KT_BYTES, sk);
+      kv.copy_v((t + 2) * BK, smem + 2 * KT_BYTES, sv);
+      sk = kv.slots(min(t + 4, it.ntiles - 1) * BK);
+      sv = kv.slots(min(t + 3, it.ntiles - 1) * BK);
+      if constexpr (ACT)
+        attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, (t + 1) * BK, nk, lg);
+      landed();
+    }
+    if (t + 1 < ntiles) {  // two tiles left, parity 0
+      kv.copy_v((t + 1) * BK, smem + 2 * KT_BYTES + VT_BYTES, sv);
+      if constexpr (ACT) attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
+      landed();
+      ++t;
+      if constexpr (ACT) {
+        if (ragged)
+          attn_step<0, 1, false, true>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
+        else
+          attn_step<0, 1, false, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
+      }
+    } else if constexpr (ACT) {  // one tile left, parity 0 (masking twice is harmless)
+      if (ragged)
+        attn_step<1, 0, false, true>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
+      else
+        attn_step<1, 0, false, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
+    }
+  };
+  if (active)
+    run(std::true_type{});
+  else
+    run(std::false_type{});
   // the guard, on the final sums (also NaN / inf)
   const bool bad = __builtin_amdgcn_ballot_w64(!(lsum[0][0] < P_GUARD && lsum[1][0] < P_GUARD)) != 0;
   l[0] = lsum[0][0];  // zero outside lanes 0..15, so the group sum is the row sum
