@@ -12,22 +12,23 @@
 // QKV and STORE can also emit per-token sums of squares over each wave's 128
 // features, the first half of an RMSNorm over the feature axis (qk-norm);
 // norm_scale_kernel finishes it.
-// Work-group tile 256 (features) x 256 (tokens) x 64 (k), eight waves of
-// 128 x 64, operands double-buffered in LDS with an XOR swizzle.  Each lane
-// holds four consecutive features of one token, so RoPE pairs stay in-lane.
+// Work-group tile 256 (features) x BN (tokens: 256, 192 or 128) x 64 (k),
+// eight waves of 128 x BN/4, operands double-buffered in LDS with an XOR
+// swizzle.  Each lane holds four consecutive features of one token, so RoPE
+// pairs stay in-lane.
 #include "device.h"
 #include "gemm.h"
 #include "internal.h"
 
 namespace sc {
 
-constexpr int GBM = 256, GBN = 256, GBK = 64;
+constexpr int GBM = 256, GBK = 64;
 constexpr int GWM = 128;
 constexpr int G_NW = 8;               // waves per work-group, two per SIMD
 constexpr int G_THREADS = 64 * G_NW;
-constexpr int GWN = 2 * GBN / G_NW;   // tokens per wave tile
-constexpr int GROWS = GBM / G_NW;     // operand rows each wave copies per stage
+constexpr int GROWS = GBM / G_NW;     // weight rows each wave copies per stage
 constexpr int G_TILE_BYTES = GBM * GBK * 2;  // 32 KB per operand per stage
+constexpr int kGemmCUs = 256;          // one work-group per CU
 
 // GELU_tanh(x) = 0.5 x (1 + tanh(u)) = x * sigmoid(2 u), u = sqrt(2/pi) (x + 0.044715 x^3),
 // evaluated as x / (1 + 2^(-2 u log2 e)).
@@ -67,7 +68,8 @@ __device__ __forceinline__ void store_sum_squares(const f32x4 (&acc)[FB][TB], fl
   }
 }
 
-template <int EPI>
+// BN tokens per work-group tile (256, 192 or 128): 64 BN / 256 tokens per wave.
+template <int EPI, int BN>
 __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t* __restrict__ W,
                                                                  const uint16_t* __restrict__ X,
                                                                  int32_t F, int32_t T, int32_t Kd,
@@ -75,7 +77,9 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   // stage s: W tile at s * 64 KB, X tile at s * 64 KB + 32 KB; rows of 64 k
   // (128 B) with 16-byte column c stored at c ^ ((row >> 1) & 7)
   __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * G_TILE_BYTES];
-  const int32_t n_tf = F / GBM, n_tt = (T + GBN - 1) / GBN;
+  constexpr int GWN = BN / 4;          // tokens per wave tile
+  constexpr int XROWS = BN / G_NW;     // token rows each wave copies per stage
+  const int32_t n_tf = F / GBM, n_tt = (T + BN - 1) / BN;
   // Each XCD takes a contiguous run of logical tiles; the run is walked in
   // groups of GT token tiles, feature tiles outermost within a group, so the
   // ~32 tiles an XCD holds at once share 4-5 weight and 8 token panels in L2.
@@ -84,24 +88,30 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   const int32_t group = tile / (GT * n_tf), in_group = tile - group * GT * n_tf;
   const int32_t gt = min(GT, n_tt - group * GT);
   const int32_t tf = in_group / gt, tt = group * GT + in_group % gt;
-  const int32_t f0 = tf * GBM, t0 = tt * GBN;
+  const int32_t f0 = tf * GBM, t0 = tt * BN;
 
   const int32_t tid = threadIdx.x, lane = tid & 63;
   const int32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: LDS copy addresses stay scalar
   const int32_t lg = lane >> 4, c16 = lane & 15;
   const int32_t wf = (wave & 1) * GWM, wt = (wave >> 1) * GWN;
 
-  // copies: each wave moves rows [GROWS wave, GROWS wave + GROWS) of both
-  // operand tiles, 8 rows (1 KB) per instruction; lane (row, p) fetches
-  // column p ^ ((row >> 1) & 7).  Byte offsets are fixed per lane; the k
-  // offset is folded into the (wave-uniform) base pointer.
-  constexpr int NCP = GROWS / 8;
-  uint32_t woff[NCP], xoff[NCP];
+  // copies: each wave moves weight rows [GROWS wave, GROWS wave + GROWS) and
+  // token rows [XROWS wave, XROWS wave + XROWS), 8 rows (1 KB) per
+  // instruction; lane (row, p) fetches column p ^ ((row >> 1) & 7).  Byte
+  // offsets are fixed per lane; the k offset is folded into the
+  // (wave-uniform) base pointer.
+  constexpr int NCP = GROWS / 8, NCPX = XROWS / 8;
+  uint32_t woff[NCP], xoff[NCPX];
 #pragma unroll
   for (int j = 0; j < NCP; ++j) {
     const int32_t row = GROWS * wave + 8 * j + (lane >> 3);
     const int32_t col = (lane & 7) ^ ((row >> 1) & 7);
     woff[j] = ((uint32_t)(f0 + row) * Kd + col * 8) * 2;
+  }
+#pragma unroll
+  for (int j = 0; j < NCPX; ++j) {
+    const int32_t row = XROWS * wave + 8 * j + (lane >> 3);
+    const int32_t col = (lane & 7) ^ ((row >> 1) & 7);
     const int32_t trow = min(t0 + row, T - 1);
     xoff[j] = ((uint32_t)trow * Kd + col * 8) * 2;
   }
@@ -115,7 +125,7 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
 #pragma unroll
     for (int j = 0; j < NCP; ++j) {
       gdma16(wk + woff[j], a + (GROWS * wave + 8 * j) * 128);
-      gdma16(xk + xoff[j], b + (GROWS * wave + 8 * j) * 128);
+      if (j < NCPX) gdma16(xk + xoff[j], b + (XROWS * wave + 8 * j) * 128);
     }
   };
   auto landed = [&]() {
@@ -284,6 +294,47 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   }
 }
 
+template <int BN>
+static void launch_gemm_bn(int epi, const uint16_t* W, const uint16_t* X, int32_t F, int32_t T, int32_t Kd,
+                           const GemmEpilogue& ep, hipStream_t stream) {
+  const dim3 grid((uint32_t)(F / GBM) * (uint32_t)((T + BN - 1) / BN));
+  switch (epi) {
+    case EPI_QKV:
+      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV, BN>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
+      break;
+    case EPI_GELU:
+      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_GELU, BN>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
+      break;
+    case EPI_RESIDUAL:
+      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_RESIDUAL, BN>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd,
+                         ep);
+      break;
+    default:
+      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_STORE, BN>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
+  }
+}
+
+// Token-tile width of a launch: one work-group per CU, so a launch of n
+// tiles takes ceil(n / CUs) rounds of one tile's time.  A tile of BN tokens
+// takes BN / 256 of a 256-token tile's time times a per-width efficiency
+// loss (more fragment reads and copies per MFMA), measured on the Wan
+// block's four GEMMs: up to 1.12 at 192 tokens, 1.4 at 128.  The width with
+// the fewest tile-times wins, the wider one on ties.
+static int gemm_tile_tokens(int32_t F, int32_t T) {
+  int best = 256;
+  double best_cost = 1e30;
+  for (const int bn : {256, 192, 128}) {
+    const int64_t tiles = (int64_t)(F / GBM) * ((T + bn - 1) / bn);
+    const double eff = bn == 256 ? 1.0 : bn == 192 ? 1.12 : 1.4;
+    const double cost = (double)((tiles + kGemmCUs - 1) / kGemmCUs) * bn / 256.0 * eff;
+    if (cost < best_cost - 1e-9) {
+      best_cost = cost;
+      best = bn;
+    }
+  }
+  return best;
+}
+
 int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, int32_t F, int32_t T,
                 int32_t Kd, const GemmEpilogue& ep, hipStream_t stream) {
   if (F % GBM || Kd % GBK || T <= 0)
@@ -293,24 +344,11 @@ int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, i
     return fail(SC_EUNSUPPORTED, "gemm operands beyond 4 GB");
   if (epi == EPI_QKV && (ep.hidden % GBM || ep.head_dim != GWM))
     return fail(SC_EUNSUPPORTED, "QKV epilogue needs hidden %% %d == 0 and head_dim %d", GBM, GWM);
-  const uint32_t tiles = (uint32_t)(F / GBM) * (uint32_t)((T + GBN - 1) / GBN);
   timer_begin(timer_kind, stream);
-  switch (epi) {
-    case EPI_QKV:
-      hipLaunchKernelGGL(gemm_bf16_kernel<EPI_QKV>, dim3(tiles), dim3(G_THREADS), 0, stream, W, X, F,
-                         T, Kd, ep);
-      break;
-    case EPI_GELU:
-      hipLaunchKernelGGL(gemm_bf16_kernel<EPI_GELU>, dim3(tiles), dim3(G_THREADS), 0, stream, W, X,
-                         F, T, Kd, ep);
-      break;
-    case EPI_RESIDUAL:
-      hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESIDUAL>, dim3(tiles), dim3(G_THREADS), 0, stream, W,
-                         X, F, T, Kd, ep);
-      break;
-    default:
-      hipLaunchKernelGGL(gemm_bf16_kernel<EPI_STORE>, dim3(tiles), dim3(G_THREADS), 0, stream, W, X,
-                         F, T, Kd, ep);
+  switch (gemm_tile_tokens(F, T)) {
+    case 128: launch_gemm_bn<128>(epi, W, X, F, T, Kd, ep, stream); break;
+    case 192: launch_gemm_bn<192>(epi, W, X, F, T, Kd, ep, stream); break;
+    default: launch_gemm_bn<256>(epi, W, X, F, T, Kd, ep, stream);
   }
   timer_end(timer_kind, stream);
   SC_HIP(hipGetLastError());

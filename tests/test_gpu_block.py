@@ -251,14 +251,25 @@ def test_block_rejects_oversized_pack():
     assert e.value.code == sc.SC_EUNSUPPORTED
 
 
-def test_wan_block_prog_sampled_rows():
-    wl = cfg4_prog(False)
-    case = BlockCase(WAN, wl.policy, wl.pack, wl.resident, seed=12)
+# Wan-shaped packs of 4, 5 and 1 nodes (T = 18720, 23400, 4680 tokens).
+# The GEMMs pick their token-tile width from T, so between them these run
+# every width: QKV on 192 / 256 / 192 tokens, the MLP-up GEMM on 256, and the
+# out-projection and MLP-down GEMMs on 256 / 192 / 128.
+WAN_BLOCK_PACKS = [
+    ("prog", cfg4_prog(False).pack, cfg4_prog(False).resident),
+    ("prog", cfg4_prog(True).pack, cfg4_prog(True).resident),
+    ("clean", [(6, 4)], [(c, 0) for c in range(6)]),
+]
+
+
+@pytest.mark.parametrize("kind,pack,resident", WAN_BLOCK_PACKS, ids=["4-node", "5-node", "1-node"])
+def test_wan_block_sampled_rows(kind, pack, resident):
+    case = BlockCase(WAN, kind, pack, resident, seed=12)
     got = case.run()
     rows = sample_rows(WAN.tokens_per_chunk, 24, seed=3)
     want, _ = case.oracle(rows=rows)
-    for i in range(len(wl.pack)):
-        block_gate(got[i][rows], want[i], f"wan node {wl.pack[i]}")
+    for i in range(len(pack)):
+        block_gate(got[i][rows], want[i], f"wan {kind} node {pack[i]}")
 
 
 def test_sampler_matches_oracle():
