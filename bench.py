@@ -43,7 +43,7 @@ METRIC = "steady-state latent frames/s per DiT block + attention TFLOP/s (% bf16
 # read for a plain 256 MiB copy (x2.0 fetch, x1.0 write).  Valid only for the
 # kernel sources it was measured on (hash below); otherwise reported as null.
 ATTN_TRAFFIC = {"sources_sha1": "08d36417edce4501609768776b5639133155d77c",
-                "fetch_bytes": 1.7942e+09, "write_bytes": 2.1524e+08}
+                "fetch_bytes": 1.7967e+09, "write_bytes": 2.1524e+08}
 
 
 def attn_traffic():
