@@ -212,12 +212,11 @@ def time_steps(setup, fn, steps, warmup, timer=False):
 
 
 def mfma_ceiling(iters=4000, launches=5):
-    """Sustained rate of the library's matrix-core probe (back-to-back bf16
-    MFMAs from registers, no memory traffic), with random and with constant
-    operands: TFLOP/s each, measured right after the timed steps.  The gap
-    between the two shows the data-dependent, power-limited clock; it is
-    context for the roofline, not a bound (tuned GEMMs exceed the random
-    rate)."""
+    """Sustained rate of the library's matrix-core probe (back-to-back
+    16x16x32 bf16 MFMAs from registers, no memory traffic), with random and
+    with constant operands: TFLOP/s each, measured right after the timed
+    steps.  The gap between the two shows the data-dependent, power-limited
+    clock; it is context for the roofline, not a bound."""
     import torch
 
     import paper_2609_22283_amd as sc

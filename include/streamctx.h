@@ -343,7 +343,7 @@ int sc_timer_enable(int on);
 int sc_timer_read(const char* kind, int32_t* launches, double* total_ms);
 
 /* ---- Matrix-core ceiling probe (measurement support) ------------------
- * Launches one kernel on `stream` that issues only 32x32x16 bf16 MFMAs from
+ * Launches one kernel on `stream` that issues only 16x16x32 bf16 MFMAs from
  * registers (two 8-wave work-groups per CU, `iters` rounds of 16 MFMAs per
  * wave) and sets *flops to the work it performs; the caller times it with
  * its own events.  random_operands != 0 fills the operands with random bf16

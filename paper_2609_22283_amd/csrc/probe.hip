@@ -1,7 +1,8 @@
 // Matrix-core ceiling probe (measurement support, not part of the method).
 // A grid of 8-wave work-groups, two per CU, issues back-to-back
-// 32x32x16 bf16 MFMAs on four accumulator chains with operands held in
-// registers: no memory traffic, no vector-ALU work.  Random operands toggle
+// 16x16x32 bf16 MFMAs (the instruction of the attention and GEMM kernels) on
+// eight accumulator chains with operands held in registers: no memory
+// traffic, no vector-ALU work.  Random operands toggle
 // many bits and draw more power than constant ones; the two sustained rates
 // show how far the power-limited clock moves with the data.
 #include "device.h"
@@ -33,16 +34,16 @@ __global__ __launch_bounds__(kProbeThreads) void mfma_probe_kernel(float* out, i
       a[r][i] = static_cast<__bf16>(va);
       b[r][i] = static_cast<__bf16>(vb);
     }
-  f32x16 acc[4];
-  for (int j = 0; j < 4; ++j) acc[j] = f32x16{};
+  f32x4 acc[8];
+  for (int j = 0; j < 8; ++j) acc[j] = f32x4{};
   for (int32_t it = 0; it < iters; ++it) {
 #pragma unroll
     for (int j = 0; j < 16; ++j)
-      acc[j & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[j & 7], b[(3 * j) & 7], acc[j & 3], 0, 0, 0);
+      acc[j & 7] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j & 7], b[(3 * j) & 7], acc[j & 7], 0, 0, 0);
   }
   float s = 0.f;
-  for (int j = 0; j < 4; ++j)
-    for (int i = 0; i < 16; ++i) s += acc[j][i];
+  for (int j = 0; j < 8; ++j)
+    for (int i = 0; i < 4; ++i) s += acc[j][i];
   out[blockIdx.x * kProbeThreads + threadIdx.x] = s;
 }
 
@@ -66,7 +67,7 @@ extern "C" int sc_probe_mfma(int32_t random_operands, int32_t iters, void* out, 
   if (need == 0) return fail(SC_EDEVICE, "no device");
   if (out_bytes < need) return fail(SC_EINVAL, "probe output of %zu bytes, need %zu", out_bytes, need);
   const uint32_t blocks = (uint32_t)(need / (kProbeThreads * sizeof(float)));
-  if (flops) *flops = 2.0 * 32 * 32 * 16 * 16.0 * iters * blocks * (kProbeThreads / 64);
+  if (flops) *flops = 2.0 * 16 * 16 * 32 * 16.0 * iters * blocks * (kProbeThreads / 64);
   hipLaunchKernelGGL(mfma_probe_kernel, dim3(blocks), dim3(kProbeThreads), 0,
                      static_cast<hipStream_t>(stream), static_cast<float*>(out), iters,
                      random_operands);
