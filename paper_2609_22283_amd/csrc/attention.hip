@@ -764,7 +764,7 @@ static TailSplit tail_split(const sc_plan* p, const sc_cache* c) {
   const double mean_tiles = (double)tiles / std::max(n, 1);
   TailSplit ts;
   ts.bq = bq;
-  const int32_t slots = kAttnCUs * (BQ_MAX / bq);  // work-groups resident at once
+  const int32_t slots = kCUs * (BQ_MAX / bq);  // work-groups resident at once
   ts.tail = units % slots;
   ts.whole = units - ts.tail;
   ts.split = 1;

@@ -28,7 +28,6 @@ constexpr int G_NW = 8;               // waves per work-group, two per SIMD
 constexpr int G_THREADS = 64 * G_NW;
 constexpr int GROWS = GBM / G_NW;     // weight rows each wave copies per stage
 constexpr int G_TILE_BYTES = GBM * GBK * 2;  // 32 KB per operand per stage
-constexpr int kGemmCUs = 256;          // one work-group per CU
 
 // GELU_tanh(x) = 0.5 x (1 + tanh(u)) = x * sigmoid(2 u), u = sqrt(2/pi) (x + 0.044715 x^3),
 // evaluated as x / (1 + 2^(-2 u log2 e)).
@@ -326,7 +325,7 @@ static int gemm_tile_tokens(int32_t F, int32_t T) {
   for (const int bn : {256, 192, 128}) {
     const int64_t tiles = (int64_t)(F / GBM) * ((T + bn - 1) / bn);
     const double eff = bn == 256 ? 1.0 : bn == 192 ? 1.12 : 1.4;
-    const double cost = (double)((tiles + kGemmCUs - 1) / kGemmCUs) * bn / 256.0 * eff;
+    const double cost = (double)((tiles + kCUs - 1) / kCUs) * bn / 256.0 * eff;
     if (cost < best_cost - 1e-9) {
       best_cost = cost;
       best = bn;

@@ -74,6 +74,10 @@ int policy_check(const sc_policy* p);
 bool policy_selects(const sc_policy* p, int32_t c, int32_t j, int32_t r);
 int32_t policy_level(const sc_policy* p, int32_t c, int32_t j, int32_t r);
 
+// Compute units of the target GPU (MI355X): one launch round of
+// one-work-group-per-CU kernels.
+constexpr int32_t kCUs = 256;
+
 // Kernel launchers (device code lives in the .hip files).
 // Whether launch_attention supports the plan's shape (pack and plan sizes,
 // head_dim and page size of the dtype's kernel): SC_OK or SC_EUNSUPPORTED.
@@ -84,7 +88,6 @@ int launch_attention(const sc_plan* plan, const sc_cache* cache, int32_t layer,
 // Workspace of the bf16 attention for a plan (0 for fp32 caches and plans
 // whose units fill whole rounds of the CUs), and its bound over all plans
 // (at most kAttnMaxPieces partial results).
-constexpr int32_t kAttnCUs = 256;         // compute units of the target GPU
 constexpr int32_t kAttnMaxPieces = 1024;
 constexpr int32_t kAttnMinSplitTiles = 32;  // mean key tiles per unit below which nothing is cut
 size_t attention_workspace_bytes(const sc_plan* plan, const sc_cache* cache);
