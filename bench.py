@@ -516,7 +516,8 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=10,
+                    help="untimed steps first: the first ~6 launches run while the clock ramps")
     ap.add_argument("--workload", default="cfg4",
                     choices=["cfg4", "cfg4R", "cfg3", "cfg2", "cfg5", "kvstream"])
     ap.add_argument("--layers", type=int, default=30, help="cfg5: blocks in the stack")
