@@ -82,6 +82,14 @@ PACK = [(6, 0), (7, 1), (8, 2), (9, 3), (10, 4)]
 RESIDENT = [(c, 0) for c in range(6)]
 
 
+# bf16 roundings of a block output that the fp64 oracle does not make: the
+# plain block's seven, plus q and k rounded again after the qk-norm (1); for
+# cross-attention its RMSNorm output, query, cached condition K/V, attention
+# output and residual (5); with its norms the query and the condition keys
+# rounded again after them (2).
+ROUNDINGS = {"qk": 8, "cross": 12, "cross_norm": 14, "all": 15}
+
+
 @pytest.mark.parametrize("variant", ["qk", "cross", "cross_norm", "all"])
 def test_small_block_qk_norm_and_cross(variant):
     """qk-norm alone; cross-attention without and with its query/key norms;
@@ -101,7 +109,7 @@ def test_small_block_qk_norm_and_cross(variant):
     got = case.run()
     want, new_kv = case.oracle()
     for i in range(len(PACK)):
-        block_gate(got[i], want[i], f"{variant} node {PACK[i]}")
+        block_gate(got[i], want[i], f"{variant} node {PACK[i]}", ROUNDINGS[variant])
         k_got, v_got = read_pages(case.pool, SMALL, case.n_slots, case.cache.slots(PACK[i]))
         (block_gate if use_qk else bf16_gates)(k_got, new_kv[i][0], f"{variant} cached K")
         bf16_gates(v_got, new_kv[i][1], f"{variant} cached V")
@@ -116,7 +124,7 @@ def test_short_block_qk_norm_and_cross():
     got = case.run()
     want, _ = case.oracle()
     for i in range(len(PACK)):
-        block_gate(got[i], want[i], f"short node {PACK[i]}")
+        block_gate(got[i], want[i], f"short node {PACK[i]}", ROUNDINGS["all"])
 
 
 def test_wan_block_qk_norm_and_cross_sampled_rows():
@@ -130,4 +138,4 @@ def test_wan_block_qk_norm_and_cross_sampled_rows():
     rows = sample_rows(WAN.tokens_per_chunk, 24, seed=4)
     want, _ = case.oracle(rows=rows)
     for i in range(len(wl.pack)):
-        block_gate(got[i][rows], want[i], f"wan qk+cross node {wl.pack[i]}")
+        block_gate(got[i][rows], want[i], f"wan qk+cross node {wl.pack[i]}", ROUNDINGS["all"])
