@@ -278,6 +278,21 @@ def test_wan_block_sampled_rows(kind, pack, resident):
         block_gate(got[i][rows], want[i], f"wan {kind} node {pack[i]}")
 
 
+def test_wan_width_block_1800_tokens():
+    """Wan widths (hidden 1536, 12 heads, MLP 8960) over one 1800-token chunk
+    (one 15 x 120 frame) with one resident state: the MLP-up GEMM runs on
+    192-token tiles here (350 tiles, 2 rounds at 0.75 of a tile, against 280
+    tiles in 2 full rounds at 256), as do the QKV GEMM, and the out/down GEMMs
+    on 128-token tiles."""
+    import dataclasses
+    geo = dataclasses.replace(WAN, grid_h=15, grid_w=120, frames_per_chunk=1)
+    case = BlockCase(geo, "clean", [(1, 4)], [(0, 0)], seed=17)
+    got = case.run()
+    rows = sample_rows(geo.tokens_per_chunk, 32, seed=5)
+    want, _ = case.oracle(rows=rows)
+    block_gate(got[0][rows], want[0], "wan-width 1800-token node (1, 4)")
+
+
 def test_sampler_matches_oracle():
     torch = torch_mod()
     nodes = [(3, 0), (4, 1), (5, 2), (6, 3), (7, 4)]
