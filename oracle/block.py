@@ -2,8 +2,10 @@
 
 The paper fixes only the network's role (F_theta in Eq. 1, reading the
 context of each node through the visibility mask of Eq. 6).  The block form
-is the Wan-shaped reading used for the workload (parity unpinned against a
-real model; no trained weights exist here):
+is the Wan-shaped reading used for the workload (no trained weights exist
+here to compare a real model with; the reading itself is pinned by a block
+worked by hand at hidden 4, every intermediate listed, and by closed-form
+special cases):
 
     h  = RMSNorm(x)                          eps = 1e-6, unit gain
     q, k, v = h Wq^T, h Wk^T, h Wv^T          heads of d channels

@@ -1,9 +1,11 @@
 """3D rotary position embedding -- oracle, test infrastructure only.
 
 The paper does not define the positional encoding of its DiT; this is the
-reading used for the Wan-shaped workload (parity unpinned beyond the
-mathematical properties checked in the tests: identity at position 0,
-norm preservation, relative-position invariance of the logits).
+reading used for the Wan-shaped workload.  Pinned by mathematical
+properties (identity at position 0, norm preservation, relative-position
+invariance of the logits) and by a hand table of single-pair rotation angles
+for the 44/42/42 split (pairs 0, 1, 2 and the last of each axis); the choice
+of split and theta itself is the reading, not a statement of the paper.
 
 The head dimension d is split into three axis groups of d_t, d_h, d_w
 channels (44/42/42 for d = 128).  Channels are taken in interleaved pairs
