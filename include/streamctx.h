@@ -32,7 +32,7 @@
 extern "C" {
 #endif
 
-#define SC_ABI_VERSION 5
+#define SC_ABI_VERSION 6
 
 enum {
   SC_OK = 0,
@@ -197,7 +197,10 @@ int sc_plan_condition(sc_cache* cache, const sc_node* conditions, int32_t n, int
  * q, o: device [n_nodes * Nq, n_heads, head_dim] in the cache dtype, node i
  * at rows [i*Nq, (i+1)*Nq) with Nq = pages_per_chunk * tokens_per_page.
  * Every page must have been written at this layer by calls enqueued earlier
- * on the same stream.  ws: device scratch, 16-byte aligned, of at least
+ * on the same stream.  Limits of this build: at most 64 pack nodes and 800
+ * pages per plan (the page lists travel by value in the kernel arguments, so
+ * no per-round host-to-device copy is needed); larger plans fail with
+ * SC_EUNSUPPORTED before anything is launched.  ws: device scratch, 16-byte aligned, of at least
  * sc_attention_workspace_bytes(plan, cache) bytes (may be NULL when that is
  * 0, as for fp32 caches); the bf16 kernel splits long key ranges across
  * work-groups and merges their partial softmax sums there.  Its contents are
@@ -238,6 +241,12 @@ int sc_condition_append(sc_cache* cache, int32_t layer, sc_node state, const voi
  * [n_nodes * Nq, hidden], updated in place.  ws: device workspace of at least
  * sc_block_workspace_bytes() bytes.  The block form is the Wan-shaped
  * reading of the workload (the paper does not define the network).
+ * Limits: hidden and mlp multiples of 256, head_dim 128, at most 64 pack
+ * nodes owning at most 256 page slots (the QKV epilogue's node table), and
+ * the attention limits above; all are checked before the first launch.
+ * The pack's states are marked written at this layer only once every launch
+ * has been enqueued: after an error they are still unwritten (their pages
+ * and x hold partial results) and the block can be run again.
  *
  * Noise-level conditioning (optional, mod != NULL): the denoiser of Eq. 1
  * depends on the node's level j.  mod is a device fp32 table
@@ -285,6 +294,15 @@ typedef struct {
   const sc_cross_attn* cross;  /* or NULL */
 } sc_block_weights;
 size_t sc_block_workspace_bytes(const sc_block_weights* w, int32_t n_tokens);
+/* For inspection of a block's intermediates: byte offsets inside the
+ * workspace of the rotated queries q and the self-attention output o of the
+ * last sc_block_forward that used it, both bf16 [n_tokens][hidden]
+ * token-major (node i at rows [i*Nq, (i+1)*Nq)).  They hold those values
+ * once the block's work on the stream has completed, until the workspace
+ * is used again; with cross-attention they hold its query and output
+ * instead.  Errors: SC_EINVAL (null pointer, n_tokens < 1). */
+int sc_block_workspace_views(const sc_block_weights* w, int32_t n_tokens, size_t* q_offset,
+                             size_t* o_offset);
 int sc_block_forward(const sc_block_weights* w, sc_cache* cache, int32_t layer,
                      const sc_plan* plan, void* x, const sc_rope* rope, void* ws,
                      size_t ws_bytes, sc_stream stream);
@@ -313,6 +331,14 @@ int sc_pipeline_rounds(int32_t K, int32_t B, int32_t refresh);
 int sc_pipeline_round_nodes(int32_t K, int32_t B, int32_t refresh, int32_t n, sc_node* out,
                             int32_t* n_out);
 
+/* Fully serial execution, Eq. 2: one node per forward, all updates of chunk
+ * c (levels K, K-1, .., 1, then the refresh (c, 0) when refresh != 0)
+ * before chunk c + 1.  sc_serial_steps returns the number of forwards
+ * (B*K, or B*(K+1) with the refresh); sc_serial_step_node writes the node of
+ * forward n.  Errors: SC_EINVAL (K < 1, B < 1, n outside the schedule). */
+int sc_serial_steps(int32_t K, int32_t B, int32_t refresh);
+int sc_serial_step_node(int32_t K, int32_t B, int32_t refresh, int32_t n, sc_node* out);
+
 /* Releases every cached state that none of the given future nodes reads
  * under the policy (Eq. 4-5 offsets and levels), keeping only what the rest
  * of the schedule needs ("earlier states are retained", Sec. 3.3).  Returns
@@ -322,38 +348,14 @@ int sc_cache_release_unread(sc_cache* cache, const sc_policy* policy, const sc_n
 
 /* The network F_theta of Eq. 1 as a stack of n_layers blocks over one pack:
  * sc_block_forward for layer 0 .. n_layers-1 in order (layers[l] holds the
- * weights of layer l), x updated in place, one plan for every layer. */
+ * weights of layer l), x updated in place, one plan for every layer.  On an
+ * error in layer l, the pack's states are left unwritten in every layer
+ * (x holds a partial result): the caller restores x and runs it again. */
 int sc_stack_forward(const sc_block_weights* layers, int32_t n_layers, sc_cache* cache,
                      const sc_plan* plan, void* x, const sc_rope* rope, void* ws, size_t ws_bytes,
                      sc_stream stream);
 
-/* ---- Kernel timing (measurement support) ------------------------------
- * While enabled, every kernel the library launches is bracketed by two HIP
- * events recorded on the launch stream.  sc_timer_read synchronises those
- * events and returns, for one kernel kind, the number of launches and the
- * summed elapsed milliseconds since the timer was last enabled.  Kinds:
- * "attention", "gemm_qkv", "gemm_out", "gemm_up", "gemm_down", "rmsnorm",
- * "append", "sampler", "attention_combine" (the merge of split key ranges;
- * "attention" is the main kernel alone), "qk_norm" (the per-token scaling of
- * qk-norm and of the normalised condition queries and keys),
- * "cross_attention", "gemm_cross_q", "gemm_cross_out", "gemm_condition"
- * (the projections of sc_condition_append).  Enabling clears earlier records.  Events are created
- * lazily and reused; the cost is two event records per launch. */
-int sc_timer_enable(int on);
-int sc_timer_read(const char* kind, int32_t* launches, double* total_ms);
-
-/* ---- Matrix-core ceiling probe (measurement support) ------------------
- * Launches one kernel on `stream` that issues only 16x16x32 bf16 MFMAs from
- * registers (two 8-wave work-groups per CU, `iters` rounds of 16 MFMAs per
- * wave) and sets *flops to the work it performs; the caller times it with
- * its own events.  random_operands != 0 fills the operands with random bf16
- * values, else with constants; the two rates show how much the
- * power-limited clock depends on the data.  out: device scratch of at least
- * sc_probe_mfma_out_bytes() bytes (one float per thread, written so the
- * work is not optimised away).  Errors: SC_EINVAL, SC_EDEVICE. */
-size_t sc_probe_mfma_out_bytes(void);
-int sc_probe_mfma(int32_t random_operands, int32_t iters, void* out, size_t out_bytes,
-                  double* flops, sc_stream stream);
+/* Measurement support (kernel timer, matrix-core probe): streamctx_measure.h */
 
 #ifdef __cplusplus
 }

@@ -155,7 +155,8 @@ def cross_attention(x: np.ndarray, cross: Dict[str, np.ndarray], shp: BlockShape
 def block_forward(sel, x_of: Callable[[int], np.ndarray], weights: Dict[str, np.ndarray],
                   resident_kv: Callable[[Tuple[int, int]], Tuple[np.ndarray, np.ndarray]],
                   shp: BlockShape, rows: Optional[Sequence[int]] = None,
-                  mod: Optional[np.ndarray] = None, qk_norm=None, cross=None):
+                  mod: Optional[np.ndarray] = None, qk_norm=None, cross=None,
+                  trace: Optional[dict] = None):
     """Run one block for every node of ``sel``.
 
     x_of(i) gives node i's input [Nq, hidden].  resident_kv(state) gives the
@@ -166,6 +167,10 @@ def block_forward(sel, x_of: Callable[[int], np.ndarray], weights: Dict[str, np.
     ``qk_norm`` the optional gains (g_q, g_k); ``cross`` the optional
     cross-attention (see cross_attention), one for every node or a function
     of the node (c, j) (nodes of one pack may read different conditions).
+    With ``trace`` (a dict) the intermediates of each node's output rows are
+    stored in it: trace[i] = {"q": rotated queries [rows, H, d], "o": the
+    attention output [rows, H, d], "a": o Wo^T [rows, hidden] (before any
+    gate)}.
     Returns ({i: y_i}, {i: (k_i, v_i)}).
     """
     def mod_row(j):
@@ -192,6 +197,8 @@ def block_forward(sel, x_of: Callable[[int], np.ndarray], weights: Dict[str, np.
         q = project_q(x_of(i), c, weights["w_qkv"], shp, rows, m, g_q)
         o = node_attention(q, sel.segments(i), kv_of, scale).reshape(q.shape[0], -1)
         a = o @ np.asarray(weights["w_o"], dtype=np.float64).T
+        if trace is not None:
+            trace[i] = {"q": q, "o": o.reshape(q.shape), "a": a}
         x1 = x + (a if m is None else m[2] * a)
         if cross is not None:
             x1 = x1 + cross_attention(x1, cross((c, j)) if callable(cross) else cross, shp)

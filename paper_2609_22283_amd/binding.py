@@ -24,6 +24,7 @@ __all__ = [
     "Selection", "Cache", "Plan", "Rope", "BlockWeights", "CrossAttn",
     "sc_plan_condition", "sc_condition_workspace_bytes", "sc_condition_append",
     "sc_pipeline_rounds", "sc_pipeline_round_nodes", "sc_cache_release_unread", "sc_stack_forward",
+    "sc_serial_steps", "sc_serial_step_node", "sc_block_workspace_views",
 ]
 
 SC_OK, SC_EINVAL, SC_EUNAVAILABLE, SC_ECAPACITY = 0, -1, -2, -3
@@ -32,7 +33,7 @@ SC_POLICY_CLEAN, SC_POLICY_SAME, SC_POLICY_PROG, SC_POLICY_TABLE = 0, 1, 2, 3
 SC_DTYPE_BF16, SC_DTYPE_F32 = 0, 1
 POLICY_KINDS = {"clean": 0, "same": 1, "prog": 2, "table": 3}
 
-# Every function include/streamctx.h declares (checked by the CPU tests).
+# Every function the headers under include/ declare (checked by the CPU tests).
 EXPORTED_SYMBOLS = [
     "sc_abi_version", "sc_last_error", "sc_status_name",
     "sc_selection_build", "sc_selection_get", "sc_visibility_get", "sc_selection_free",
@@ -45,6 +46,7 @@ EXPORTED_SYMBOLS = [
     "sc_block_workspace_bytes", "sc_block_forward", "sc_sampler_step",
     "sc_timer_enable", "sc_timer_read", "sc_probe_mfma_out_bytes", "sc_probe_mfma",
     "sc_pipeline_rounds", "sc_pipeline_round_nodes", "sc_cache_release_unread", "sc_stack_forward",
+    "sc_serial_steps", "sc_serial_step_node", "sc_block_workspace_views",
 ]
 
 # The library and PyTorch must share one HIP runtime: torch ships its own
@@ -153,9 +155,13 @@ _SIG = {
     "sc_cache_release_unread": (C.c_int, [_P, C.POINTER(sc_policy), C.POINTER(sc_node), C.c_int32]),
     "sc_stack_forward": (C.c_int, [C.POINTER(sc_block_weights), C.c_int32, _P, _P, _P,
                                    C.POINTER(sc_rope), _P, C.c_size_t, _P]),
+    "sc_serial_steps": (C.c_int, [C.c_int32, C.c_int32, C.c_int32]),
+    "sc_serial_step_node": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.POINTER(sc_node)]),
+    "sc_block_workspace_views": (C.c_int, [C.POINTER(sc_block_weights), C.c_int32, C.POINTER(C.c_size_t),
+                                           C.POINTER(C.c_size_t)]),
 }
 # ABI version this binding marshals for (SC_ABI_VERSION of the header)
-ABI_VERSION = 5
+ABI_VERSION = 6
 if not hasattr(lib, "sc_abi_version") or lib.sc_abi_version() != ABI_VERSION:
     raise ImportError(f"{library_path} does not implement ABI version {ABI_VERSION}; rebuild it "
                       "(__graft_entry__.build())")
@@ -450,6 +456,14 @@ def sc_block_forward(w: BlockWeights, cache: Cache, layer: int, plan: Plan, x, r
                                 ws_bytes, _stream(stream)))
 
 
+def sc_block_workspace_views(w: BlockWeights, n_tokens: int) -> Tuple[int, int]:
+    """Byte offsets (q, o) of the last block's rotated queries and attention
+    output inside its workspace (bf16 [n_tokens, hidden] each)."""
+    q, o = C.c_size_t(), C.c_size_t()
+    _check(lib.sc_block_workspace_views(C.byref(w.struct), n_tokens, C.byref(q), C.byref(o)))
+    return q.value, o.value
+
+
 def sc_sampler_step(nodes, t: Sequence[float], K: int, out, y, noise, elems_per_node: int,
                     stream=None) -> None:
     arr = (sc_node * max(1, len(nodes)))(*[sc_node(int(c), int(j)) for c, j in nodes])
@@ -492,6 +506,17 @@ def sc_pipeline_round_nodes(K: int, B: int, refresh: bool, n: int):
     m = C.c_int32()
     _check(lib.sc_pipeline_round_nodes(K, B, 1 if refresh else 0, n, buf, C.byref(m)))
     return [(buf[i].chunk, buf[i].level) for i in range(m.value)]
+
+
+def sc_serial_steps(K: int, B: int, refresh: bool) -> int:
+    return _check(lib.sc_serial_steps(K, B, 1 if refresh else 0))
+
+
+def sc_serial_step_node(K: int, B: int, refresh: bool, n: int) -> Tuple[int, int]:
+    """Node of forward n of fully serial execution (Eq. 2)."""
+    nd = sc_node()
+    _check(lib.sc_serial_step_node(K, B, 1 if refresh else 0, n, C.byref(nd)))
+    return nd.chunk, nd.level
 
 
 def sc_cache_release_unread(cache: "Cache", kind, K, W, future, phi_table=None, r_mask=None,

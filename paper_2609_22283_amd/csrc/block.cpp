@@ -27,6 +27,15 @@ extern "C" size_t sc_block_workspace_bytes(const sc_block_weights* w, int32_t n_
          align256(T * (2 * w->hidden / 128) * 4);
 }
 
+extern "C" int sc_block_workspace_views(const sc_block_weights* w, int32_t n_tokens, size_t* q_offset,
+                                        size_t* o_offset) {
+  if (!w || n_tokens <= 0 || !q_offset || !o_offset) return fail(SC_EINVAL, "null argument or no tokens");
+  const size_t act = align256((size_t)n_tokens * w->hidden * 2);
+  *q_offset = act;
+  *o_offset = 2 * act;
+  return SC_OK;
+}
+
 static bool misaligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) & 15; }
 
 // Checks of the optional cross-attention against the block's pack plan.
@@ -59,6 +68,10 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
                 w->head_dim, w->hidden);
   if (p->cache != c) return fail(SC_EINVAL, "plan was built for another cache");
   if (layer < 0 || layer >= d.n_layers) return fail(SC_EINVAL, "layer %d out of range", layer);
+  // every projection's shape is checked before the first launch
+  if (w->hidden % 256 || w->mlp <= 0 || w->mlp % 256)
+    return fail(SC_EUNSUPPORTED, "block GEMMs need hidden and mlp multiples of 256 (got %d, %d)", w->hidden,
+                w->mlp);
   const int32_t n = (int32_t)p->nodes.size();
   if (n == 0) return SC_OK;
   if (n > kGemmMaxNodes || n * d.pages_per_chunk > kGemmMaxNodePages)
@@ -180,8 +193,6 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
     std::memcpy(ns.node_slot, ep.node_slot, sizeof ns.node_slot);
     if ((rc = launch_norm_scale(T, ns, stream)) != SC_OK) return rc;
   }
-  for (int32_t i = 0; i < n; ++i)
-    c->states.at(StateKey(p->nodes[i].chunk, p->nodes[i].level)).written[layer] = 1;
   if ((rc = launch_attention(p, c, layer, qb, ob, 1.0f / std::sqrt((float)d.head_dim), attn_ws,
                              attention_workspace_bound(), stream)) != SC_OK)
     return rc;
@@ -247,6 +258,10 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
   e4.gate_row = 5;  // gate_m
   if ((rc = launch_gemm(EPI_RESIDUAL, TK_GEMM_DOWN, static_cast<const uint16_t*>(w->w_down), ub, D, T, w->mlp, e4, stream)) != SC_OK)
     return rc;
+  // only now are the pack's K/V of this layer complete: a failed call leaves
+  // them unwritten, so the caller can run the block again
+  for (int32_t i = 0; i < n; ++i)
+    c->states.at(StateKey(p->nodes[i].chunk, p->nodes[i].level)).written[layer] = 1;
   return SC_OK;
 }
 

@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "../../include/streamctx.h"
+#include "../../include/streamctx_measure.h"
 
 namespace sc {
 

@@ -26,6 +26,23 @@ extern "C" int sc_pipeline_round_nodes(int32_t K, int32_t B, int32_t refresh, in
   return SC_OK;
 }
 
+extern "C" int sc_serial_steps(int32_t K, int32_t B, int32_t refresh) {
+  if (K < 1 || B < 1) return fail(SC_EINVAL, "need K >= 1 and B >= 1");
+  return B * (refresh ? K + 1 : K);
+}
+
+extern "C" int sc_serial_step_node(int32_t K, int32_t B, int32_t refresh, int32_t n, sc_node* out) {
+  if (!out) return fail(SC_EINVAL, "null argument");
+  const int steps = sc_serial_steps(K, B, refresh);
+  if (steps < 0) return steps;
+  if (n < 0 || n >= steps) return fail(SC_EINVAL, "step %d outside [0, %d)", n, steps);
+  // chunk by chunk; within a chunk the levels K .. 1, then the refresh (c, 0)
+  const int32_t per = refresh ? K + 1 : K;
+  out->chunk = n / per;
+  out->level = K - n % per;
+  return SC_OK;
+}
+
 extern "C" int sc_cache_release_unread(sc_cache* c, const sc_policy* p, const sc_node* future,
                                        int32_t n_future) {
   if (!c || !p || (n_future > 0 && !future)) return fail(SC_EINVAL, "null argument");
@@ -57,7 +74,16 @@ extern "C" int sc_stack_forward(const sc_block_weights* layers, int32_t n_layers
     return fail(SC_EINVAL, "%d layers but the cache holds %d", n_layers, cache ? cache->d.n_layers : 0);
   for (int32_t l = 0; l < n_layers; ++l) {
     int rc = sc_block_forward(&layers[l], cache, l, plan, x, rope, ws, ws_bytes, stream);
-    if (rc != SC_OK) return rc;
+    if (rc != SC_OK) {
+      // layers before l are complete, but the forward as a whole is not:
+      // mark none of the pack's layers written so the caller can rerun it
+      for (int32_t e = 0; e < l; ++e)
+        for (const sc_node& nd : plan->nodes) {
+          auto it = cache->states.find(StateKey(nd.chunk, nd.level));
+          if (it != cache->states.end()) it->second.written[e] = 0;
+        }
+      return rc;
+    }
   }
   return SC_OK;
 }

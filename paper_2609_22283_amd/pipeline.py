@@ -54,12 +54,19 @@ class StackPipeline:
         return [sc.sc_pipeline_round_nodes(self.K, self.B, self.refresh, r) for r in range(n)]
 
     def serial_nodes(self) -> List[Tuple[int, int]]:
-        lo = 0 if self.refresh else 1
-        return [(c, j) for c in range(self.B) for j in range(self.K, lo - 1, -1)]
+        n = sc.sc_serial_steps(self.K, self.B, self.refresh)
+        return [sc.sc_serial_step_node(self.K, self.B, self.refresh, i) for i in range(n)]
 
     # ------------------------------------------------------------ forwards
-    def forward(self, nodes: Sequence[Tuple[int, int]]) -> None:
-        """One packed forward of ``nodes`` through every layer, then the sampler."""
+    def forward(self, nodes: Sequence[Tuple[int, int]], layer_hook=None) -> None:
+        """One packed forward of ``nodes`` through every layer, then the sampler.
+
+        ``layer_hook(layer, phase, x, plan, layers)``, when given, observes the
+        forward layer by layer: it is called with phase "in" before and "out"
+        after each layer's block is enqueued (x: the pack's activations,
+        layers: the block weights in use).  The layers then run one
+        sc_block_forward call each instead of one sc_stack_forward call;
+        the work is the same."""
         n = self.n_tok
         sel = sc.sc_selection_build(self.policy, self.K, self.W, nodes)
         plan = sc.sc_plan_build(sel, self.cache)
@@ -73,8 +80,15 @@ class StackPipeline:
             plan_c = sc.sc_plan_condition(cond["cache"], [of(c) for c, _ in nodes], n)
             layers = [w.with_cross(sc.CrossAttn(wq, wo, cond["cache"], plan_c, q_norm=qn))
                       for w, (wq, wo, qn) in zip(self.layers, cond["cross"])]
-        sc.sc_stack_forward(layers, self.cache, plan, x, self.rope, self.ws, self.ws_bytes,
-                            self.stream)
+        if layer_hook is None:
+            sc.sc_stack_forward(layers, self.cache, plan, x, self.rope, self.ws, self.ws_bytes,
+                                self.stream)
+        else:
+            for l, w in enumerate(layers):
+                layer_hook(l, "in", x, plan, layers)
+                sc.sc_block_forward(w, self.cache, l, plan, x, self.rope, self.ws, self.ws_bytes,
+                                    self.stream)
+                layer_hook(l, "out", x, plan, layers)
         for i, (c, j) in enumerate(nodes):
             if j >= 1:
                 sc.sc_sampler_step([(c, j)], self.t_sched, self.K, self.xs[c],
@@ -82,12 +96,15 @@ class StackPipeline:
                                    n * self.hidden, self.stream)
 
     def run(self, mode: str = "packed", time_rounds: bool = False,
-            kernel_timer_rounds: Tuple[int, int] = None) -> List[float]:
+            kernel_timer_rounds: Tuple[int, int] = None, layer_hooks=None,
+            stop_after: int = None) -> List[float]:
         """Run the whole schedule; returns per-round (or per-node for serial)
         milliseconds when ``time_rounds``.  With ``kernel_timer_rounds =
         (first, last)`` the library's kernel timer records the launches of
         those rounds; ``self.kernel_times`` then maps kernel kinds to
-        (launches, total ms)."""
+        (launches, total ms).  ``layer_hooks`` maps a round (a forward in
+        serial mode) to a layer hook of its forwards (see ``forward``);
+        ``stop_after`` ends the run after that round."""
         torch = self.torch
         times = []
         self.kernel_times = {}
@@ -107,7 +124,7 @@ class StackPipeline:
                 e1 = torch.cuda.Event(enable_timing=True)
                 e0.record()
             for nodes in group:
-                self.forward(nodes)
+                self.forward(nodes, (layer_hooks or {}).get(g))
                 done += len(nodes)
             sc.sc_cache_release_unread(self.cache, self.policy, self.K, self.W, flat[done:])
             if time_rounds:
@@ -118,6 +135,8 @@ class StackPipeline:
                              "gemm_down", "qk_norm", "cross_attention", "gemm_cross_q", "gemm_cross_out"):
                     self.kernel_times[kind] = sc.sc_timer_read(kind)
                 sc.sc_timer_enable(False)
+            if stop_after is not None and g == stop_after:
+                break
         if time_rounds:
             torch.cuda.synchronize()
             return [a.elapsed_time(b) for a, b in times]

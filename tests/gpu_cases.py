@@ -38,6 +38,12 @@ def to_device(x: np.ndarray, dtype: int):
     return t, x.astype(np.float64)
 
 
+def bits_to_device(bits: np.ndarray):
+    """bf16 bit patterns (uint16 numpy) -> a bf16 device tensor."""
+    torch = torch_mod()
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+
+
 def from_device(t) -> np.ndarray:
     torch = torch_mod()
     if t.dtype == torch.bfloat16:

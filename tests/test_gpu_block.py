@@ -17,16 +17,13 @@ import numpy as np
 import pytest
 
 import paper_2609_22283_amd as sc
-from oracle.block import BlockShape, block_forward, project_kv
 from oracle.pipeline import sampler_step
-from oracle.policy import policy as oracle_policy
-from oracle.policy import select
 from oracle.rope import chunk_positions, rope
-from synth import (TAG_K, TAG_NOISE, TAG_V, TAG_W_DOWN, TAG_W_O, TAG_W_QKV, TAG_W_UP, TAG_X,
-                   normal, normal_parallel)
-from synth.configs import SHORT, SMALL, WAN, cfg4_prog
+from synth import TAG_K, TAG_NOISE, TAG_V, TAG_X, normal
+from synth.configs import SHORT, SMALL, WAN, cfg3_same, cfg4_prog
 
-from gpu_cases import bf16_gates, from_device, sample_rows, to_device, torch_mod
+from block_inputs import X_SMALL, BlockInputs, branch_gate, oracle_traces, planted_must_fail
+from gpu_cases import bf16_gates, bits_to_device, from_device, sample_rows, to_device, torch_mod
 
 pytestmark = pytest.mark.gpu
 
@@ -82,20 +79,6 @@ def test_append_with_rope_matches_oracle():
     assert e.value.code == sc.SC_EEXIST
 
 
-def _weights(geo, layer, seed):
-    D, M = geo.hidden, geo.mlp
-    big = D * M > 1 << 22
-    gen = normal_parallel if big else normal
-    w = {"w_qkv": gen((3 * D, D), (seed, TAG_W_QKV, layer), 0.02),
-         "w_o": gen((D, D), (seed, TAG_W_O, layer), 0.02),
-         "w_up": gen((M, D), (seed, TAG_W_UP, layer), 0.02),
-         "w_down": gen((D, M), (seed, TAG_W_DOWN, layer), 0.02)}
-    dev, exact = {}, {}
-    for k, v in w.items():
-        dev[k], exact[k] = to_device(v, sc.SC_DTYPE_BF16)
-    return dev, exact
-
-
 def _mod_table(geo, seed):
     """Random per-level modulation [K+1][6][hidden] fp32 (gates around 1)."""
     m = np.stack([np.stack([normal((geo.hidden,), (seed, 30, j, r), 0.2) for r in range(6)])
@@ -106,15 +89,20 @@ def _mod_table(geo, seed):
 
 
 class BlockCase:
-    """One block over a pack.  Options: ``mod`` (host fp32 modulation table),
-    ``qk`` (host fp32 qk-norm gains [2][hidden]), ``cross`` (a ConditionCase
-    whose condition 0 every node reads)."""
+    """One block over a pack, on the inputs of ``BlockInputs`` (the same
+    bf16 values the oracle reads).  Options: ``mod`` (host fp32 modulation
+    table), ``qk`` (host fp32 qk-norm gains [2][hidden]), ``cross`` (a
+    ConditionCase whose condition 0 every node reads), ``x_scale`` and
+    ``zero_down`` (the attention-branch case: x scaled by a power of two and
+    w_down = 0)."""
 
-    def __init__(self, geo, kind, pack, resident, seed=0, mod=None, qk=None, cross=None):
+    def __init__(self, geo, kind, pack, resident, seed=0, mod=None, qk=None, cross=None, x_scale=1.0,
+                 zero_down=False):
         torch = torch_mod()
+        self.inp = BlockInputs(geo, kind, pack, resident, seed, x_scale, zero_down)
         self.mod = mod                                   # host fp32 table or None
         self.qk, self.cross = qk, cross
-        self.geo, self.kind, self.pack = geo, kind, pack
+        self.geo, self.kind, self.pack = geo, kind, list(pack)
         ppc, tpp = geo.frames_per_chunk, geo.tokens_per_page
         n_slots = (len(resident) + len(pack) + 2) * ppc
         nbytes = sc.sc_cache_pool_bytes(1, geo.heads, geo.head_dim, tpp, ppc, n_slots)
@@ -122,37 +110,30 @@ class BlockCase:
         self.n_slots = n_slots
         self.cache = sc.sc_cache_create(self.pool, 1, geo.heads, geo.head_dim, tpp, ppc, n_slots)
         self.rope = make_rope(geo)
-        big = geo.tokens_per_chunk * geo.hidden > 1 << 20
-        gen = normal_parallel if big else normal
-        shape = (geo.tokens_per_chunk, geo.heads, geo.head_dim)
-        self.res_kv, keep = {}, []
-        for st in resident:
-            kd, kv = to_device(gen(shape, (seed, TAG_K) + st), sc.SC_DTYPE_BF16)
-            vd, vv = to_device(gen(shape, (seed, TAG_V) + st), sc.SC_DTYPE_BF16)
+        keep = []
+        for st in resident:                              # K rotated by the cache on append
+            kd, vd = (bits_to_device(b) for b in self.inp.res_bits[tuple(st)])
             self.cache.append(0, st, kd, vd, rope=self.rope)
-            pos = chunk_positions(st[0], ppc, geo.grid_h, geo.grid_w)
-            self.res_kv[st] = (rope(kv, pos, geo.rope_dims, geo.theta), vv)
             keep += [kd, vd]
         torch.cuda.synchronize()
         del keep
+        self.res_kv = self.inp.res_kv
         self.sel = sc.sc_selection_build(kind, geo.K, geo.W, pack)
         self.plan = sc.sc_plan_build(self.sel, self.cache)
-        xs = [gen((geo.tokens_per_chunk, geo.hidden), (seed, TAG_X) + st) for st in pack]
-        self.x_dev, xv = to_device(np.concatenate(xs), sc.SC_DTYPE_BF16)
-        n = geo.tokens_per_chunk
-        self.x = [xv[i * n:(i + 1) * n] for i in range(len(pack))]
-        self.w_dev, self.w = _weights(geo, 0, seed)
+        self.x_dev = bits_to_device(self.inp.x_bits)
+        self.x = self.inp.x
+        self.w_dev = {k: bits_to_device(v) for k, v in self.inp.w_bits.items()}
+        self.w = self.inp.w
         self.mod_dev = None if mod is None else torch.from_numpy(mod).cuda()
         self.qk_dev = None if qk is None else torch.from_numpy(np.ascontiguousarray(qk)).cuda()
         ca = None if cross is None else cross.cross_attn(len(pack), geo.tokens_per_chunk)
         self.bw = sc.BlockWeights(geo.hidden, geo.heads, geo.head_dim, geo.mlp, self.w_dev["w_qkv"],
                                   self.w_dev["w_o"], self.w_dev["w_up"], self.w_dev["w_down"],
                                   mod=self.mod_dev, qk_norm=self.qk_dev, cross=ca)
-        T = len(pack) * n
-        self.ws_bytes = sc.sc_block_workspace_bytes(self.bw, T)
+        self.T = len(pack) * geo.tokens_per_chunk
+        self.ws_bytes = sc.sc_block_workspace_bytes(self.bw, self.T)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device="cuda")
-        self.shape = BlockShape(geo.hidden, geo.heads, geo.head_dim, geo.mlp, geo.frames_per_chunk,
-                                geo.grid_h, geo.grid_w, geo.rope_dims, geo.theta)
+        self.shape = self.inp.shape
 
     def run(self):
         torch = torch_mod()
@@ -163,12 +144,25 @@ class BlockCase:
         n = self.geo.tokens_per_chunk
         return [out[i * n:(i + 1) * n] for i in range(len(self.pack))]
 
-    def oracle(self, rows=None):
-        sel = select(oracle_policy(self.kind, self.geo.K, self.geo.W), self.pack)
+    def views(self):
+        """The block's rotated q and attention output o from its workspace,
+        per node, as [Nq, H, d] fp64 (after run())."""
+        qo, oo = sc.sc_block_workspace_views(self.bw, self.T)
+        g, n = self.geo, self.geo.tokens_per_chunk
+        out = []
+        for off in (qo, oo):
+            t = self.ws[off:off + self.T * g.hidden * 2].view(torch_mod().bfloat16)
+            a = from_device(t).reshape(len(self.pack), n, g.heads, g.head_dim)
+            out.append([a[i] for i in range(len(self.pack))])
+        return out
+
+    def oracle_options(self):
         qk = None if self.qk is None else tuple(self.qk.astype(np.float64))
         cross = None if self.cross is None else self.cross.oracle_dict(0)
-        return block_forward(sel, lambda i: self.x[i], self.w, self.res_kv.__getitem__, self.shape,
-                             rows=rows, mod=self.mod, qk_norm=qk, cross=cross)
+        return {"mod": self.mod, "qk_norm": qk, "cross": cross}
+
+    def oracle(self, rows=None, trace=None):
+        return self.inp.oracle(rows, trace, **self.oracle_options())
 
 
 def block_gate(got, want, what, roundings=7):
@@ -257,25 +251,129 @@ def test_block_rejects_oversized_pack():
     assert e.value.code == sc.SC_EUNSUPPORTED
 
 
-# Wan-shaped packs of 4, 5 and 1 nodes (T = 18720, 23400, 4680 tokens).
+def check_branches(case, got, rows, what, options=None, small_x=False):
+    """The block's branches against the oracle's trace of the same inputs:
+    the rotated q and attention output o read from the workspace, and for
+    the small-x case (w_down = 0) the attention branch y - x (gated by
+    gate_a when modulated); the pack's K/V written into the cache.  The
+    oracle with each planted mistake must fail the same gates (checked on
+    the CPU, on these inputs).  Returns the worst error/limit ratio."""
+    tr = oracle_traces(case.inp, rows, **(options or {}))
+    planted_must_fail(tr)
+    q_got, o_got = case.views()
+    sel = slice(None) if rows is None else rows
+    worst = 0.0
+    for i, node in enumerate(case.pack):
+        t = tr["exact"][i]
+        worst = max(worst, branch_gate(q_got[i][sel], t["q"], f"{what} node {node}: q"))
+        worst = max(worst, branch_gate(o_got[i][sel], t["o"], f"{what} node {node}: o"))
+        if small_x:
+            a = t["a"]
+            if case.mod is not None:
+                a = case.mod[node[1], 2] * a
+            worst = max(worst, branch_gate(got[i][sel] - case.x[i][sel], a,
+                                           f"{what} node {node}: y - x (attention branch)"))
+        else:
+            block_gate(got[i][sel], tr["y"][i], f"{what} node {node}: block output")
+        k_got, v_got = read_pages(case.pool, case.geo, case.n_slots, case.cache.slots(node))
+        worst = max(worst, branch_gate(k_got[sel], tr["kv"][i][0][sel], f"{what} node {node}: cached K"))
+        worst = max(worst, branch_gate(v_got[sel], tr["kv"][i][1][sel], f"{what} node {node}: cached V"))
+    return worst
+
+
+@pytest.mark.parametrize("small_x", [False, True], ids=["x", "small-x"])
+@pytest.mark.parametrize("kind,pack,resident", SMALL_BLOCK_PACKS, ids=["prog4", "prog5", "same", "clean"])
+def test_small_block_branches(kind, pack, resident, small_x):
+    """q, o, the attention branch and the cached K/V at small shapes, every
+    row (Eq. 6 through the block: the in-pack pages written by the QKV
+    epilogue are read by the attention in the same forward)."""
+    case = BlockCase(SMALL, kind, pack, resident, seed=11, x_scale=X_SMALL if small_x else 1.0,
+                     zero_down=small_x)
+    got = case.run()
+    check_branches(case, got, None, f"small {kind}", small_x=small_x)
+
+
+@pytest.mark.parametrize("use_qk", [False, True], ids=["mod", "mod+qk-norm"])
+def test_small_block_branches_modulated(use_qk):
+    """The attention branch with level modulation (its gate_a) and qk-norm
+    (q and k normalised over the hidden width before RoPE)."""
+    from gpu_cases import gains
+    qk = np.stack([gains(SMALL.hidden, (18, 45, 0)), gains(SMALL.hidden, (18, 45, 1))]) if use_qk else None
+    case = BlockCase(SMALL, *SMALL_BLOCK_PACKS[1], seed=18, mod=_mod_table(SMALL, 18), qk=qk,
+                     x_scale=X_SMALL, zero_down=True)
+    got = case.run()
+    check_branches(case, got, None, "small modulated", case.oracle_options(), small_x=True)
+
+
+def test_block_error_leaves_pack_unwritten():
+    """A block refused before its launches (an MLP width the GEMMs do not
+    support) leaves the pack unwritten; a two-layer stack whose second layer
+    is refused leaves the first layer unwritten too, and runs again once the
+    weights are fixed."""
+    torch = torch_mod()
+    geo, (kind, pack, resident) = SMALL, SMALL_BLOCK_PACKS[0]
+    case = BlockCase(geo, kind, pack, resident, seed=19)
+    w = case.w_dev
+    bad = sc.BlockWeights(geo.hidden, geo.heads, geo.head_dim, 320, w["w_qkv"], w["w_o"], w["w_up"],
+                          w["w_down"])
+    with pytest.raises(sc.ScError) as e:
+        sc.sc_block_forward(bad, case.cache, 0, case.plan, case.x_dev, case.rope, case.ws, case.ws_bytes)
+    assert e.value.code == sc.SC_EUNSUPPORTED
+    assert not any(case.cache.contains(st, 0) for st in pack)
+    # two layers: the first runs, the second is refused
+    ppc, tpp = geo.frames_per_chunk, geo.tokens_per_page
+    n_slots = (len(resident) + len(pack) + 2) * ppc
+    pool = torch.full((sc.sc_cache_pool_bytes(2, geo.heads, geo.head_dim, tpp, ppc, n_slots),), 0xFF,
+                      dtype=torch.uint8, device="cuda")
+    cache = sc.sc_cache_create(pool, 2, geo.heads, geo.head_dim, tpp, ppc, n_slots)
+    for layer in range(2):
+        for st in resident:
+            kd, vd = (bits_to_device(b) for b in case.inp.res_bits[tuple(st)])
+            cache.append(layer, st, kd, vd, rope=case.rope)
+    plan = sc.sc_plan_build(sc.sc_selection_build(kind, geo.K, geo.W, pack), cache)
+    x = case.x_dev.clone()
+    with pytest.raises(sc.ScError) as e:
+        sc.sc_stack_forward([case.bw, bad], cache, plan, x, case.rope, case.ws, case.ws_bytes)
+    assert e.value.code == sc.SC_EUNSUPPORTED
+    assert not any(cache.contains(st, l) for st in pack for l in range(2))
+    x.copy_(case.x_dev)
+    sc.sc_stack_forward([case.bw, case.bw], cache, plan, x, case.rope, case.ws, case.ws_bytes)
+    torch.cuda.synchronize()
+    assert all(cache.contains(st, l) for st in pack for l in range(2))
+    assert np.all(np.isfinite(from_device(x)))
+
+
+# Wan-shaped packs: progressive diagonals of 4 and 5 nodes (T = 18720, 23400
+# tokens), the same-level pack of 4 (level 2) and one clean node (4680).
 # The GEMMs pick their token-tile width from T, so between them these run
 # every width: QKV on 192 / 256 / 192 tokens, the MLP-up GEMM on 256, and the
 # out-projection and MLP-down GEMMs on 256 / 192 / 128.
 WAN_BLOCK_PACKS = [
     ("prog", cfg4_prog(False).pack, cfg4_prog(False).resident),
     ("prog", cfg4_prog(True).pack, cfg4_prog(True).resident),
+    ("same", cfg3_same(2).pack, cfg3_same(2).resident),
     ("clean", [(6, 4)], [(c, 0) for c in range(6)]),
 ]
 
 
-@pytest.mark.parametrize("kind,pack,resident", WAN_BLOCK_PACKS, ids=["4-node", "5-node", "1-node"])
+@pytest.mark.parametrize("kind,pack,resident", WAN_BLOCK_PACKS, ids=["4-node", "5-node", "same-4-node",
+                                                                     "1-node"])
 def test_wan_block_sampled_rows(kind, pack, resident):
+    """Wan shape, sampled rows: block output, q, o and the cached K/V."""
     case = BlockCase(WAN, kind, pack, resident, seed=12)
     got = case.run()
     rows = sample_rows(WAN.tokens_per_chunk, 24, seed=3)
-    want, _ = case.oracle(rows=rows)
-    for i in range(len(pack)):
-        block_gate(got[i][rows], want[i], f"wan {kind} node {pack[i]}")
+    check_branches(case, got, rows, f"wan {kind}")
+
+
+def test_wan_block_attention_branch():
+    """Wan shape, x of scale 2^-8 and w_down = 0: y - x is the attention
+    branch o Wo^T of each node of the progressive diagonal."""
+    case = BlockCase(WAN, "prog", cfg4_prog(False).pack, cfg4_prog(False).resident, seed=12,
+                     x_scale=X_SMALL, zero_down=True)
+    got = case.run()
+    rows = sample_rows(WAN.tokens_per_chunk, 24, seed=4)
+    check_branches(case, got, rows, "wan small-x", small_x=True)
 
 
 def test_wan_width_block_1800_tokens():

@@ -238,3 +238,137 @@ def test_wan_two_layer_pipeline_schedules_agree():
     xa, xb = from_device(a.xs), from_device(b.xs)
     for c in range(B):
         _stack_gate(xa[c], xb[c], L, c, runs=2)
+
+
+def test_small_clean_serial_matches_oracle():
+    """The clean-serial baseline of the paper's latency table (Eq. 2 order,
+    clean history, the refresh node last in each chunk) against the oracle's
+    run of the same single-node forwards."""
+    from oracle.pipeline import serial_order
+    geo, L, B, W = SMALL, 2, 6, 2
+    make, w_np, noise_np, keep = _setup(geo, L, B, W, "clean", seed=27, n_slots=60)
+    torch = torch_mod()
+    p = make()
+    p.run("serial")
+    torch.cuda.synchronize()
+    got = from_device(p.xs)
+    shp = BlockShape(geo.hidden, geo.heads, geo.head_dim, geo.mlp, geo.frames_per_chunk,
+                     geo.grid_h, geo.grid_w, geo.rope_dims, geo.theta)
+    packs = [[node] for node in serial_order(B, geo.K, True)]
+    outs, _, _ = run_stack(packs, policy("clean", geo.K, W), L, lambda l: w_np[l],
+                           lambda c, j: noise_np[c, j], shp, t_sched=T_SCHED)
+    for c in range(B):
+        _stack_gate(got[c], outs[(c, 1)], L, ("clean serial", c))
+
+
+def test_small_sixteen_chunk_stream_matches_oracle():
+    """A 16-chunk progressive stream (20 rounds with the refresh node, the
+    full window reached from round 10 on) run packed, against the oracle's
+    run of the same rounds."""
+    geo, L, B, W = SMALL, 2, 16, 6
+    make, w_np, noise_np, keep = _setup(geo, L, B, W, "prog", seed=28, n_slots=(W + 2 * geo.K + 4) * 3)
+    torch = torch_mod()
+    p = make()
+    p.run("packed")
+    torch.cuda.synchronize()
+    got = from_device(p.xs)
+    assert p.cache.free_slot_count() == (W + 2 * geo.K + 4) * 3
+    shp = BlockShape(geo.hidden, geo.heads, geo.head_dim, geo.mlp, geo.frames_per_chunk,
+                     geo.grid_h, geo.grid_w, geo.rope_dims, geo.theta)
+    outs, _, _ = run_stack(pipeline_rounds(B, geo.K, True), policy("prog", geo.K, W), L,
+                           lambda l: w_np[l], lambda c, j: noise_np[c, j], shp, t_sched=T_SCHED)
+    for c in range(B):
+        _stack_gate(got[c], outs[(c, 1)], L, ("16-chunk stream", c))
+
+
+def test_wan_stack_teacher_forced_layers():
+    """The 30-block Wan-shaped stack run as the progressive pipeline of 16
+    chunks with the refresh node (Sec. 3.3, Eq. 7), packed, up to steady
+    round 10: pack [(6,0), (7,1), (8,2), (9,3), (10,4)], every node with its
+    full 6-chunk window.  Teacher-forced check of layers 0, 15 and 29 of that
+    round: the block's input x_l and the history pages it reads at layer l
+    are read back, and the oracle recomputes the block from them on 24
+    sampled rows per node (the in-pack K/V it recomputes itself from x_l).
+    Gates: the block gate on the output, the branch gates on q, o and on the
+    K/V the block wrote, and the planted mistakes must fail the branch
+    gates."""
+    from oracle.policy import select
+    from block_inputs import block_shape, branch_gate, planted_must_fail, traces_of, weight_bits
+    from synth import TAG_K, TAG_V, bf16_value
+    from test_gpu_block import block_gate, read_pages
+    from gpu_cases import bits_to_device, sample_rows
+    torch = torch_mod()
+    geo, L, B, K, W, seed = WAN, 30, 16, WAN.K, WAN.W, 26
+    n, D = geo.tokens_per_chunk, geo.hidden
+    check, n_round = (0, 15, 29), 10
+    layers, keep, exact = [], [], {}
+    for l in range(L):
+        bits = weight_bits(geo, l, seed)
+        dev = {k: bits_to_device(v) for k, v in bits.items()}
+        keep.append(dev)
+        if l in check:
+            exact[l] = {k: bf16_value(v).astype(np.float64) for k, v in bits.items()}
+        layers.append(sc.BlockWeights(D, geo.heads, geo.head_dim, geo.mlp, dev["w_qkv"], dev["w_o"],
+                                      dev["w_up"], dev["w_down"]))
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(seed)
+    noise = torch.empty((B, K + 2, n, D), dtype=torch.bfloat16, device="cuda")
+    for c in range(B):                       # the sampler's noise (not an oracle input here)
+        noise[c].copy_(torch.randn((K + 2, n, D), generator=gen, device="cuda"))
+    rt = torch.empty(sc.sc_rope_table_bytes(geo.grid_h, geo.grid_w, geo.rope_dims, 3 * B + 3),
+                     dtype=torch.uint8, device="cuda")
+    rope = sc.sc_rope_table_build(rt, geo.grid_h, geo.grid_w, geo.rope_dims, 3 * B + 3, geo.theta)
+    n_slots = (W + 2 * K + 4) * geo.frames_per_chunk
+    pool = torch.empty(sc.sc_cache_pool_bytes(L, geo.heads, geo.head_dim, geo.tokens_per_page,
+                                              geo.frames_per_chunk, n_slots), dtype=torch.uint8, device="cuda")
+    cache = sc.sc_cache_create(pool, L, geo.heads, geo.head_dim, geo.tokens_per_page, geo.frames_per_chunk,
+                               n_slots)
+    p = StackPipeline(layers=layers, cache=cache, rope=rope, xs=noise[:, K + 1].clone(), noise=noise,
+                      policy="prog", K=K, W=W, B=B, t_sched=T_SCHED, refresh=True)
+    pack = sc.sc_pipeline_round_nodes(K, B, True, n_round)
+    assert pack == [(6, 0), (7, 1), (8, 2), (9, 3), (10, 4)]
+    sel = select(policy("prog", K, W), pack)
+    rows = sample_rows(n, 24, seed=6)
+    shp = block_shape(geo)
+    T = len(pack) * n
+    seen, x_in = [], {}
+
+    def hook(l, phase, x, plan, layers_in_use):
+        if l not in check:
+            return
+        torch.cuda.synchronize()
+        if phase == "in":
+            x_in["x"] = from_device(x)
+            return
+        y = from_device(x)
+        qo, oo = sc.sc_block_workspace_views(layers_in_use[l], T)
+        q_got = from_device(p.ws[qo:qo + T * D * 2].view(torch.bfloat16)).reshape(len(pack), n, geo.heads, -1)
+        o_got = from_device(p.ws[oo:oo + T * D * 2].view(torch.bfloat16)).reshape(len(pack), n, geo.heads, -1)
+        pages = {}
+
+        def resident_kv(st):
+            if st not in pages:
+                if cache.contains(st, l):
+                    pages[st] = read_pages(pool, geo, n_slots, cache.slots(st), layer=l)
+                else:                        # read only by a planted mistake
+                    shape = (n, geo.heads, geo.head_dim)
+                    pages[st] = (normal_parallel(shape, (seed, TAG_K) + st).astype(np.float64),
+                                 normal_parallel(shape, (seed, TAG_V) + st).astype(np.float64))
+            return pages[st]
+
+        xv = x_in.pop("x")
+        tr = traces_of(sel, lambda i: xv[i * n:(i + 1) * n], exact[l], resident_kv, shp, K, rows)
+        planted_must_fail(tr)
+        for i, node in enumerate(pack):
+            what = f"layer {l} node {node}"
+            block_gate(y[i * n + rows], tr["y"][i], what)
+            branch_gate(q_got[i][rows], tr["exact"][i]["q"], what + ": q")
+            branch_gate(o_got[i][rows], tr["exact"][i]["o"], what + ": o")
+            k_got, v_got = read_pages(pool, geo, n_slots, cache.slots(node), layer=l)
+            branch_gate(k_got[rows], tr["kv"][i][0][rows], what + ": cached K")
+            branch_gate(v_got[rows], tr["kv"][i][1][rows], what + ": cached V")
+        seen.append(l)
+
+    p.run("packed", layer_hooks={n_round: hook}, stop_after=n_round)
+    torch.cuda.synchronize()
+    assert seen == list(check)

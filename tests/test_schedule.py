@@ -98,3 +98,19 @@ def test_release_rule_with_position_dependent_policy():
         future = [node for p in rounds[n + 1:] for node in p]
         sc.sc_cache_release_unread(cache, "table", K, W, future, phi_table=phi, n_chunks=B)
     assert cache.free_slot_count() == 1024
+
+
+@pytest.mark.parametrize("K,B,refresh", [(1, 1, False), (3, 5, True), (4, 16, True), (4, 16, False),
+                                         (6, 3, True)])
+def test_serial_order_matches_oracle(K, B, refresh):
+    """Fully serial execution (Eq. 2): every update of chunk c before chunk
+    c + 1, levels K .. 1, the refresh (c, 0) last."""
+    from oracle.pipeline import serial_order
+    n = sc.sc_serial_steps(K, B, refresh)
+    got = [sc.sc_serial_step_node(K, B, refresh, i) for i in range(n)]
+    assert got == serial_order(B, K, refresh)
+    assert n == B * (K + 1 if refresh else K)
+    for bad in (-1, n):
+        with pytest.raises(sc.ScError) as e:
+            sc.sc_serial_step_node(K, B, refresh, bad)
+        assert e.value.code == sc.SC_EINVAL
