@@ -32,7 +32,7 @@
 extern "C" {
 #endif
 
-#define SC_ABI_VERSION 6
+#define SC_ABI_VERSION 7
 
 enum {
   SC_OK = 0,
@@ -211,6 +211,24 @@ int sc_plan_condition(sc_cache* cache, const sc_node* conditions, int32_t n, int
 size_t sc_attention_workspace_bytes(const sc_plan* plan, const sc_cache* cache);
 int sc_attention(const sc_plan* plan, const sc_cache* cache, int32_t layer, const void* q,
                  void* o, float scale, void* ws, size_t ws_bytes, sc_stream stream);
+
+/* ---- Attention that allocates nothing -----------------------------------
+ * For callers that cannot allocate device memory or hand over a workspace:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation.  sc_attention with its split-key partials kept in a
+ * library-owned device array of sc_attention_noalloc_scratch_bytes() bytes
+ * (64 MiB) on each GPU, held from the first call on that GPU until the
+ * process ends; the call itself allocates nothing.  Key ranges are cut into
+ * no more pieces than that array holds partials for, so the output equals
+ * sc_attention's up to the summation order.  Every call on a GPU shares that
+ * GPU's array (its contents are undefined between calls): calls that overlap
+ * on one GPU -- other streams, other threads -- race, and the caller must
+ * order them.  Arguments and errors as sc_attention, plus SC_ECAPACITY if a
+ * plan needed more partials than the array holds and SC_EDEVICE if the
+ * array's address cannot be resolved on the current device. */
+size_t sc_attention_noalloc_scratch_bytes(void);
+int sc_attention_noalloc(const sc_plan* plan, const sc_cache* cache, int32_t layer, const void* q,
+                         void* o, float scale, sc_stream stream);
 
 /* ---- Condition K/V (the condition c of Eq. 1) ---------------------------
  * Projects a condition sequence once per layer and caches it:

@@ -25,6 +25,7 @@ __all__ = [
     "sc_plan_condition", "sc_condition_workspace_bytes", "sc_condition_append",
     "sc_pipeline_rounds", "sc_pipeline_round_nodes", "sc_cache_release_unread", "sc_stack_forward",
     "sc_serial_steps", "sc_serial_step_node", "sc_block_workspace_views",
+    "sc_attention_noalloc", "sc_attention_noalloc_scratch_bytes",
 ]
 
 SC_OK, SC_EINVAL, SC_EUNAVAILABLE, SC_ECAPACITY = 0, -1, -2, -3
@@ -47,6 +48,7 @@ EXPORTED_SYMBOLS = [
     "sc_timer_enable", "sc_timer_read", "sc_probe_mfma_out_bytes", "sc_probe_mfma",
     "sc_pipeline_rounds", "sc_pipeline_round_nodes", "sc_cache_release_unread", "sc_stack_forward",
     "sc_serial_steps", "sc_serial_step_node", "sc_block_workspace_views",
+    "sc_attention_noalloc", "sc_attention_noalloc_scratch_bytes",
 ]
 
 # The library and PyTorch must share one HIP runtime: torch ships its own
@@ -155,13 +157,15 @@ _SIG = {
     "sc_cache_release_unread": (C.c_int, [_P, C.POINTER(sc_policy), C.POINTER(sc_node), C.c_int32]),
     "sc_stack_forward": (C.c_int, [C.POINTER(sc_block_weights), C.c_int32, _P, _P, _P,
                                    C.POINTER(sc_rope), _P, C.c_size_t, _P]),
+    "sc_attention_noalloc": (C.c_int, [_P, _P, C.c_int32, _P, _P, C.c_float, _P]),
+    "sc_attention_noalloc_scratch_bytes": (C.c_size_t, []),
     "sc_serial_steps": (C.c_int, [C.c_int32, C.c_int32, C.c_int32]),
     "sc_serial_step_node": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.POINTER(sc_node)]),
     "sc_block_workspace_views": (C.c_int, [C.POINTER(sc_block_weights), C.c_int32, C.POINTER(C.c_size_t),
                                            C.POINTER(C.c_size_t)]),
 }
 # ABI version this binding marshals for (SC_ABI_VERSION of the header)
-ABI_VERSION = 6
+ABI_VERSION = 7
 if not hasattr(lib, "sc_abi_version") or lib.sc_abi_version() != ABI_VERSION:
     raise ImportError(f"{library_path} does not implement ABI version {ABI_VERSION}; rebuild it "
                       "(__graft_entry__.build())")
@@ -411,6 +415,16 @@ def sc_attention(plan: Plan, cache: Cache, layer: int, q, o, scale: float, ws=No
 
 
 # ---------------------------------------------------------------------- block
+def sc_attention_noalloc(plan: Plan, cache: Cache, layer: int, q, o, scale: float, stream=None) -> None:
+    """sc_attention with the library's own scratch (no workspace argument)."""
+    _check(lib.sc_attention_noalloc(plan.handle, cache.handle, layer, _ptr(q), _ptr(o), scale,
+                                    _stream(stream)))
+
+
+def sc_attention_noalloc_scratch_bytes() -> int:
+    return lib.sc_attention_noalloc_scratch_bytes()
+
+
 class CrossAttn:
     """Cross-attention of a block to a condition cache: device weights w_q,
     w_o, optional fp32 query gain q_norm, the condition cache and its plan

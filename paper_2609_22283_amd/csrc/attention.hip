@@ -16,6 +16,8 @@
 #include <algorithm>
 #include <climits>
 #include <cstring>
+#include <map>
+#include <mutex>
 #include <type_traits>
 
 #include "device.h"
@@ -742,13 +744,13 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(uint16_t* __restrict_
 // (units mod resident work-groups) are cut into S pieces, S chosen to
 // minimise the tail's rounds (in units of one whole unit) plus a per-piece
 // cost of about two key tiles (prologue and partial write), with at most
-// kAttnMaxPieces pieces and no more pieces than the shortest node has key
+// max_pieces pieces and no more pieces than the shortest node has key
 // tiles.
 struct TailSplit {
   int32_t bq;       // queries per work-group of the shape used (128 or 256)
   int32_t whole, tail, split;
 };
-static TailSplit tail_split(const sc_plan* p, const sc_cache* c) {
+static TailSplit tail_split(const sc_plan* p, const sc_cache* c, int32_t max_pieces = kAttnMaxPieces) {
   const int32_t n = (int32_t)p->nodes.size();
   const int32_t bq = p->nq <= BQ_SMALL ? BQ_SMALL : BQ_MAX;
   const int32_t n_qtiles = (p->nq + bq - 1) / bq;
@@ -773,7 +775,7 @@ static TailSplit tail_split(const sc_plan* p, const sc_cache* c) {
   // K/V streaming sweep).
   if (ts.tail == 0 || mean_tiles < kAttnMinSplitTiles) return ts;
   double best = 1e30;
-  const int32_t smax = std::max(1, std::min({16, kAttnMaxPieces / ts.tail, min_tiles}));
+  const int32_t smax = std::max(1, std::min({16, max_pieces / ts.tail, min_tiles}));
   for (int32_t sp = 1; sp <= smax; ++sp) {
     const double rounds = (double)((ts.tail * sp + slots - 1) / slots);
     const double cost = rounds * (1.0 / sp + 2.0 / mean_tiles);
@@ -810,8 +812,19 @@ int attention_check(const sc_plan* p, const sc_cache* c) {
   return SC_OK;
 }
 
+// The launch of a plan whose split uses at most max_pieces pieces.
+static int launch_attention_pieces(const sc_plan* p, const sc_cache* c, int32_t layer, const void* q,
+                                   void* o, float scale, void* ws, size_t ws_bytes, int32_t max_pieces,
+                                   hipStream_t stream);
+
 int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const void* q, void* o,
                      float scale, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return launch_attention_pieces(p, c, layer, q, o, scale, ws, ws_bytes, kAttnMaxPieces, stream);
+}
+
+static int launch_attention_pieces(const sc_plan* p, const sc_cache* c, int32_t layer, const void* q,
+                                   void* o, float scale, void* ws, size_t ws_bytes, int32_t max_pieces,
+                                   hipStream_t stream) {
   const sc_cache_desc& d = c->d;
   const int32_t n = (int32_t)p->nodes.size();
   const int rc = attention_check(p, c);
@@ -845,11 +858,11 @@ int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const v
     SC_HIP(hipGetLastError());
     return SC_OK;
   }
-  const size_t need = attention_workspace_bytes(p, c);
+  const TailSplit ts = tail_split(p, c, max_pieces);
+  const size_t need = ts.split == 1 ? 0 : (size_t)ts.tail * ts.split * ts.bq * (HDB + 2) * sizeof(float);
   if (ws_bytes < need || (need && !ws))
     return fail(SC_EINVAL, "attention workspace of %zu bytes, need %zu", ws_bytes, need);
   if (reinterpret_cast<uintptr_t>(ws) & 15) return fail(SC_EINVAL, "workspace must be 16-byte aligned");
-  const TailSplit ts = tail_split(p, c);
   const int32_t bq = ts.bq;
   g.n_qtiles = (p->nq + bq - 1) / bq;
   g.whole_units = ts.whole;
@@ -884,4 +897,58 @@ int launch_attention(const sc_plan* p, const sc_cache* c, int32_t layer, const v
   return SC_OK;
 }
 
+// ------------------------------------------------ attention without allocation
+// The split-key partials of sc_attention_noalloc live in this library-owned
+// array; every GPU the library runs on holds its own copy until the process
+// ends.  Host code never passes the array's name to a kernel (on the host it
+// is a stand-in, not a device address): the device address comes from
+// hipGetSymbolAddress, once per device, with that device current.
+constexpr size_t kNoAllocScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+static std::mutex g_scratch_mu;
+static std::map<int, void*> g_scratch_ptr;  // device ordinal -> address of its scratch
+
+static int scratch_address(void** out) {
+  int dev = -1;
+  SC_HIP(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  auto it = g_scratch_ptr.find(dev);
+  if (it == g_scratch_ptr.end()) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!ptr || (reinterpret_cast<uintptr_t>(ptr) & 255))
+      return fail(SC_EDEVICE, "scratch of device %d at unusable address %p", dev, ptr);
+    it = g_scratch_ptr.emplace(dev, ptr).first;
+  }
+  *out = it->second;
+  return SC_OK;
+}
+
 }  // namespace sc
+
+extern "C" size_t sc_attention_noalloc_scratch_bytes(void) { return sc::kNoAllocScratchBytes; }
+
+extern "C" int sc_attention_noalloc(const sc_plan* p, const sc_cache* c, int32_t layer, const void* q,
+                                    void* o, float scale, sc_stream stream) {
+  using namespace sc;
+  if (!p || !c || !q || !o) return fail(SC_EINVAL, "null argument");
+  int rc = plan_check(p, c, layer);
+  if (rc != SC_OK) return rc;
+  if (p->nodes.empty()) return SC_OK;
+  if ((rc = attention_check(p, c)) != SC_OK) return rc;
+  void* ptr = nullptr;
+  if (c->d.dtype == SC_DTYPE_BF16 && (rc = scratch_address(&ptr)) != SC_OK) return rc;
+  // as many key-range pieces as the scratch holds partials for
+  const int32_t bq = p->nq <= BQ_SMALL ? BQ_SMALL : BQ_MAX;
+  const size_t piece_bytes = (size_t)bq * (HDB + 2) * sizeof(float);
+  const int32_t max_pieces = (int32_t)std::min<size_t>(kAttnMaxPieces, kNoAllocScratchBytes / piece_bytes);
+  const TailSplit ts = tail_split(p, c, max_pieces);
+  const size_t need = ts.split == 1 ? 0 : (size_t)ts.tail * ts.split * piece_bytes;
+  if (need > kNoAllocScratchBytes)
+    return fail(SC_ECAPACITY, "attention partials of %zu bytes exceed the %zu-byte scratch", need,
+                kNoAllocScratchBytes);
+  return launch_attention_pieces(p, c, layer, q, o, scale, ptr, ptr ? kNoAllocScratchBytes : 0, max_pieces,
+                                 static_cast<hipStream_t>(stream));
+}

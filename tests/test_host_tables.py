@@ -28,7 +28,7 @@ def test_header_symbols_exported():
     assert declared == set(sc.EXPORTED_SYMBOLS)
     for name in declared:
         assert hasattr(sc.lib, name), name
-    assert sc.sc_abi_version() == sc.ABI_VERSION == 6
+    assert sc.sc_abi_version() == sc.ABI_VERSION == 7
 
 
 def _random_pack(rnd, K, max_chunk=9, max_n=6):
