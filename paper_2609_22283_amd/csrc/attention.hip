@@ -378,12 +378,13 @@ __device__ __forceinline__ void landed() {  // this wave's copies are in LDS, th
   __syncthreads();
 }
 
-// Schedule.  A unit is a (head, node, query tile) triple, numbered head-major
-// then node then query tile; a unit's key tiles are processed in order by one
-// work-group.  Units of one (head, node) are consecutive and every unit
-// starts at its node's first key tile, so the work-groups an XCD runs side
-// by side read the same K/V tiles at about the same time and share them in
-// its L2.  Equal units fill the resident work-groups in whole rounds but the
+// Schedule.  A unit is a (head, query tile, node) triple, numbered head-major
+// then query tile then node; a unit's key tiles are processed in order by one
+// work-group.  Units of one head are consecutive, and every node's page list
+// starts at the state most nodes of the pack read (see shared_order), so the
+// work-groups an XCD runs side by side -- a few query tiles of every node of
+// one head -- read the same K/V tiles at about the same time and share them
+// in its L2.  Equal units fill the resident work-groups in whole rounds but the
 // last U mod R; those "tail" units are each cut into S pieces of their key
 // range, numbered piece-major (piece p of every tail unit before piece p+1),
 // so the last round is S times shorter.  Pieces leave unnormalised partials
@@ -411,8 +412,8 @@ __device__ __forceinline__ AttnItem decode_item(const AttnPlan& plan, const Attn
     unit = g.whole_units + j % g.tail_units;
     it.slot = j;
   }
-  it.qt = unit % g.n_qtiles;
-  it.node = (unit / g.n_qtiles) % g.n_nodes;
+  it.node = unit % g.n_nodes;
+  it.qt = (unit / g.n_nodes) % g.n_qtiles;
   it.head = unit / (g.n_qtiles * g.n_nodes);
   it.ntiles = node_tiles(plan, g, it.node);
   if (it.slot < 0) {
@@ -710,8 +711,8 @@ template <int BQ>
 __global__ __launch_bounds__(256) void attn_combine_kernel(uint16_t* __restrict__ o, AttnGeom g, AttnPlan plan) {
   const int32_t tu = blockIdx.x;
   const int32_t unit = g.whole_units + tu;
-  const int32_t qt = unit % g.n_qtiles;
-  const int32_t node = (unit / g.n_qtiles) % g.n_nodes;
+  const int32_t node = unit % g.n_nodes;
+  const int32_t qt = (unit / g.n_nodes) % g.n_qtiles;
   const int32_t head = unit / (g.n_qtiles * g.n_nodes);
   const int32_t lrow = blockIdx.y * 8 + (threadIdx.x >> 5);
   const int32_t dl = threadIdx.x & 31;
@@ -812,6 +813,38 @@ int attention_check(const sc_plan* p, const sc_cache* c) {
   return SC_OK;
 }
 
+// Page lists in a traversal order shared by the pack's nodes.  The softmax
+// sum does not depend on the order of a node's keys, so each node's list (its
+// states' pages, oldest state first) is rotated to start at the anchor: the
+// state read by the most nodes, the oldest of those.  Nodes of a progressive
+// or same-level pack read overlapping windows of consecutive chunks; rotated
+// this way, their work-groups read the shared states at the same time
+// instead of one chunk apart.
+static void shared_order(const sc_plan* p, AttnPlan& plan) {
+  const int32_t n = (int32_t)p->nodes.size();
+  std::map<StateKey, int32_t> readers;
+  for (int32_t i = 0; i < n; ++i)
+    for (int32_t q = p->page_off[i]; q < p->page_off[i + 1]; ++q)
+      if (q == p->page_off[i] || p->page_state[q] != p->page_state[q - 1]) ++readers[p->page_state[q]];
+  StateKey anchor(INT32_MIN, INT32_MIN);
+  int32_t most = 0;
+  for (const auto& kv : readers)  // ascending (chunk, level): the oldest wins ties
+    if (kv.second > most) {
+      most = kv.second;
+      anchor = kv.first;
+    }
+  for (int32_t i = 0; i <= n; ++i) plan.page_off[i] = p->page_off[i];
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t a = p->page_off[i], b = p->page_off[i + 1];
+    int32_t r = a;
+    while (r < b && p->page_state[r] < anchor) ++r;
+    if (r == b) r = a;
+    int32_t o = a;
+    for (int32_t q = r; q < b; ++q) plan.page_slot[o++] = p->page_slot[q];
+    for (int32_t q = a; q < r; ++q) plan.page_slot[o++] = p->page_slot[q];
+  }
+}
+
 // The launch of a plan whose split uses at most max_pieces pieces.
 static int launch_attention_pieces(const sc_plan* p, const sc_cache* c, int32_t layer, const void* q,
                                    void* o, float scale, void* ws, size_t ws_bytes, int32_t max_pieces,
@@ -830,8 +863,7 @@ static int launch_attention_pieces(const sc_plan* p, const sc_cache* c, int32_t 
   const int rc = attention_check(p, c);
   if (rc != SC_OK) return rc;
   AttnPlan plan;
-  for (int32_t i = 0; i <= n; ++i) plan.page_off[i] = p->page_off[i];
-  for (size_t i = 0; i < p->page_slot.size(); ++i) plan.page_slot[i] = p->page_slot[i];
+  shared_order(p, plan);
   AttnGeom g;
   std::memset(&g, 0, sizeof g);
   g.layer_base = c->pool + (size_t)layer * d.n_slots * c->slot_bytes;

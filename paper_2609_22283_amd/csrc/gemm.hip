@@ -67,8 +67,11 @@ __device__ __forceinline__ void store_sum_squares(const f32x4 (&acc)[FB][TB], fl
   }
 }
 
-// BN tokens per work-group tile (256, 192 or 128): 64 BN / 256 tokens per wave.
-template <int EPI, int BN>
+// BN tokens per work-group tile.  Wave layout WL = 0: 2 (features) x 4
+// (tokens) waves of 128 x BN/4 (BN a multiple of 64; required by the QKV
+// epilogue and the sums of squares, which take one head of 128 features per
+// wave); WL = 1: 4 x 2 waves of 64 x BN/2 (BN a multiple of 32, e.g. 224).
+template <int EPI, int BN, int WL>
 __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t* __restrict__ W,
                                                                  const uint16_t* __restrict__ X,
                                                                  int32_t F, int32_t T, int32_t Kd,
@@ -76,8 +79,10 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   // stage s: W tile at s * 64 KB, X tile at s * 64 KB + 32 KB; rows of 64 k
   // (128 B) with 16-byte column c stored at c ^ ((row >> 1) & 7)
   __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * G_TILE_BYTES];
-  constexpr int GWN = BN / 4;          // tokens per wave tile
-  constexpr int XROWS = BN / G_NW;     // token rows each wave copies per stage
+  static_assert(WL == 0 || (EPI != EPI_QKV && EPI != EPI_STORE), "layout 1 is for the plain epilogues");
+  constexpr int WM = WL ? 64 : GWM;    // features per wave tile
+  constexpr int GWN = WL ? BN / 2 : BN / 4;  // tokens per wave tile
+  static_assert(GWN % 16 == 0, "wave tiles hold whole 16-token blocks");
   const int32_t n_tf = F / GBM, n_tt = (T + BN - 1) / BN;
   // Each XCD takes a contiguous run of logical tiles; the run is walked in
   // groups of GT token tiles, feature tiles outermost within a group, so the
@@ -92,14 +97,16 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   const int32_t tid = threadIdx.x, lane = tid & 63;
   const int32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: LDS copy addresses stay scalar
   const int32_t lg = lane >> 4, c16 = lane & 15;
-  const int32_t wf = (wave & 1) * GWM, wt = (wave >> 1) * GWN;
+  const int32_t wf = WL ? (wave & 3) * WM : (wave & 1) * WM;
+  const int32_t wt = WL ? (wave >> 2) * GWN : (wave >> 1) * GWN;
 
   // copies: each wave moves weight rows [GROWS wave, GROWS wave + GROWS) and
-  // token rows [XROWS wave, XROWS wave + XROWS), 8 rows (1 KB) per
-  // instruction; lane (row, p) fetches column p ^ ((row >> 1) & 7).  Byte
-  // offsets are fixed per lane; the k offset is folded into the
+  // the 8-row token groups wave, wave + 8, ... (BN / 8 groups in all), 8 rows
+  // (1 KB) per instruction; lane (row, p) fetches column p ^ ((row >> 1) & 7).
+  // Byte offsets are fixed per lane; the k offset is folded into the
   // (wave-uniform) base pointer.
-  constexpr int NCP = GROWS / 8, NCPX = XROWS / 8;
+  constexpr int NCP = GROWS / 8, XGROUPS = BN / 8, NCPX = (XGROUPS + G_NW - 1) / G_NW;
+  static_assert(BN % 32 == 0 && BN <= GBM && NCPX <= NCP, "token copies ride with the weight copies");
   uint32_t woff[NCP], xoff[NCPX];
 #pragma unroll
   for (int j = 0; j < NCP; ++j) {
@@ -109,7 +116,7 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   }
 #pragma unroll
   for (int j = 0; j < NCPX; ++j) {
-    const int32_t row = XROWS * wave + 8 * j + (lane >> 3);
+    const int32_t row = 8 * min(wave + G_NW * j, XGROUPS - 1) + (lane >> 3);
     const int32_t col = (lane & 7) ^ ((row >> 1) & 7);
     const int32_t trow = min(t0 + row, T - 1);
     xoff[j] = ((uint32_t)trow * Kd + col * 8) * 2;
@@ -124,7 +131,8 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
 #pragma unroll
     for (int j = 0; j < NCP; ++j) {
       gdma16(wk + woff[j], a + (GROWS * wave + 8 * j) * 128);
-      if (j < NCPX) gdma16(xk + xoff[j], b + (XROWS * wave + 8 * j) * 128);
+      if (j < NCPX && (XGROUPS % G_NW == 0 || wave + G_NW * j < XGROUPS))  // wave-uniform
+        gdma16(xk + xoff[j], b + (8 * (wave + G_NW * j)) * 128);
     }
   };
   auto landed = [&]() {
@@ -135,7 +143,7 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   // LDS read offsets of this lane's fragments (16-byte column 4 s + lg)
   // 16x16x32 MFMAs: lane (lg, c16) supplies row c16 of each 16-row operand
   // block with k values 8 lg .. 8 lg + 7 of a 32-k step
-  constexpr int FB = GWM / 16, TB = GWN / 16;
+  constexpr int FB = WM / 16, TB = GWN / 16;
   uint32_t aoff[FB], boff[TB];
 #pragma unroll
   for (int fb = 0; fb < FB; ++fb) aoff[fb] = (uint32_t)(wf + 16 * fb + c16) * 128;
@@ -156,6 +164,22 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) bf[tb] = *reinterpret_cast<const bf16x8*>(b + boff[tb] + c);
   };
+
+  // The residual epilogue's reads of out[t][f] are issued before the main
+  // loop, so they land during it instead of after it, when every CU of the
+  // launch would read its residual tile at once.  Rows past T read
+  // the last row (valid memory, values unused).
+  constexpr bool PREFETCH = EPI == EPI_RESIDUAL;
+  u32x2 res[PREFETCH ? TB : 1][PREFETCH ? FB : 1];
+  if constexpr (PREFETCH) {
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) {
+      const int32_t t = min(t0 + wt + 16 * tb + c16, T - 1);
+      const uint16_t* orow = ep.out + (size_t)t * ep.ld_out + f0 + wf + 4 * lg;
+#pragma unroll
+      for (int fb = 0; fb < FB; ++fb) res[tb][fb] = *reinterpret_cast<const u32x2*>(orow + 16 * fb);
+    }
+  }
 
   const int32_t nk = Kd / GBK;
   issue(0, 0);
@@ -275,7 +299,11 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
 #pragma unroll
               for (int e = 0; e < 4; ++e) v[e] *= gv[e];
             }
-            const u32x2 r = *reinterpret_cast<const u32x2*>(dst);
+            u32x2 r;
+            if constexpr (PREFETCH)
+              r = res[tb][fb];
+            else
+              r = *reinterpret_cast<const u32x2*>(dst);
             v[0] += __uint_as_float(r.x << 16);
             v[1] += __uint_as_float(r.x & 0xffff0000u);
             v[2] += __uint_as_float(r.y << 16);
@@ -293,42 +321,56 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   }
 }
 
-template <int BN>
+template <int BN, int WL>
 static void launch_gemm_bn(int epi, const uint16_t* W, const uint16_t* X, int32_t F, int32_t T, int32_t Kd,
                            const GemmEpilogue& ep, hipStream_t stream) {
   const dim3 grid((uint32_t)(F / GBM) * (uint32_t)((T + BN - 1) / BN));
+  if constexpr (WL == 1) {  // the plain epilogues only
+    if (epi == EPI_GELU)
+      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_GELU, BN, 1>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
+    else
+      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_RESIDUAL, BN, 1>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd,
+                         ep);
+  } else {
   switch (epi) {
     case EPI_QKV:
-      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV, BN>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
+      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV, BN, 0>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
       break;
     case EPI_GELU:
-      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_GELU, BN>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
+      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_GELU, BN, 0>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
       break;
     case EPI_RESIDUAL:
-      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_RESIDUAL, BN>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd,
+      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_RESIDUAL, BN, 0>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd,
                          ep);
       break;
     default:
-      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_STORE, BN>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
+      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_STORE, BN, 0>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
+  }
   }
 }
 
-// Token-tile width of a launch: one work-group per CU, so a launch of n
-// tiles takes ceil(n / CUs) rounds of one tile's time.  A tile of BN tokens
-// takes BN / 256 of a 256-token tile's time times a per-width efficiency
-// loss (more fragment reads and copies per MFMA), measured on the Wan
-// block's four GEMMs: up to 1.12 at 192 tokens, 1.4 at 128.  The width with
-// the fewest tile-times wins, the wider one on ties.
-static int gemm_tile_tokens(int32_t F, int32_t T) {
-  int best = 256;
+// Tile shape of a launch: one work-group per CU, so a launch of n tiles
+// takes ceil(n / CUs) rounds of one tile's time.  A tile of BN tokens takes
+// BN / 256 of a 256-token tile's time times a per-shape efficiency loss
+// (more fragment reads and copies per MFMA), measured on the Wan block's
+// GEMMs.  The shape with the fewest tile-times wins, the wider one on ties.
+// Layout 1 (224-token tiles) serves the GELU and residual epilogues.
+struct GemmShape {
+  int bn, wl;
+};
+static GemmShape gemm_tile_shape(int epi, int32_t F, int32_t T) {
+  GemmShape best{256, 0};
   double best_cost = 1e30;
-  for (const int bn : {256, 192, 128}) {
-    const int64_t tiles = (int64_t)(F / GBM) * ((T + bn - 1) / bn);
-    const double eff = bn == 256 ? 1.0 : bn == 192 ? 1.12 : 1.4;
-    const double cost = (double)((tiles + kCUs - 1) / kCUs) * bn / 256.0 * eff;
+  const bool plain = epi == EPI_GELU || epi == EPI_RESIDUAL;
+  const GemmShape cands[] = {{256, 0}, {224, 1}, {192, 0}, {128, 0}};
+  for (const GemmShape c : cands) {
+    if (c.wl == 1 && !plain) continue;
+    const int64_t tiles = (int64_t)(F / GBM) * ((T + c.bn - 1) / c.bn);
+    const double eff = c.bn == 256 ? 1.0 : c.bn == 224 ? 1.02 : c.bn == 192 ? 1.12 : 1.4;
+    const double cost = (double)((tiles + kCUs - 1) / kCUs) * c.bn / 256.0 * eff;
     if (cost < best_cost - 1e-9) {
       best_cost = cost;
-      best = bn;
+      best = c;
     }
   }
   return best;
@@ -344,11 +386,15 @@ int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, i
   if (epi == EPI_QKV && (ep.hidden % GBM || ep.head_dim != GWM))
     return fail(SC_EUNSUPPORTED, "QKV epilogue needs hidden %% %d == 0 and head_dim %d", GBM, GWM);
   timer_begin(timer_kind, stream);
-  switch (gemm_tile_tokens(F, T)) {
-    case 128: launch_gemm_bn<128>(epi, W, X, F, T, Kd, ep, stream); break;
-    case 192: launch_gemm_bn<192>(epi, W, X, F, T, Kd, ep, stream); break;
-    default: launch_gemm_bn<256>(epi, W, X, F, T, Kd, ep, stream);
-  }
+  const GemmShape shape = gemm_tile_shape(epi, F, T);
+  if (shape.wl == 1)
+    launch_gemm_bn<224, 1>(epi, W, X, F, T, Kd, ep, stream);
+  else if (shape.bn == 128)
+    launch_gemm_bn<128, 0>(epi, W, X, F, T, Kd, ep, stream);
+  else if (shape.bn == 192)
+    launch_gemm_bn<192, 0>(epi, W, X, F, T, Kd, ep, stream);
+  else
+    launch_gemm_bn<256, 0>(epi, W, X, F, T, Kd, ep, stream);
   timer_end(timer_kind, stream);
   SC_HIP(hipGetLastError());
   return SC_OK;
