@@ -493,27 +493,37 @@ def bench_stack(args):
                              policy=policy, K=K, W=W, B=B, t_sched=(0.0, 5 / 8, 5 / 6, 15 / 16, 1.0),
                              refresh=True, condition=condition)
 
-    steady = [r for r in range(K + B) if r - K >= W and r < B]      # full pack, full window
-    res = {}
+    # steady rounds: full pack, full window; at most 20 of them, as the
+    # paper's latency table measures 20 steady output chunks
+    steady = [r for r in range(K + B) if r - K >= W and r < B][:20]
+    res = {"trials": args.trials, "steady_rounds": [steady[0], steady[-1]], "per_trial": {}}
+
+    def trials(key, run_once):
+        vals = [run_once() for _ in range(args.trials)]
+        res["per_trial"][key] = [round(v, 3) for v in vals]
+        res[key] = float(np.median(vals))
+        log(f"[bench] cfg5 {key}: {res[key]:.2f} ms (median of {args.trials} trials of the median "
+            f"steady round, rounds {steady[0]}..{steady[-1]}; trials {res['per_trial'][key]})")
+
     for key, mode, policy in (("packed", "packed", "prog"), ("sequential", "sequential", "prog"),
                               ("same_packed", "packed", "same")):
-        p = pipeline(policy)
-        ms = p.run(mode, time_rounds=True)
-        if key == "packed":  # kernel averages from a second run with the kernel timer on
+        def once(mode=mode, policy=policy):
+            ms = pipeline(policy).run(mode, time_rounds=True)
+            return float(np.median([ms[r] for r in steady]))
+        trials(key, once)
+        if key == "packed":  # kernel averages from a further run with the kernel timer on
             pt = pipeline(policy)
             pt.run(mode, kernel_timer_rounds=(steady[0], steady[-1]))
             n_attn, attn_tot = pt.kernel_times["attention"]
             del pt
             res["attn_ms_per_launch"] = attn_tot / max(1, n_attn)
             res["attn_launches"] = n_attn
-        res[key] = float(np.median([ms[r] for r in steady]))
-        log(f"[bench] cfg5 {key}: median steady round {res[key]:.2f} ms "
-            f"(rounds {steady[0]}..{steady[-1]})")
-    p = pipeline("clean")
-    ms = p.run("serial", time_rounds=True)                          # one entry per node
-    per_chunk = [sum(ms[c * (K + 1):(c + 1) * (K + 1)]) for c in range(B)]
-    res["clean_serial"] = float(np.median([per_chunk[c] for c in range(W, B)]))
-    log(f"[bench] cfg5 clean serial: median steady chunk {res['clean_serial']:.2f} ms")
+
+    def clean_once():
+        ms = pipeline("clean").run("serial", time_rounds=True)      # one entry per node
+        per_chunk = [sum(ms[c * (K + 1):(c + 1) * (K + 1)]) for c in range(B)]
+        return float(np.median([per_chunk[c] for c in range(W, min(B, W + 20))]))
+    trials("clean_serial", clean_once)
     return res
 
 
@@ -526,6 +536,8 @@ def main():
     ap.add_argument("--workload", default="cfg4",
                     choices=["cfg4", "cfg4R", "cfg3", "cfg2", "cfg5", "kvstream"])
     ap.add_argument("--layers", type=int, default=30, help="cfg5: blocks in the stack")
+    ap.add_argument("--trials", type=int, default=3,
+                    help="cfg5: trials per mode (the median is reported)")
     ap.add_argument("--chunks", type=int, default=16,
                     help="cfg5: chunks in the stream (40 = the paper's 477-frame videos)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -593,6 +605,7 @@ def main():
             "clean_serial_ms_per_chunk": round(r["clean_serial"], 3),
             "packed_vs_sequential": round(r["sequential"] / r["packed"], 3),
             "prog_pipeline_vs_clean_serial": round(r["clean_serial"] / r["packed"], 3),
+            "trials": r["trials"], "steady_rounds": r["steady_rounds"], "per_trial_ms": r["per_trial"],
             "attention_tflops": round(attn_tflops, 1),
             "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 1), "peak": PEAK_BF16_TFLOPS,
                          "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),

@@ -156,18 +156,23 @@ __device__ __forceinline__ AttnLane attn_lane(int32_t c, int32_t g) {
   return L;
 }
 
-// Q^T operand of a 16-query block: lane holds Q[row][32 ds + 8 g .. +7],
-// pre-scaled to log2 units.  Rows past the node's end repeat its last row.
+// Q^T operand of a 16-query block: lane holds Q[row][32 ds + 8 g .. +7].
+// Rows past the node's end repeat its last row.  The loads are issued with
+// the first tile copies (their latencies overlap); scale_q then pre-scales
+// the values to log2 units once they have landed.
 __device__ __forceinline__ void load_q(const uint16_t* q, const AttnGeom& g, int32_t node, int32_t head,
                                        int32_t qrow, int32_t lg, bf16x8 (&qreg)[4]) {
   const int32_t qrow_c = qrow < g.nq ? qrow : g.nq - 1;
   const uint16_t* qp = q + (((size_t)node * g.nq + qrow_c) * g.n_heads + head) * HDB + 8 * lg;
 #pragma unroll
-  for (int ds = 0; ds < 4; ++ds) {
-    const bf16x8 raw = *reinterpret_cast<const bf16x8*>(qp + 32 * ds);
+  for (int ds = 0; ds < 4; ++ds) qreg[ds] = *reinterpret_cast<const bf16x8*>(qp + 32 * ds);
+}
+
+__device__ __forceinline__ void scale_q(const AttnGeom& g, bf16x8 (&qreg)[4]) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) qreg[ds][e] = static_cast<__bf16>(static_cast<float>(raw[e]) * g.scale_log2);
-  }
+  for (int ds = 0; ds < 4; ++ds)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) qreg[ds][e] = static_cast<__bf16>(static_cast<float>(qreg[ds][e]) * g.scale_log2);
 }
 
 // Logits of one 64-key tile for a wave's two 16-query blocks:
@@ -606,9 +611,6 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
   const int32_t nk = kv.nk;
   const bool ragged = it.tb == it.ntiles && (nk % BK) != 0;
   bf16x8 qreg[2][4];
-#pragma unroll
-  for (int qb = 0; qb < 2; ++qb)
-    load_q(q, g, it.node, it.head, it.qt * BQ + wave * 32 + 16 * qb + c, lg, qreg[qb]);
   const AttnLane L = attn_lane(c, lg);
 
   f32x4 oacc[2][8];
@@ -633,7 +635,12 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
       kv.copy_v(ta * BK, smem + 2 * KT_BYTES, s0);
       if (ta + 1 < ntiles) kv.copy_k((ta + 1) * BK, smem + KT_BYTES, kv.slots((ta + 1) * BK));
     }
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+      load_q(q, g, it.node, it.head, it.qt * BQ + wave * 32 + 16 * qb + c, lg, qreg[qb]);
     landed();
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) scale_q(g, qreg[qb]);
     if constexpr (ACT) {
       qk_tile(smem, L, qreg, s, m);
       if (ta + 1 == ntiles && ragged) mask_tile(s, ta * BK, nk, lg);
