@@ -200,7 +200,9 @@ int sc_plan_condition(sc_cache* cache, const sc_node* conditions, int32_t n, int
  * on the same stream.  Limits of this build: at most 64 pack nodes and 800
  * pages per plan (the page lists travel by value in the kernel arguments, so
  * no per-round host-to-device copy is needed); larger plans fail with
- * SC_EUNSUPPORTED before anything is launched.  ws: device scratch, 16-byte aligned, of at least
+ * SC_EUNSUPPORTED before anything is launched.  bf16 caches need head_dim
+ * 128 and pages of at least one key tile: 32 tokens when Nq <= 64, 64
+ * otherwise (else SC_EUNSUPPORTED).  ws: device scratch, 16-byte aligned, of at least
  * sc_attention_workspace_bytes(plan, cache) bytes (may be NULL when that is
  * 0, as for fp32 caches); the bf16 kernel splits long key ranges across
  * work-groups and merges their partial softmax sums there.  Its contents are

@@ -94,16 +94,24 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 }
 
 // ------------------------------------------------------------- bf16 kernel
-// Two work-group shapes, both with two waves per SIMD: 8 waves x 32 queries
-// (256 per work-group, one work-group per CU) and 4 waves x 32 queries (128,
-// two per CU), the latter for nodes of at most 128 queries.  A wave's 32
-// queries are two 16-query blocks of the 16x16x32 MFMA.
-constexpr int BK = 64;                 // keys per LDS tile
-constexpr int HDB = 128;               // head dim of the bf16 kernels
-constexpr int KT_BYTES = BK * HDB * 2;  // 16 KB
-constexpr int VT_BYTES = HDB * BK * 2;  // 16 KB
-constexpr int SMEM_BYTES = 2 * (KT_BYTES + VT_BYTES);
-constexpr int BQ_SMALL = 128, BQ_MAX = 256;  // queries per work-group of the two shapes
+// Three work-group shapes: 8 waves x 32 queries (256 per work-group, one
+// work-group per CU) and 4 waves x 32 queries (128, two per CU, for nodes of
+// at most 128 queries), both with two waves per SIMD and 64-key tiles; and
+// 2 waves x 32 queries (64, for nodes of at most 64) on 32-key tiles, whose
+// deeper K/V rings (3 or 4 tiles of 16 KB) keep two or three tiles in flight
+// per work-group, three or two work-groups per CU.  Such nodes are short and
+// their attention streams K/V from HBM: in-flight copies, bounded by LDS,
+// set its rate.  A wave's 32 queries are two 16-query blocks of the
+// 16x16x32 MFMA; key tiles hold KH halves of 32 keys.
+constexpr int HDB = 128;  // head dim of the bf16 kernels
+template <int KH>
+struct Tile {
+  static constexpr int BK = 32 * KH;                  // keys per LDS tile
+  static constexpr int KT_BYTES = BK * HDB * 2;       // K tile: BK rows of 256 bytes
+  static constexpr int VT_BYTES = HDB * BK * 2;       // V^T tile: 128 rows of 2 BK bytes
+};
+constexpr int BQ_TINY = 64, BQ_SMALL = 128, BQ_MAX = 256;  // queries per work-group of the three shapes
+constexpr int kh_of(int bq) { return bq == BQ_TINY ? 1 : 2; }
 // Softmax bookkeeping.  Q is pre-scaled by scale*log2(e), so S is in log2
 // units, and each S tile starts its accumulation at -m: p = exp2(S)
 // directly.  m is the exact maximum of the work item's first tile and is
@@ -136,13 +144,22 @@ __device__ __forceinline__ uint32_t kswz(int32_t row) { return (uint32_t)((row &
 struct AttnLane {
   // per-lane LDS read offsets (bytes) inside one buffer
   uint32_t koff[2][4];  // K row of block b, 16-byte column 4 ds + g (second 32 rows add 8192)
-  uint32_t voff[2];     // V^T row c, 16-byte column 4 h + g           (16-row block db adds 2048)
+  uint32_t voff[2];     // V^T row c, 16-byte column 4 h + g (16-row block db adds 32 BK)
 };
+
+// XOR swizzle of a V^T tile row d (16-byte columns): 64-key rows (128 bytes)
+// take (d / 2) mod 8, 32-key rows (64 bytes) (d / 4) mod 4, so the 16 rows
+// of a PV operand read fall on distinct banks.
+template <int KH>
+__device__ __forceinline__ uint32_t vswz(int32_t d) {
+  return KH == 2 ? (uint32_t)((d >> 1) & 7) : (uint32_t)((d >> 2) & 3);
+}
 
 // A row i of the S^T MFMA for 16-key block b of a 32-key half holds key
 // 8 (i / 4) + 4 b + i % 4: each lane's four results of blocks 0 and 1 are
 // then keys 8 g .. 8 g + 7 of the half -- exactly the B operand of the PV
 // MFMA, which therefore needs no shuffle.
+template <int KH>
 __device__ __forceinline__ AttnLane attn_lane(int32_t c, int32_t g) {
   AttnLane L;
 #pragma unroll
@@ -152,7 +169,8 @@ __device__ __forceinline__ AttnLane attn_lane(int32_t c, int32_t g) {
     for (int ds = 0; ds < 4; ++ds) L.koff[b][ds] = row * 256 + (((4 * ds + g) ^ kswz(row)) << 4);
   }
 #pragma unroll
-  for (int h = 0; h < 2; ++h) L.voff[h] = c * 128 + (((4 * h + g) ^ ((c >> 1) & 7)) << 4);
+  for (int h = 0; h < 2; ++h)
+    L.voff[h] = c * (64 * KH) + (((4 * h + g) ^ vswz<KH>(c)) << 4);  // h < KH only is used
   return L;
 }
 
@@ -178,7 +196,8 @@ __device__ __forceinline__ void scale_q(const AttnGeom& g, bf16x8 (&qreg)[4]) {
 // Logits of one 64-key tile for a wave's two 16-query blocks:
 // s[h][b][qb] holds, in lane (g, c) value r, key 32 h + 8 g + 4 b + r of the
 // tile for query c of block qb.
-typedef f32x4 STile[2][2][2];
+template <int KH>
+using STile = f32x4[KH][2][2];
 
 // Sum / maximum of one query's values over the four lane groups.
 __device__ __forceinline__ float group_sum(float x) {
@@ -201,12 +220,13 @@ __device__ __forceinline__ bf16x8 ones_row(int32_t c) {
 }
 
 // Column maxima of a tile, per query block.
-__device__ __forceinline__ void tile_max(const STile& s, float (&mx)[2]) {
+template <int KH>
+__device__ __forceinline__ void tile_max(const STile<KH>& s, float (&mx)[2]) {
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
     float m = s[0][0][qb][0];
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < KH; ++h)
 #pragma unroll
       for (int b = 0; b < 2; ++b)
 #pragma unroll
@@ -216,9 +236,10 @@ __device__ __forceinline__ void tile_max(const STile& s, float (&mx)[2]) {
 }
 
 // Keys at or past the node's end get no weight (t0: the tile's first key).
-__device__ __forceinline__ void mask_tile(STile& s, int32_t t0, int32_t nk, int32_t lg) {
+template <int KH>
+__device__ __forceinline__ void mask_tile(STile<KH>& s, int32_t t0, int32_t nk, int32_t lg) {
 #pragma unroll
-  for (int h = 0; h < 2; ++h)
+  for (int h = 0; h < KH; ++h)
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
@@ -230,11 +251,12 @@ __device__ __forceinline__ void mask_tile(STile& s, int32_t t0, int32_t nk, int3
 
 // p = exp2(s) rounded to bf16: pb[h][qb] is the B operand of the PV MFMA for
 // the 32-key half h.
-__device__ __forceinline__ void probs(const STile& s, bf16x8 (&pb)[2][2]) {
+template <int KH>
+__device__ __forceinline__ void probs(const STile<KH>& s, bf16x8 (&pb)[KH][2]) {
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < KH; ++h)
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         pb[h][qb][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(s[h][e >> 2][qb][e & 3]));
@@ -242,13 +264,14 @@ __device__ __forceinline__ void probs(const STile& s, bf16x8 (&pb)[2][2]) {
 
 // The same, also returning this lane's sums of the rounded values per block
 // (the exact redo path).
-__device__ __forceinline__ void probs_tile(const STile& s, bf16x8 (&pb)[2][2], float (&lt)[2]) {
+template <int KH>
+__device__ __forceinline__ void probs_tile(const STile<KH>& s, bf16x8 (&pb)[KH][2], float (&lt)[2]) {
   const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
     float l0 = 0.f, l1 = 0.f;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < KH; ++h) {
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         pb[h][qb][e] = static_cast<__bf16>(__builtin_amdgcn_exp2f(s[h][e >> 2][qb][e & 3]));
@@ -272,19 +295,25 @@ __device__ __forceinline__ void dma16(const char* src, char* lds_wave_base) {
                                    16, 0, 0);
 }
 
-// Copies of 64-key K and V^T tiles of one (node, head) from the paged cache
-// into LDS, split over the NW waves of a work-group.  64 keys span at most
-// two pages (pages hold >= 64 tokens), so the page of a key is chosen against
+// Copies of BK-key K and V^T tiles of one (node, head) from the paged cache
+// into LDS, split over the NW waves of a work-group.  A tile spans at most
+// two pages (pages hold >= BK tokens), so the page of a key is chosen against
 // one wave-uniform boundary.
 // Offsets are 32-bit, relative to the layer's slots (the host checks that a
-// layer fits in 4 GB); the per-page parts are wave-uniform.  Each wave copies
-// 16 / NW groups of 4 K rows (1 KB each) and 16 / NW groups of 8 V^T rows; lane
-// (row, physical column p) fetches logical column p ^ swizzle(row).  K rows
-// of keys past the node's end fetch its last key, V^T columns the tile's
-// first key (valid memory; their probabilities are zero).
-template <int NW>
+// layer fits in 4 GB); the per-page parts are wave-uniform.  A copy
+// instruction moves 1 KB: 4 K rows, or RPI = 512 / BK V^T rows of BK / 8
+// 16-byte columns.  Each wave issues KCP of the first and VCP of the second
+// per tile; lane (row, physical column p) fetches logical column
+// p ^ swizzle(row).  K rows of keys past the node's end fetch its last key,
+// V^T columns the tile's first key (valid memory; their probabilities are
+// zero).
+template <int NW, int KH>
 struct KvTiles {
-  static constexpr int KCP = 64 / (4 * NW), VCP = 128 / (8 * NW);
+  static constexpr int BK = Tile<KH>::BK;
+  static constexpr int KCP = BK / (4 * NW), VCP = BK / (4 * NW);
+  static constexpr int LPR = BK / 8, RPI = 64 / LPR;  // V^T: lanes per row, rows per copy instruction
+  static_assert(LPR == 1 << (KH + 1), "V^T lanes per row");
+  static_assert(KCP >= 1 && KCP * 4 * NW == BK, "K copy split");
   struct Slots {
     uint32_t lo, hi;  // byte offsets of the slots of the tile's first page and the next one
     int32_t plo;      // index of the tile's first page within the node
@@ -313,7 +342,7 @@ struct KvTiles {
     kbad = (uint32_t)page_slot[npages - 1] * slot_bytes + khead + (uint32_t)(tpp - 1) * 256;
     krow0 = 4 * KCP * wave + (lane >> 4);
     const int32_t kp = lane & 15;
-    const int32_t vrow0 = 8 * VCP * wave + (lane >> 3), vp = lane & 7;
+    const int32_t vrow0 = RPI * VCP * wave + (lane >> (KH + 1)), vp = lane & (LPR - 1);  // LPR = 2^(KH+1)
 #pragma unroll
     for (int j = 0; j < KCP; ++j) {
       const int32_t row = krow0 + 4 * j;
@@ -321,8 +350,8 @@ struct KvTiles {
     }
 #pragma unroll
     for (int j = 0; j < VCP; ++j) {
-      const int32_t d = vrow0 + 8 * j;
-      vkey[j] = 8 * (vp ^ ((d >> 1) & 7));                           // key offset in tile
+      const int32_t d = vrow0 + RPI * j;
+      vkey[j] = 8 * (vp ^ (int32_t)vswz<KH>(d));                     // key offset in tile
       vlane[j] = (uint32_t)d * tpp * 2 + (uint32_t)vkey[j] * 2;      // plus key t0 * 2
     }
   }
@@ -354,7 +383,7 @@ struct KvTiles {
       dma16(lbase + src, kl + rg * 256);
     }
   }
-  // A V^T row holds the tile's 64 keys; a page boundary or the node's end
+  // A V^T row holds the tile's BK keys; a page boundary or the node's end
   // falls inside the tile for about one tile in a page, so the per-lane
   // choice is taken only then (wave-uniform branch).
   __device__ __forceinline__ void copy_v(int32_t t0, char* vl, const Slots& sl) const {
@@ -363,7 +392,7 @@ struct KvTiles {
     const int32_t lim = nk - t0, split = bkey - t0;
     if (split >= BK && lim >= BK) {
 #pragma unroll
-      for (int j = 0; j < VCP; ++j) dma16(lbase + (lo + vlane[j]), vl + (8 * VCP * wave + 8 * j) * 128);
+      for (int j = 0; j < VCP; ++j) dma16(lbase + (lo + vlane[j]), vl + (RPI * VCP * wave + RPI * j) * 2 * BK);
       return;
     }
     const uint32_t hi = sl.hi + vhead + (uint32_t)(t0 - bkey) * 2;
@@ -373,7 +402,7 @@ struct KvTiles {
       const bool in = rk < lim;
       const uint32_t off = in ? vlane[j] : vlane[j] - (uint32_t)rk * 2;
       const uint32_t base = (in && rk >= split) ? hi : lo;
-      dma16(lbase + (base + off), vl + (8 * VCP * wave + 8 * j) * 128);
+      dma16(lbase + (base + off), vl + (RPI * VCP * wave + RPI * j) * 2 * BK);
     }
   }
 };
@@ -381,6 +410,21 @@ struct KvTiles {
 __device__ __forceinline__ void landed() {  // this wave's copies are in LDS, then everyone's
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
+}
+
+// The same for all but this wave's n most recent vector-memory operations (a
+// wave's loads complete in issue order for this counter), n a multiple of 4
+// up to 16 (wave-uniform).  The barrier is issued without __syncthreads'
+// release fence, which would wait for every outstanding copy; the memory
+// clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void landed_but(int32_t n) {
+  switch (n) {
+    case 0: asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory"); break;
+    case 4: asm volatile("s_waitcnt vmcnt(4)\n\ts_barrier" ::: "memory"); break;
+    case 8: asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory"); break;
+    case 12: asm volatile("s_waitcnt vmcnt(12)\n\ts_barrier" ::: "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(16)\n\ts_barrier" ::: "memory"); break;
+  }
 }
 
 // Schedule.  A unit is a (head, query tile, node) triple, numbered head-major
@@ -401,10 +445,13 @@ struct AttnItem {
   int32_t slot;     // partial slot, or -1 for a whole unit
 };
 
+template <int KH>
 __device__ __forceinline__ int32_t node_tiles(const AttnPlan& plan, const AttnGeom& g, int32_t node) {
+  constexpr int BK = Tile<KH>::BK;
   return ((plan.page_off[node + 1] - plan.page_off[node]) * g.tpp + BK - 1) / BK;
 }
 
+template <int KH>
 __device__ __forceinline__ AttnItem decode_item(const AttnPlan& plan, const AttnGeom& g, uint32_t b) {
   AttnItem it;
   int32_t unit;
@@ -420,7 +467,7 @@ __device__ __forceinline__ AttnItem decode_item(const AttnPlan& plan, const Attn
   it.node = unit % g.n_nodes;
   it.qt = (unit / g.n_nodes) % g.n_qtiles;
   it.head = unit / (g.n_qtiles * g.n_nodes);
-  it.ntiles = node_tiles(plan, g, it.node);
+  it.ntiles = node_tiles<KH>(plan, g, it.node);
   if (it.slot < 0) {
     it.ta = 0;
     it.tb = it.ntiles;
@@ -464,13 +511,14 @@ __device__ __forceinline__ void store_rows(const AttnItem& it, const AttnGeom& g
   }
 }
 
-// S^T of one 64-key tile, s[h][b][qb] = K_(h,b) Q_qb^T - m_qb: all eight
+// S^T of one tile, s[h][b][qb] = K_(h,b) Q_qb^T - m_qb: all 4 KH
 // accumulators advance together.
+template <int KH>
 __device__ __forceinline__ void qk_tile(const char* kl, const AttnLane& L, const bf16x8 (&qreg)[2][4],
-                                        STile& s, const float (&m)[2]) {
-  f32x4 acc[2][2][2];
+                                        STile<KH>& s, const float (&m)[2]) {
+  f32x4 acc[KH][2][2];
 #pragma unroll
-  for (int h = 0; h < 2; ++h)
+  for (int h = 0; h < KH; ++h)
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
@@ -480,7 +528,7 @@ __device__ __forceinline__ void qk_tile(const char* kl, const AttnLane& L, const
 #pragma unroll
   for (int ds = 0; ds < 4; ++ds)
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < KH; ++h)
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
         const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + L.koff[b][ds] + h * 8192);
@@ -488,21 +536,22 @@ __device__ __forceinline__ void qk_tile(const char* kl, const AttnLane& L, const
         acc[h][b][1] = mfma16(a, qreg[1][ds], acc[h][b][1]);
       }
 #pragma unroll
-  for (int h = 0; h < 2; ++h)
+  for (int h = 0; h < KH; ++h)
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) s[h][b][qb] = acc[h][b][qb];
 }
 
-// O^T += V^T P^T for a 64-key tile whose V^T sits at vl.
-__device__ __forceinline__ void pv_tile(const char* vl, const AttnLane& L, const bf16x8 (&pb)[2][2],
+// O^T += V^T P^T for a tile whose V^T sits at vl.
+template <int KH>
+__device__ __forceinline__ void pv_tile(const char* vl, const AttnLane& L, const bf16x8 (&pb)[KH][2],
                                         f32x4 (&oacc)[2][8]) {
 #pragma unroll
-  for (int h = 0; h < 2; ++h)
+  for (int h = 0; h < KH; ++h)
 #pragma unroll
     for (int db = 0; db < 8; ++db) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(vl + L.voff[h] + db * 2048);
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(vl + L.voff[h] + db * (16 * 2 * Tile<KH>::BK));
       oacc[0][db] = mfma16(a, pb[h][0], oacc[0][db]);
       oacc[1][db] = mfma16(a, pb[h][1], oacc[1][db]);
     }
@@ -513,25 +562,26 @@ __device__ __forceinline__ void pv_tile(const char* vl, const AttnLane& L, const
 // cores while the exponentials of tile t run on the vector ALUs, then
 // O^T += V(t)^T P(t) and the row sums lsum += 1^T P(t).  K runs one tile
 // ahead of V: K(t+1) sits in K buffer KN, V(t) in V buffer VC.
-template <int KN, int VC, bool NEXT, bool MASK>
+template <int KH, int KN, int VC, bool NEXT, bool MASK>
 __device__ __forceinline__ void attn_step(const char* smem, const AttnLane& L, const bf16x8 (&qreg)[2][4],
-                                          f32x4 (&oacc)[2][8], STile& s, const float (&m)[2],
+                                          f32x4 (&oacc)[2][8], STile<KH>& s, const float (&m)[2],
                                           f32x4 (&lsum)[2], const bf16x8& ones, int32_t t0, int32_t nk,
                                           int32_t lg) {
-  if constexpr (MASK) mask_tile(s, t0, nk, lg);
-  bf16x8 pb[2][2];
-  probs(s, pb);
-  STile sn;
-  if constexpr (NEXT) qk_tile(smem + KN * KT_BYTES, L, qreg, sn, m);
-  pv_tile(smem + 2 * KT_BYTES + VC * VT_BYTES, L, pb, oacc);
+  using T = Tile<KH>;
+  if constexpr (MASK) mask_tile<KH>(s, t0, nk, lg);
+  bf16x8 pb[KH][2];
+  probs<KH>(s, pb);
+  STile<KH> sn;
+  if constexpr (NEXT) qk_tile<KH>(smem + KN * T::KT_BYTES, L, qreg, sn, m);
+  pv_tile<KH>(smem + 2 * T::KT_BYTES + VC * T::VT_BYTES, L, pb, oacc);
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
+  for (int h = 0; h < KH; ++h) {
     lsum[0] = mfma16(ones, pb[h][0], lsum[0]);
     lsum[1] = mfma16(ones, pb[h][1], lsum[1]);
   }
   if constexpr (NEXT) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < KH; ++h)
 #pragma unroll
       for (int b = 0; b < 2; ++b)
 #pragma unroll
@@ -543,23 +593,24 @@ __device__ __forceinline__ void attn_step(const char* smem, const AttnLane& L, c
 // each query's maximum logit over the item's keys, then the softmax from
 // that maximum (every p <= 1).  Single-buffered K and V tiles; slow, and
 // taken only for logits far above the first tile's maximum.
-template <int NW>
-__device__ __forceinline__ void attn_exact(char* smem, const KvTiles<NW>& kv, const AttnLane& L,
+template <int NW, int KH>
+__device__ __forceinline__ void attn_exact(char* smem, const KvTiles<NW, KH>& kv, const AttnLane& L,
                                            const bf16x8 (&qreg)[2][4], f32x4 (&oacc)[2][8], float (&m)[2],
                                            float (&l)[2], int32_t ta, int32_t ntiles, int32_t lg) {
+  constexpr int BK = Tile<KH>::BK;
   char* const kl = smem;
-  char* const vl = smem + 2 * KT_BYTES;
+  char* const vl = smem + 2 * Tile<KH>::KT_BYTES;
   const int32_t nk = kv.nk;
   const float zero[2] = {0.f, 0.f};
   float mx[2] = {-INFINITY, -INFINITY};
   for (int32_t t = ta; t < ntiles; ++t) {
     kv.copy_k(t * BK, kl, kv.slots(t * BK));
     landed();
-    STile s;
-    qk_tile(kl, L, qreg, s, zero);
-    mask_tile(s, t * BK, nk, lg);
+    STile<KH> s;
+    qk_tile<KH>(kl, L, qreg, s, zero);
+    mask_tile<KH>(s, t * BK, nk, lg);
     float tm[2];
-    tile_max(s, tm);
+    tile_max<KH>(s, tm);
     mx[0] = fmaxf(mx[0], tm[0]);
     mx[1] = fmaxf(mx[1], tm[1]);
     __syncthreads();
@@ -572,46 +623,53 @@ __device__ __forceinline__ void attn_exact(char* smem, const KvTiles<NW>& kv, co
     for (int db = 0; db < 8; ++db) oacc[qb][db] = f32x4{};
   }
   for (int32_t t = ta; t < ntiles; ++t) {
-    const typename KvTiles<NW>::Slots sl = kv.slots(t * BK);
+    const typename KvTiles<NW, KH>::Slots sl = kv.slots(t * BK);
     kv.copy_k(t * BK, kl, sl);
     kv.copy_v(t * BK, vl, sl);
     landed();
-    STile s;
-    qk_tile(kl, L, qreg, s, m);
-    mask_tile(s, t * BK, nk, lg);
-    bf16x8 pb[2][2];
+    STile<KH> s;
+    qk_tile<KH>(kl, L, qreg, s, m);
+    mask_tile<KH>(s, t * BK, nk, lg);
+    bf16x8 pb[KH][2];
     float lt[2];
-    probs_tile(s, pb, lt);
+    probs_tile<KH>(s, pb, lt);
     l[0] += lt[0];
     l[1] += lt[1];
-    pv_tile(vl, L, pb, oacc);
+    pv_tile<KH>(vl, L, pb, oacc);
     __syncthreads();
   }
 }
 
 // NW = 8: 256 queries per work-group, one work-group per CU; NW = 4: 128
-// queries, two per CU.  Both keep two waves per SIMD; each wave owns two
-// 16-query blocks.
-template <int NW>
-__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16_t* __restrict__ q,
+// queries, two per CU; both keep two waves per SIMD.  NW = 2: 64 queries on
+// 32-key tiles (KH = 1), three or two per CU.  Each wave owns two 16-query
+// blocks.  D: tiles of the K and of the V^T ring.  With D = 2 the loop below
+// keeps one tile in flight, its buffer parity unrolled; the 64-query shape
+// runs D = 3 or 4 (runtime ring slots, D - 1 tiles in flight): its nodes
+// are short and streamed, so it trades resident waves for copies in flight.
+template <int NW, int KH, int D>
+__global__ __launch_bounds__(64 * NW, NW == 8 || D == 4 ? 1 : 2) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                                     uint16_t* __restrict__ o, AttnGeom g,
                                                                     AttnPlan plan) {
   constexpr int BQ = 32 * NW;
-  // K buffers 0, 1 then V^T buffers 0, 1 (16 KB each)
-  __shared__ __attribute__((aligned(1024))) char smem[SMEM_BYTES];
+  using T = Tile<KH>;
+  constexpr int BK = T::BK, KT_BYTES = T::KT_BYTES, VT_BYTES = T::VT_BYTES;
+  static_assert((D == 2 && KH == 2) || (KH == 1 && (D == 3 || D == 4)), "ring depth");
+  // K buffers 0 .. D-1 then V^T buffers 0 .. D-1 (KT_BYTES, VT_BYTES each)
+  __shared__ __attribute__((aligned(1024))) char smem[D * (KT_BYTES + VT_BYTES)];
   __shared__ int32_t any_bad;
-  const AttnItem it = decode_item(plan, g, blockIdx.x);
+  const AttnItem it = decode_item<KH>(plan, g, blockIdx.x);
   if (it.ta == it.tb) return;  // empty piece of a unit shorter than the split
   const int32_t ta = it.ta, ntiles = it.tb;  // this item's key tiles: [ta, ntiles)
   const int32_t tid = threadIdx.x, lane = tid & 63;
   const int32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: LDS copy addresses stay scalar
   const int32_t lg = lane >> 4, c = lane & 15;
   if (tid == 0) any_bad = 0;
-  const KvTiles<NW> kv(plan, g, it.node, it.head, wave, lane);
+  const KvTiles<NW, KH> kv(plan, g, it.node, it.head, wave, lane);
   const int32_t nk = kv.nk;
   const bool ragged = it.tb == it.ntiles && (nk % BK) != 0;
   bf16x8 qreg[2][4];
-  const AttnLane L = attn_lane(c, lg);
+  const AttnLane L = attn_lane<KH>(c, lg);
 
   f32x4 oacc[2][8];
 #pragma unroll
@@ -625,12 +683,12 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
   // query tile) still copies its share of every tile and meets every
   // barrier, but skips the matrix and softmax work.
   const bool active = it.qt * BQ + wave * 32 < g.nq;
-  STile s;
+  STile<KH> s;
   auto run = [&](auto act) __attribute__((always_inline)) {
     constexpr bool ACT = decltype(act)::value;
     // prologue: K(ta), V(ta), K(ta+1) in flight; S(ta) = K(ta) Q^T; m = its exact column maxima
     {
-      const typename KvTiles<NW>::Slots s0 = kv.slots(ta * BK);
+      const typename KvTiles<NW, KH>::Slots s0 = kv.slots(ta * BK);
       kv.copy_k(ta * BK, smem, s0);
       kv.copy_v(ta * BK, smem + 2 * KT_BYTES, s0);
       if (ta + 1 < ntiles) kv.copy_k((ta + 1) * BK, smem + KT_BYTES, kv.slots((ta + 1) * BK));
@@ -642,11 +700,11 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) scale_q(g, qreg[qb]);
     if constexpr (ACT) {
-      qk_tile(smem, L, qreg, s, m);
-      if (ta + 1 == ntiles && ragged) mask_tile(s, ta * BK, nk, lg);
-      tile_max(s, m);
+      qk_tile<KH>(smem, L, qreg, s, m);
+      if (ta + 1 == ntiles && ragged) mask_tile<KH>(s, ta * BK, nk, lg);
+      tile_max<KH>(s, m);
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+      for (int h = 0; h < KH; ++h)
 #pragma unroll
         for (int b = 0; b < 2; ++b)
 #pragma unroll
@@ -659,45 +717,145 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const uint16
     // iteration t (buffer parity counted from ta): copy K(t+2) over K(t) and
     // V(t+1) over V(t-1), then step t
     int32_t t = ta;
-    typename KvTiles<NW>::Slots sk = kv.slots(min(ta + 2, it.ntiles - 1) * BK);
-    typename KvTiles<NW>::Slots sv = kv.slots(min(ta + 1, it.ntiles - 1) * BK);
+    typename KvTiles<NW, KH>::Slots sk = kv.slots(min(ta + 2, it.ntiles - 1) * BK);
+    typename KvTiles<NW, KH>::Slots sv = kv.slots(min(ta + 1, it.ntiles - 1) * BK);
     for (; t + 2 < ntiles; t += 2) {
       kv.copy_k((t + 2) * BK, smem, sk);
       kv.copy_v((t + 1) * BK, smem + 2 * KT_BYTES + VT_BYTES, sv);
       sk = kv.slots(min(t + 3, it.ntiles - 1) * BK);
       sv = kv.slots(min(t + 2, it.ntiles - 1) * BK);
-      if constexpr (ACT) attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
+      if constexpr (ACT) attn_step<KH, 1, 0, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
       landed();
       if (t + 3 < ntiles) kv.copy_k((t + 3) * BK, smem + KT_BYTES, sk);
       kv.copy_v((t + 2) * BK, smem + 2 * KT_BYTES, sv);
       sk = kv.slots(min(t + 4, it.ntiles - 1) * BK);
       sv = kv.slots(min(t + 3, it.ntiles - 1) * BK);
       if constexpr (ACT)
-        attn_step<0, 1, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, (t + 1) * BK, nk, lg);
+        attn_step<KH, 0, 1, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, (t + 1) * BK, nk, lg);
       landed();
     }
     if (t + 1 < ntiles) {  // two tiles left, parity 0
       kv.copy_v((t + 1) * BK, smem + 2 * KT_BYTES + VT_BYTES, sv);
-      if constexpr (ACT) attn_step<1, 0, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
+      if constexpr (ACT) attn_step<KH, 1, 0, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
       landed();
       ++t;
       if constexpr (ACT) {
         if (ragged)
-          attn_step<0, 1, false, true>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
+          attn_step<KH, 0, 1, false, true>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
         else
-          attn_step<0, 1, false, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
+          attn_step<KH, 0, 1, false, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
       }
     } else if constexpr (ACT) {  // one tile left, parity 0 (masking twice is harmless)
       if (ragged)
-        attn_step<1, 0, false, true>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
+        attn_step<KH, 1, 0, false, true>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
       else
-        attn_step<1, 0, false, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
+        attn_step<KH, 1, 0, false, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
     }
   };
-  if (active)
-    run(std::true_type{});
-  else
-    run(std::false_type{});
+  // The ring form: tile r of the item (key tile ta + r) sits in K slot and
+  // V^T slot r mod D.  Copies are issued in pairs (V(j), K(j + 1)), j = 1,
+  // 2, ...: pairs up to D - 2 in the prologue, pair r + D - 1 at step r into
+  // the slots steps r - 1 (V) and r - 1 (K, read by the QK of step r - 1)
+  // have finished with.  After step r, tiles K(r + 2) and V(r + 1) (pair
+  // r + 1) must have landed: the wait leaves the copies of the later pairs
+  // in flight, counted exactly (a pair past the item's end issues nothing).
+  auto run_ring = [&](auto act) __attribute__((always_inline)) {
+    constexpr bool ACT = decltype(act)::value;
+    using KV = KvTiles<NW, KH>;
+    constexpr int32_t KC = KV::KCP, VC = KV::VCP;
+    static_assert(KC % 4 == 0 && VC % 4 == 0 && (D - 2) * (KC + VC) <= 16, "wait counts of landed_but");
+    const int32_t n = ntiles - ta;
+    auto kbuf = [&](int32_t r) { return smem + (r % D) * KT_BYTES; };
+    auto vbuf = [&](int32_t r) { return smem + D * KT_BYTES + (r % D) * VT_BYTES; };
+    // copies of pair j (relative tiles); returns nothing, issues V(j) if it
+    // exists, then K(j + 1) if it exists
+    auto issue_pair = [&](int32_t j) __attribute__((always_inline)) {
+      if (j < n) kv.copy_v((ta + j) * BK, vbuf(j), kv.slots((ta + j) * BK));
+      if (j + 1 < n) kv.copy_k((ta + j + 1) * BK, kbuf(j + 1), kv.slots((ta + j + 1) * BK));
+    };
+    // copy instructions of pairs a .. b issued by this wave: V(j) for j < n,
+    // K(j + 1) for j < n - 1
+    auto copies = [&](int32_t a, int32_t b) {
+      return VC * max(0, min(b, n - 1) - a + 1) + KC * max(0, min(b, n - 2) - a + 1);
+    };
+    {
+      const typename KV::Slots s0 = kv.slots(ta * BK);
+      kv.copy_k(ta * BK, kbuf(0), s0);
+      kv.copy_v(ta * BK, vbuf(0), s0);
+      if (n > 1) kv.copy_k((ta + 1) * BK, kbuf(1), kv.slots((ta + 1) * BK));
+    }
+    if constexpr (ACT) {
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+        load_q(q, g, it.node, it.head, it.qt * BQ + wave * 32 + 16 * qb + c, lg, qreg[qb]);
+    }
+    landed();
+    for (int32_t j = 1; j <= D - 2; ++j) issue_pair(j);
+    if constexpr (ACT) {
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) scale_q(g, qreg[qb]);
+      qk_tile<KH>(kbuf(0), L, qreg, s, m);
+      if (n == 1 && ragged) mask_tile<KH>(s, ta * BK, nk, lg);
+      tile_max<KH>(s, m);
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) s[0][b][qb][r] -= m[qb];
+    } else {
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int ds = 0; ds < 4; ++ds) qreg[qb][ds] = bf16x8{};  // defined values for the exact redo
+    }
+    landed_but(copies(1, D - 2));  // K(ta) read by every wave before pair D - 1 overwrites its slot
+    for (int32_t r = 0; r + 1 < n; ++r) {
+      issue_pair(r + D - 1);
+      if constexpr (ACT) {
+        // step r with runtime slots: the same arithmetic as attn_step
+        bf16x8 pb[KH][2];
+        probs<KH>(s, pb);
+        STile<KH> sn;
+        qk_tile<KH>(kbuf(r + 1), L, qreg, sn, m);
+        if (r + 2 == n && ragged) mask_tile<KH>(sn, (ta + r + 1) * BK, nk, lg);
+        pv_tile<KH>(vbuf(r), L, pb, oacc);
+#pragma unroll
+        for (int h = 0; h < KH; ++h) {
+          lsum[0] = mfma16(ones, pb[h][0], lsum[0]);
+          lsum[1] = mfma16(ones, pb[h][1], lsum[1]);
+        }
+#pragma unroll
+        for (int h = 0; h < KH; ++h)
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb) s[h][b][qb] = sn[h][b][qb];
+      }
+      landed_but(copies(r + 2, r + D - 1));
+    }
+    if constexpr (ACT) {  // the last tile (already masked if ragged)
+      bf16x8 pb[KH][2];
+      probs<KH>(s, pb);
+      pv_tile<KH>(vbuf(n - 1), L, pb, oacc);
+#pragma unroll
+      for (int h = 0; h < KH; ++h) {
+        lsum[0] = mfma16(ones, pb[h][0], lsum[0]);
+        lsum[1] = mfma16(ones, pb[h][1], lsum[1]);
+      }
+    }
+  };
+  if constexpr (D == 2) {
+    if (active)
+      run(std::true_type{});
+    else
+      run(std::false_type{});
+  } else {
+    if (active)
+      run_ring(std::true_type{});
+    else
+      run_ring(std::false_type{});
+  }
   // the guard, on the final sums (also NaN / inf)
   const bool bad = __builtin_amdgcn_ballot_w64(!(lsum[0][0] < P_GUARD && lsum[1][0] < P_GUARD)) != 0;
   l[0] = lsum[0][0];  // zero outside lanes 0..15, so the group sum is the row sum
@@ -725,7 +883,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(uint16_t* __restrict_
   const int32_t dl = threadIdx.x & 31;
   const int32_t qrow = qt * BQ + lrow;
   if (qrow >= g.nq) return;
-  const int32_t nt = node_tiles(plan, g, node);
+  const int32_t nt = node_tiles<kh_of(BQ)>(plan, g, node);
   auto nonempty = [&](int32_t p) { return p * nt / g.tail_split < (p + 1) * nt / g.tail_split; };
   float m = -INFINITY;
   for (int32_t p = 0; p < g.tail_split; ++p)
@@ -755,33 +913,50 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(uint16_t* __restrict_
 // max_pieces pieces and no more pieces than the shortest node has key
 // tiles.
 struct TailSplit {
-  int32_t bq;       // queries per work-group of the shape used (128 or 256)
+  int32_t bq;       // queries per work-group of the shape used (64, 128 or 256)
+  int32_t ring;     // tiles of its K and V^T rings
   int32_t whole, tail, split;
 };
+// The work-group shape for nodes of nq queries: the smallest that holds them.
+static int32_t shape_queries(int32_t nq) { return nq <= BQ_TINY ? BQ_TINY : nq <= BQ_SMALL ? BQ_SMALL : BQ_MAX; }
+// Work-groups of a shape resident per CU: VGPRs allow two waves per SIMD;
+// LDS (160 KB) holds 2 ring x 8 KB per 64-query work-group.
+static int32_t per_cu(int32_t bq, int32_t ring) {
+  if (bq != BQ_TINY) return BQ_MAX / bq;
+  return ring == 3 ? 3 : 2;
+}
+// The 64-query shape keeps 3 tiles in flight per work-group when its units
+// fit the 512 work-groups resident with that ring, else 2 (768 resident).
+static int32_t ring_for(int32_t bq, int32_t units) {
+  if (bq != BQ_TINY) return 2;
+  return units <= kCUs * per_cu(bq, 4) ? 4 : 3;
+}
 static TailSplit tail_split(const sc_plan* p, const sc_cache* c, int32_t max_pieces = kAttnMaxPieces) {
   const int32_t n = (int32_t)p->nodes.size();
-  const int32_t bq = p->nq <= BQ_SMALL ? BQ_SMALL : BQ_MAX;
+  const int32_t bq = shape_queries(p->nq);
+  const int32_t bk = 32 * kh_of(bq);
   const int32_t n_qtiles = (p->nq + bq - 1) / bq;
   const int32_t units = n * c->d.n_heads * n_qtiles;
   int64_t tiles = 0;
   int32_t min_tiles = INT32_MAX;
   for (int32_t i = 0; i < n; ++i) {
     const int32_t nt = (int32_t)(((int64_t)(p->page_off[i + 1] - p->page_off[i]) * c->d.tokens_per_page +
-                                  BK - 1) / BK);
+                                  bk - 1) / bk);
     tiles += nt;
     min_tiles = std::min(min_tiles, nt);
   }
   const double mean_tiles = (double)tiles / std::max(n, 1);
   TailSplit ts;
   ts.bq = bq;
-  const int32_t slots = kCUs * (BQ_MAX / bq);  // work-groups resident at once
+  ts.ring = ring_for(bq, units);
+  const int32_t slots = kCUs * per_cu(bq, ts.ring);  // work-groups resident at once
   ts.tail = units % slots;
   ts.whole = units - ts.tail;
   ts.split = 1;
   // Short units are not cut: the combine launch and the partial traffic are
   // fixed costs that a few-tile unit cannot repay (measured on the short
-  // K/V streaming sweep).
-  if (ts.tail == 0 || mean_tiles < kAttnMinSplitTiles) return ts;
+  // K/V streaming sweep).  The threshold is in 64-key tiles.
+  if (ts.tail == 0 || mean_tiles * bk < kAttnMinSplitTiles * 64) return ts;
   double best = 1e30;
   const int32_t smax = std::max(1, std::min({16, max_pieces / ts.tail, min_tiles}));
   for (int32_t sp = 1; sp <= smax; ++sp) {
@@ -812,9 +987,10 @@ int attention_check(const sc_plan* p, const sc_cache* c) {
     return fail(SC_EUNSUPPORTED, "plan of %zu pages exceeds %d", p->page_slot.size(), kMaxPages);
   if (d.dtype == SC_DTYPE_F32) return SC_OK;
   if (d.head_dim != HDB) return fail(SC_EUNSUPPORTED, "bf16 attention needs head_dim 128");
-  if (d.tokens_per_page < BK)
-    return fail(SC_EUNSUPPORTED, "bf16 attention needs pages of >= %d tokens (got %d)", BK,
-                d.tokens_per_page);
+  const int32_t bk = 32 * kh_of(shape_queries(p->nq));  // a key tile spans at most two pages
+  if (d.tokens_per_page < bk)
+    return fail(SC_EUNSUPPORTED, "bf16 attention of %d-query nodes needs pages of >= %d tokens (got %d)",
+                p->nq, bk, d.tokens_per_page);
   if ((uint64_t)d.n_slots * c->slot_bytes > 0xffffffffull)
     return fail(SC_EUNSUPPORTED, "bf16 attention needs one layer of the pool within 4 GB");
   return SC_OK;
@@ -917,19 +1093,24 @@ static int launch_attention_pieces(const sc_plan* p, const sc_cache* c, int32_t 
   const uint16_t* qb = static_cast<const uint16_t*>(q);
   uint16_t* ob = static_cast<uint16_t*>(o);
   timer_begin(TK_ATTENTION, stream);
-  if (bq == BQ_SMALL)
-    hipLaunchKernelGGL(attn_bf16_kernel<4>, dim3(items), dim3(256), 0, stream, qb, ob, g, plan);
+  if (bq == BQ_TINY && ts.ring == 4)
+    hipLaunchKernelGGL((attn_bf16_kernel<2, 1, 4>), dim3(items), dim3(128), 0, stream, qb, ob, g, plan);
+  else if (bq == BQ_TINY)
+    hipLaunchKernelGGL((attn_bf16_kernel<2, 1, 3>), dim3(items), dim3(128), 0, stream, qb, ob, g, plan);
+  else if (bq == BQ_SMALL)
+    hipLaunchKernelGGL((attn_bf16_kernel<4, 2, 2>), dim3(items), dim3(256), 0, stream, qb, ob, g, plan);
   else
-    hipLaunchKernelGGL(attn_bf16_kernel<8>, dim3(items), dim3(512), 0, stream, qb, ob, g, plan);
+    hipLaunchKernelGGL((attn_bf16_kernel<8, 2, 2>), dim3(items), dim3(512), 0, stream, qb, ob, g, plan);
   timer_end(TK_ATTENTION, stream);
   if (g.tail_units) {
     timer_begin(TK_ATTN_COMBINE, stream);
-    if (bq == BQ_SMALL)
-      hipLaunchKernelGGL(attn_combine_kernel<BQ_SMALL>, dim3((uint32_t)g.tail_units, BQ_SMALL / 8), dim3(256),
-                         0, stream, ob, g, plan);
+    const dim3 grid((uint32_t)g.tail_units, (uint32_t)bq / 8);
+    if (bq == BQ_TINY)
+      hipLaunchKernelGGL(attn_combine_kernel<BQ_TINY>, grid, dim3(256), 0, stream, ob, g, plan);
+    else if (bq == BQ_SMALL)
+      hipLaunchKernelGGL(attn_combine_kernel<BQ_SMALL>, grid, dim3(256), 0, stream, ob, g, plan);
     else
-      hipLaunchKernelGGL(attn_combine_kernel<BQ_MAX>, dim3((uint32_t)g.tail_units, BQ_MAX / 8), dim3(256), 0,
-                         stream, ob, g, plan);
+      hipLaunchKernelGGL(attn_combine_kernel<BQ_MAX>, grid, dim3(256), 0, stream, ob, g, plan);
     timer_end(TK_ATTN_COMBINE, stream);
   }
   SC_HIP(hipGetLastError());
@@ -980,7 +1161,7 @@ extern "C" int sc_attention_noalloc(const sc_plan* p, const sc_cache* c, int32_t
   void* ptr = nullptr;
   if (c->d.dtype == SC_DTYPE_BF16 && (rc = scratch_address(&ptr)) != SC_OK) return rc;
   // as many key-range pieces as the scratch holds partials for
-  const int32_t bq = p->nq <= BQ_SMALL ? BQ_SMALL : BQ_MAX;
+  const int32_t bq = shape_queries(p->nq);
   const size_t piece_bytes = (size_t)bq * (HDB + 2) * sizeof(float);
   const int32_t max_pieces = (int32_t)std::min<size_t>(kAttnMaxPieces, kNoAllocScratchBytes / piece_bytes);
   const TailSplit ts = tail_split(p, c, max_pieces);

@@ -57,6 +57,13 @@ SHORT = Geometry(heads=2, head_dim=128, grid_h=8, grid_w=12, frames_per_chunk=1,
                  hidden=256, mlp=512)
 
 
+# Narrow nodes (one 40-token latent frame per chunk, 40 queries): the
+# 64-query work-group shape of the bf16 kernel with its 32-key tiles, pages
+# (40 tokens) that end inside tiles and ragged last tiles.
+NARROW = Geometry(heads=2, head_dim=128, grid_h=5, grid_w=8, frames_per_chunk=1, K=4, W=6,
+                  hidden=256, mlp=512)
+
+
 def kv_stream(nq: int, W: int = 20) -> Geometry:
     """Short-context K/V streaming shape: Wan heads (12 x 128), one latent
     frame of ``nq`` tokens per chunk, up to W + 1 = 21 pages per node."""

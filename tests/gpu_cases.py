@@ -107,6 +107,7 @@ class AttnCase:
     def run(self):
         torch = torch_mod()
         nws = sc.sc_attention_workspace_bytes(self.plan, self.cache)
+        self.workspace_bytes = nws
         # stale contents must not matter: fill the workspace with NaN bytes
         ws = torch.full((max(nws, 1),), 0xFF, dtype=torch.uint8, device="cuda")
         sc.sc_attention(self.plan, self.cache, self.layer, self.q_dev, self.o_dev, self.scale,

@@ -1,8 +1,10 @@
 """GPU parity of the packed paged attention against the CPU oracle.
 
 Covers the tiny fp32 case (every node of 4 chunks x 5 levels under all three
-policies, several pack shapes), small bf16 packs whose pages (40 tokens) leave
-ragged tails inside 64-key tiles, the Wan-shaped clean / same-level /
+policies, several pack shapes), small bf16 packs on each work-group shape
+(256, 128 and 64 queries) whose pages (104, 96 and 40 tokens) leave ragged
+tails inside key tiles, the short-context streaming shape whole and cut into
+key-range pieces, the Wan-shaped clean / same-level /
 progressive packs on sampled rows, the segment probe, negative controls
 (mistakes planted in the oracle must fail the gates), NaN poisoning of
 unused slots, packed vs sequential, run-to-run determinism and the workspace
@@ -18,7 +20,8 @@ from oracle.attention import node_attention
 from oracle.pipeline import pipeline_rounds
 from oracle.policy import policy as oracle_policy
 from oracle.policy import select
-from synth.configs import SHORT, SMALL, TINY, WAN, cfg2_clean, cfg3_same, cfg4_prog, kv_stream
+from synth.configs import (NARROW, SHORT, SMALL, TINY, WAN, cfg2_clean, cfg3_same, cfg4_prog,
+                           kv_stream)
 
 from gpu_cases import (AttnCase, BF16_MAX_ABS, F32_MAX_ABS, bf16_gates, from_device, sample_rows,
                        to_device, torch_mod)
@@ -74,6 +77,46 @@ def test_short_bf16_packs(kind, pack, resident):
     out = case.run()
     for i in range(len(pack)):
         bf16_gates(out[i], case.oracle(i), f"short {kind} node {pack[i]}")
+
+
+@pytest.mark.parametrize("kind,pack,resident", SMALL_PACKS)
+def test_narrow_bf16_packs(kind, pack, resident):
+    """Nodes of 40 queries run on the 64-query (2-wave, 32-key tile) shape."""
+    case = AttnCase(NARROW, sc.SC_DTYPE_BF16, kind, pack, resident, seed=12)
+    out = case.run()
+    for i in range(len(pack)):
+        bf16_gates(out[i], case.oracle(i), f"narrow {kind} node {pack[i]}")
+
+
+def test_narrow_long_windows_cut_into_pieces():
+    """64-query nodes over 41 pages of 64 keys (2624 keys, 82 tiles of 32):
+    the 36 units of three nodes are cut into key-range pieces (a workspace is
+    needed) and merged; every row against the oracle."""
+    geo = kv_stream(64, W=40)
+    W = geo.W
+    pack = [(41 * i + W, 4) for i in range(3)]
+    resident = [(41 * i + r, 0) for i in range(3) for r in range(W)]
+    case = AttnCase(geo, sc.SC_DTYPE_BF16, "clean", pack, resident, seed=13)
+    out = case.run()
+    assert case.workspace_bytes > 0
+    for i in range(len(pack)):
+        bf16_gates(out[i], case.oracle(i), f"narrow pieces node {pack[i]}")
+
+
+@pytest.mark.parametrize("heads", [12, 16])
+def test_narrow_many_units(heads):
+    """64 one-frame nodes of 64 queries over 3 pages each: 768 units (12
+    heads) run at once on the 64-query shape's 2-tile-in-flight ring; 1024
+    (16 heads) take more than one round of it.  Nodes 0, 21, 42 and 63
+    checked against the oracle."""
+    geo = dataclasses.replace(kv_stream(64, W=2), heads=heads)
+    pack = [(3 * i + 2, 4) for i in range(64)]
+    resident = [(3 * i + r, 0) for i in range(64) for r in range(2)]
+    case = AttnCase(geo, sc.SC_DTYPE_BF16, "clean", pack, resident, seed=14)
+    out = case.run()
+    assert case.workspace_bytes == 0
+    for i in (0, 21, 42, 63):
+        bf16_gates(out[i], case.oracle(i), f"narrow {heads} heads node {pack[i]}")
 
 
 @pytest.mark.parametrize("nq", [64, 128])
@@ -206,7 +249,7 @@ def test_negative_controls_fail_gates():
             bf16_gates(out[node], want, name)
 
 
-@pytest.mark.parametrize("geo", [SMALL, SHORT], ids=["256-query", "128-query"])
+@pytest.mark.parametrize("geo", [SMALL, SHORT, NARROW], ids=["256-query", "128-query", "64-query"])
 def test_logits_far_above_first_tile(geo):
     """K channel 0 is 0 on each node's first page and 600 on most later
     pages (first page of every state for three-frame chunks; chunks 0..3,

@@ -180,23 +180,29 @@ def test_stale_plan_detected_on_cpu():
 def test_attention_workspace_size():
     """Workspace of the bf16 attention: units (head, node, query tile) that
     fill whole rounds of the CUs' work-group slots run whole; when units are
-    long (a mean of at least 32 key tiles) the remaining units are cut into S
-    pieces, each leaving a partial (one row per query of the tile: 128 fp32
-    outputs plus max and sum).  Nodes of at most 128 queries use 128-query
-    tiles (512 slots), larger ones 256-query tiles (256 slots).  S minimises
-    the tail's rounds plus a per-piece cost of two key tiles, within 1024
-    pieces and the shortest node's key tiles.  No workspace for fp32 caches
-    or when nothing is cut."""
+    long (a mean of at least 2048 keys, 32 key tiles of 64) the remaining
+    units are cut into S pieces, each leaving a partial (one row per query of
+    the tile: 128 fp32 outputs plus max and sum).  Nodes of at most 64
+    queries use 64-query tiles with 32-key tiles (1024 slots), of at most 128
+    128-query tiles (512 slots), larger ones 256-query tiles (256 slots), the
+    last two with 64-key tiles.  S minimises the tail's rounds plus a
+    per-piece cost of two key tiles, within 1024 pieces and the shortest
+    node's key tiles.  No workspace for fp32 caches or when nothing is cut."""
     row = (128 + 2) * 4
     cache = sc.sc_cache_create(0x100000, 1, 2, 128, 64, 1, 64)      # 64 queries per node
     plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(0, 0)]), cache)
-    assert sc.sc_attention_workspace_bytes(plan, cache) == 0          # 1 key tile: no cut
+    assert sc.sc_attention_workspace_bytes(plan, cache) == 0          # 2 key tiles: no cut
     sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(c, 0) for c in range(1, 40)]), cache)
     plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 3, [(40, 4)]), cache)
-    assert sc.sc_attention_workspace_bytes(plan, cache) == 0          # 4 tiles: too short to cut
+    assert sc.sc_attention_workspace_bytes(plan, cache) == 0          # 256 keys: too short to cut
     plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 39, [(40, 4)]), cache)
-    # 2 units of 40 tiles: S = 16 (one round of sixteenths + 16 x 2/40 overhead)
-    assert sc.sc_attention_workspace_bytes(plan, cache) == 2 * 16 * 128 * row
+    # 2 units of 2560 keys (80 tiles of 32): S = 16 (one round of sixteenths + 16 x 2/80 overhead)
+    assert sc.sc_attention_workspace_bytes(plan, cache) == 2 * 16 * 64 * row
+    mid = sc.sc_cache_create(0x100000, 1, 2, 128, 128, 1, 64)       # 128 queries per node
+    sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(c, 0) for c in range(20)]), mid)
+    plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 20, [(20, 4)]), mid)
+    # 2 units of 2688 keys (42 tiles of 64): S = 16
+    assert sc.sc_attention_workspace_bytes(plan, mid) == 2 * 16 * 128 * row
     wide = sc.sc_cache_create(0x100000, 1, 2, 128, 160, 1, 64)      # 160 queries per node
     sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(c, 0) for c in range(13)]), wide)
     plan = sc.sc_plan_build(sc.sc_selection_build("clean", 4, 13, [(13, 4)]), wide)
@@ -325,8 +331,9 @@ def test_condition_append_and_cross_block_checks_without_device():
             sc.sc_block_forward(bw, cache, 0, plan, 0x6000, None, 0x7000, ws_bytes)
         assert e.value.code == code, (cross, qk)
     assert not cache.contains((0, 4), 0)                  # nothing was written
-    # a condition shorter than one 64-key tile has no bf16 kernel
-    short = sc.sc_cache_create(0x400000, 1, 2, 128, 32, 1, 1)
+    # condition pages shorter than one key tile (32 keys for nodes of at most
+    # 64 queries, 64 keys above) have no bf16 kernel
+    short = sc.sc_cache_create(0x400000, 1, 2, 128, 24, 1, 1)
     sc.sc_plan_build(sc.sc_selection_build("clean", 4, 0, [(0, 0)]), short)
     sp = sc.sc_plan_condition(short, [(0, 0), (0, 0)], 64)
     bw = sc.BlockWeights(D, 2, 128, 512, 0x1000, 0x2000, 0x3000, 0x4000,
