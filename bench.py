@@ -380,7 +380,8 @@ def bench_kv_stream(args):
     pages each, windows disjoint between nodes so every page is read by one
     node only.  Arithmetic intensity is about Nq FLOP per byte of K/V, below
     the bf16 ridge, so the attention streams K/V at HBM speed.  Reports, per
-    (Nq, P): kernel time, algorithmic bytes (K/V of the visible pages, Q, O)
+    (Nq, P): the time per launch of back-to-back launches (and with events
+    around each launch), algorithmic bytes (K/V of the visible pages, Q, O)
     and GB/s against 8 TB/s."""
     import numpy as np
     import torch
@@ -420,23 +421,36 @@ def bench_kv_stream(args):
             for _ in range(3):
                 sc.sc_attention(plan, cache, 0, q, o, scale, ws, nws)
             torch.cuda.synchronize()
+            # (a) back-to-back launches between two events: the time per
+            # launch of a stream of them
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(args.steps):
+                sc.sc_attention(plan, cache, 0, q, o, scale, ws, nws)
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / args.steps
+            # (b) events around each launch (main kernel plus combine)
             sc.sc_timer_enable(True)
             for _ in range(args.steps):
                 sc.sc_attention(plan, cache, 0, q, o, scale, ws, nws)
             n, tot = sc.sc_timer_read("attention")
             nc, totc = sc.sc_timer_read("attention_combine")
             sc.sc_timer_enable(False)
-            ms = (tot + totc) / n
+            ms_each = (tot + totc) / n
             kv_bytes = n_nodes * P * g.heads * nq * g.head_dim * 2 * 2
             qo_bytes = 2 * n_nodes * nq * g.heads * g.head_dim * 2
             flops = 4.0 * g.head_dim * g.heads * n_nodes * nq * P * nq
             gbs = (kv_bytes + qo_bytes) / (ms * 1e-3) / 1e9
             rows.append({"nq": nq, "pages": P, "nodes": n_nodes, "ms": round(ms, 4),
+                         "ms_event_each": round(ms_each, 4),
                          "kv_mb": round(kv_bytes / 1e6, 1), "gb_s": round(gbs, 1),
+                         "gb_s_event_each": round((kv_bytes + qo_bytes) / (ms_each * 1e-3) / 1e9, 1),
                          "frac_hbm": round(gbs / PEAK_HBM_GBS, 3),
                          "tflops": round(flops / (ms * 1e-3) / 1e12, 1)})
-            log(f"[bench] kv stream nq={nq} pages={P} nodes={n_nodes}: {ms:.4f} ms, "
-                f"{gbs:.0f} GB/s, {rows[-1]['tflops']} TFLOP/s")
+            log(f"[bench] kv stream nq={nq} pages={P} nodes={n_nodes}: {ms:.4f} ms per launch "
+                f"back to back ({ms_each:.4f} with events around each), {gbs:.0f} GB/s, "
+                f"{rows[-1]['tflops']} TFLOP/s")
             del cache, pool
     return rows
 

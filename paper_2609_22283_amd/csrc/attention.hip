@@ -111,7 +111,6 @@ struct Tile {
   static constexpr int VT_BYTES = HDB * BK * 2;       // V^T tile: 128 rows of 2 BK bytes
 };
 constexpr int BQ_TINY = 64, BQ_SMALL = 128, BQ_MAX = 256;  // queries per work-group of the three shapes
-constexpr int kh_of(int bq) { return bq == BQ_TINY ? 1 : 2; }
 // Softmax bookkeeping.  Q is pre-scaled by scale*log2(e), so S is in log2
 // units, and each S tile starts its accumulation at -m: p = exp2(S)
 // directly.  m is the exact maximum of the work item's first tile and is
@@ -413,18 +412,21 @@ __device__ __forceinline__ void landed() {  // this wave's copies are in LDS, th
 }
 
 // The same for all but this wave's n most recent vector-memory operations (a
-// wave's loads complete in issue order for this counter), n a multiple of 4
-// up to 16 (wave-uniform).  The barrier is issued without __syncthreads'
-// release fence, which would wait for every outstanding copy; the memory
-// clobber keeps the compiler from moving LDS accesses across it.
+// wave's loads complete in issue order for this counter), n even, at most
+// 16 (wave-uniform).  The barrier is issued without __syncthreads' release
+// fence, which would wait for every outstanding copy; the memory clobber
+// keeps the compiler from moving LDS accesses across it.
 __device__ __forceinline__ void landed_but(int32_t n) {
+#define SC_LANDED_BUT(k) \
+  case k:                \
+    asm volatile("s_waitcnt vmcnt(" #k ")\n\ts_barrier" ::: "memory"); \
+    break;
   switch (n) {
-    case 0: asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory"); break;
-    case 4: asm volatile("s_waitcnt vmcnt(4)\n\ts_barrier" ::: "memory"); break;
-    case 8: asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory"); break;
-    case 12: asm volatile("s_waitcnt vmcnt(12)\n\ts_barrier" ::: "memory"); break;
-    default: asm volatile("s_waitcnt vmcnt(16)\n\ts_barrier" ::: "memory"); break;
+    SC_LANDED_BUT(2) SC_LANDED_BUT(4) SC_LANDED_BUT(6) SC_LANDED_BUT(8) SC_LANDED_BUT(10)
+    SC_LANDED_BUT(12) SC_LANDED_BUT(14) SC_LANDED_BUT(16)
+    default: asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory"); break;
   }
+#undef SC_LANDED_BUT
 }
 
 // Schedule.  A unit is a (head, query tile, node) triple, numbered head-major
@@ -641,12 +643,13 @@ __device__ __forceinline__ void attn_exact(char* smem, const KvTiles<NW, KH>& kv
 }
 
 // NW = 8: 256 queries per work-group, one work-group per CU; NW = 4: 128
-// queries, two per CU; both keep two waves per SIMD.  NW = 2: 64 queries on
-// 32-key tiles (KH = 1), three or two per CU.  Each wave owns two 16-query
-// blocks.  D: tiles of the K and of the V^T ring.  With D = 2 the loop below
-// keeps one tile in flight, its buffer parity unrolled; the 64-query shape
-// runs D = 3 or 4 (runtime ring slots, D - 1 tiles in flight): its nodes
-// are short and streamed, so it trades resident waves for copies in flight.
+// queries, two per CU; NW = 2: 64 queries, three or two per CU.  Each wave
+// owns two 16-query blocks.  KH: 32-key halves per key tile; D: tiles of the
+// K and of the V^T ring.  The long-context form (KH = 2, D = 2; NW = 8, 4)
+// keeps one tile in flight, its buffer parity unrolled, two waves per SIMD.
+// The streaming form (KH = 1, D = 3 or 4: runtime ring slots, D - 1 tiles in
+// flight; NW = 2) serves nodes of at most 64 queries, whose attention
+// streams K/V from HBM: it trades resident waves for copies in flight.
 template <int NW, int KH, int D>
 __global__ __launch_bounds__(64 * NW, NW == 8 || D == 4 ? 1 : 2) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                                     uint16_t* __restrict__ o, AttnGeom g,
@@ -763,7 +766,7 @@ __global__ __launch_bounds__(64 * NW, NW == 8 || D == 4 ? 1 : 2) void attn_bf16_
     constexpr bool ACT = decltype(act)::value;
     using KV = KvTiles<NW, KH>;
     constexpr int32_t KC = KV::KCP, VC = KV::VCP;
-    static_assert(KC % 4 == 0 && VC % 4 == 0 && (D - 2) * (KC + VC) <= 16, "wait counts of landed_but");
+    static_assert(KC % 2 == 0 && VC % 2 == 0 && (D - 2) * (KC + VC) <= 16, "wait counts of landed_but");
     const int32_t n = ntiles - ta;
     auto kbuf = [&](int32_t r) { return smem + (r % D) * KT_BYTES; };
     auto vbuf = [&](int32_t r) { return smem + D * KT_BYTES + (r % D) * VT_BYTES; };
@@ -872,7 +875,7 @@ __global__ __launch_bounds__(64 * NW, NW == 8 || D == 4 ? 1 : 2) void attn_bf16_
 // 128 outputs, so every partial row is read as one contiguous 512-byte run.
 // With m = max m_p:
 //   O = sum_p 2^(m_p - m) O_p / sum_p 2^(m_p - m) l_p.
-template <int BQ>
+template <int BQ, int KH>
 __global__ __launch_bounds__(256) void attn_combine_kernel(uint16_t* __restrict__ o, AttnGeom g, AttnPlan plan) {
   const int32_t tu = blockIdx.x;
   const int32_t unit = g.whole_units + tu;
@@ -883,7 +886,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(uint16_t* __restrict_
   const int32_t dl = threadIdx.x & 31;
   const int32_t qrow = qt * BQ + lrow;
   if (qrow >= g.nq) return;
-  const int32_t nt = node_tiles<kh_of(BQ)>(plan, g, node);
+  const int32_t nt = node_tiles<KH>(plan, g, node);
   auto nonempty = [&](int32_t p) { return p * nt / g.tail_split < (p + 1) * nt / g.tail_split; };
   float m = -INFINITY;
   for (int32_t p = 0; p < g.tail_split; ++p)
@@ -912,29 +915,46 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(uint16_t* __restrict_
 // cost of about two key tiles (prologue and partial write), with at most
 // max_pieces pieces and no more pieces than the shortest node has key
 // tiles.
+// The kernel form for a plan: queries per work-group (the smallest of 64,
+// 128, 256 that holds a node), 32-key halves per key tile and ring depth.
+// Nodes of at most 64 queries take the streaming form (ring 4 when the units
+// fit the 512 work-groups resident with it, else ring 3 with 768); larger
+// ones the long-context form.  (The streaming form with 128 queries per
+// work-group measured 2-8 % slower than the long-context one on the
+// short-context sweep: its 32-key steps cost more than the deeper ring
+// gains.)
+struct AttnShape {
+  int32_t bq, kh, ring;
+};
+static int32_t shape_queries(int32_t nq) { return nq <= BQ_TINY ? BQ_TINY : nq <= BQ_SMALL ? BQ_SMALL : BQ_MAX; }
+// Work-groups resident per CU: at most 8 waves (256 VGPRs each, 2 per SIMD)
+// and 160 KB of LDS, 2 x ring x 8 KB per streaming work-group.
+static int32_t per_cu(const AttnShape& s) {
+  const int32_t by_vgpr = 8 / (s.bq / 32);
+  return s.kh == 2 ? by_vgpr : std::min(by_vgpr, (160 * 1024) / (s.ring * 16 * 1024 + 4));
+}
+static AttnShape attn_shape(const sc_plan* p, const sc_cache* c) {
+  AttnShape s;
+  s.bq = shape_queries(p->nq);
+  s.kh = s.bq == BQ_TINY ? 1 : 2;
+  s.ring = 2;
+  if (s.kh == 1) {
+    const int32_t units = (int32_t)p->nodes.size() * c->d.n_heads * ((p->nq + s.bq - 1) / s.bq);
+    s.ring = 4;
+    if (units > kCUs * per_cu(s)) s.ring = 3;
+  }
+  return s;
+}
+
 struct TailSplit {
-  int32_t bq;       // queries per work-group of the shape used (64, 128 or 256)
-  int32_t ring;     // tiles of its K and V^T rings
+  AttnShape sh;
   int32_t whole, tail, split;
 };
-// The work-group shape for nodes of nq queries: the smallest that holds them.
-static int32_t shape_queries(int32_t nq) { return nq <= BQ_TINY ? BQ_TINY : nq <= BQ_SMALL ? BQ_SMALL : BQ_MAX; }
-// Work-groups of a shape resident per CU: VGPRs allow two waves per SIMD;
-// LDS (160 KB) holds 2 ring x 8 KB per 64-query work-group.
-static int32_t per_cu(int32_t bq, int32_t ring) {
-  if (bq != BQ_TINY) return BQ_MAX / bq;
-  return ring == 3 ? 3 : 2;
-}
-// The 64-query shape keeps 3 tiles in flight per work-group when its units
-// fit the 512 work-groups resident with that ring, else 2 (768 resident).
-static int32_t ring_for(int32_t bq, int32_t units) {
-  if (bq != BQ_TINY) return 2;
-  return units <= kCUs * per_cu(bq, 4) ? 4 : 3;
-}
 static TailSplit tail_split(const sc_plan* p, const sc_cache* c, int32_t max_pieces = kAttnMaxPieces) {
   const int32_t n = (int32_t)p->nodes.size();
-  const int32_t bq = shape_queries(p->nq);
-  const int32_t bk = 32 * kh_of(bq);
+  TailSplit ts;
+  ts.sh = attn_shape(p, c);
+  const int32_t bq = ts.sh.bq, bk = 32 * ts.sh.kh;
   const int32_t n_qtiles = (p->nq + bq - 1) / bq;
   const int32_t units = n * c->d.n_heads * n_qtiles;
   int64_t tiles = 0;
@@ -946,10 +966,7 @@ static TailSplit tail_split(const sc_plan* p, const sc_cache* c, int32_t max_pie
     min_tiles = std::min(min_tiles, nt);
   }
   const double mean_tiles = (double)tiles / std::max(n, 1);
-  TailSplit ts;
-  ts.bq = bq;
-  ts.ring = ring_for(bq, units);
-  const int32_t slots = kCUs * per_cu(bq, ts.ring);  // work-groups resident at once
+  const int32_t slots = kCUs * per_cu(ts.sh);  // work-groups resident at once
   ts.tail = units % slots;
   ts.whole = units - ts.tail;
   ts.split = 1;
@@ -974,7 +991,7 @@ size_t attention_workspace_bytes(const sc_plan* p, const sc_cache* c) {
   if (c->d.dtype != SC_DTYPE_BF16 || p->nodes.empty()) return 0;
   const TailSplit ts = tail_split(p, c);
   if (ts.split == 1) return 0;
-  return (size_t)ts.tail * ts.split * ts.bq * (HDB + 2) * sizeof(float);
+  return (size_t)ts.tail * ts.split * ts.sh.bq * (HDB + 2) * sizeof(float);
 }
 
 size_t attention_workspace_bound() { return (size_t)kAttnMaxPieces * BQ_MAX * (HDB + 2) * sizeof(float); }
@@ -987,7 +1004,7 @@ int attention_check(const sc_plan* p, const sc_cache* c) {
     return fail(SC_EUNSUPPORTED, "plan of %zu pages exceeds %d", p->page_slot.size(), kMaxPages);
   if (d.dtype == SC_DTYPE_F32) return SC_OK;
   if (d.head_dim != HDB) return fail(SC_EUNSUPPORTED, "bf16 attention needs head_dim 128");
-  const int32_t bk = 32 * kh_of(shape_queries(p->nq));  // a key tile spans at most two pages
+  const int32_t bk = 32 * attn_shape(p, c).kh;  // a key tile spans at most two pages
   if (d.tokens_per_page < bk)
     return fail(SC_EUNSUPPORTED, "bf16 attention of %d-query nodes needs pages of >= %d tokens (got %d)",
                 p->nq, bk, d.tokens_per_page);
@@ -1003,29 +1020,36 @@ int attention_check(const sc_plan* p, const sc_cache* c) {
 // or same-level pack read overlapping windows of consecutive chunks; rotated
 // this way, their work-groups read the shared states at the same time
 // instead of one chunk apart.
+// The order is a property of the plan alone: computed on its first launch
+// and kept in it (a plan is immutable once built).
 static void shared_order(const sc_plan* p, AttnPlan& plan) {
   const int32_t n = (int32_t)p->nodes.size();
-  std::map<StateKey, int32_t> readers;
-  for (int32_t i = 0; i < n; ++i)
-    for (int32_t q = p->page_off[i]; q < p->page_off[i + 1]; ++q)
-      if (q == p->page_off[i] || p->page_state[q] != p->page_state[q - 1]) ++readers[p->page_state[q]];
-  StateKey anchor(INT32_MIN, INT32_MIN);
-  int32_t most = 0;
-  for (const auto& kv : readers)  // ascending (chunk, level): the oldest wins ties
-    if (kv.second > most) {
-      most = kv.second;
-      anchor = kv.first;
+  if (p->attn_slot.size() != p->page_slot.size()) {
+    std::map<StateKey, int32_t> readers;
+    for (int32_t i = 0; i < n; ++i)
+      for (int32_t q = p->page_off[i]; q < p->page_off[i + 1]; ++q)
+        if (q == p->page_off[i] || p->page_state[q] != p->page_state[q - 1]) ++readers[p->page_state[q]];
+    StateKey anchor(INT32_MIN, INT32_MIN);
+    int32_t most = 0;
+    for (const auto& kv : readers)  // ascending (chunk, level): the oldest wins ties
+      if (kv.second > most) {
+        most = kv.second;
+        anchor = kv.first;
+      }
+    std::vector<int32_t> order(p->page_slot.size());
+    for (int32_t i = 0; i < n; ++i) {
+      const int32_t a = p->page_off[i], b = p->page_off[i + 1];
+      int32_t r = a;
+      while (r < b && p->page_state[r] < anchor) ++r;
+      if (r == b) r = a;
+      int32_t o = a;
+      for (int32_t q = r; q < b; ++q) order[o++] = p->page_slot[q];
+      for (int32_t q = a; q < r; ++q) order[o++] = p->page_slot[q];
     }
-  for (int32_t i = 0; i <= n; ++i) plan.page_off[i] = p->page_off[i];
-  for (int32_t i = 0; i < n; ++i) {
-    const int32_t a = p->page_off[i], b = p->page_off[i + 1];
-    int32_t r = a;
-    while (r < b && p->page_state[r] < anchor) ++r;
-    if (r == b) r = a;
-    int32_t o = a;
-    for (int32_t q = r; q < b; ++q) plan.page_slot[o++] = p->page_slot[q];
-    for (int32_t q = a; q < r; ++q) plan.page_slot[o++] = p->page_slot[q];
+    p->attn_slot.swap(order);
   }
+  for (int32_t i = 0; i <= n; ++i) plan.page_off[i] = p->page_off[i];
+  std::copy(p->attn_slot.begin(), p->attn_slot.end(), plan.page_slot);
 }
 
 // The launch of a plan whose split uses at most max_pieces pieces.
@@ -1074,11 +1098,11 @@ static int launch_attention_pieces(const sc_plan* p, const sc_cache* c, int32_t 
     return SC_OK;
   }
   const TailSplit ts = tail_split(p, c, max_pieces);
-  const size_t need = ts.split == 1 ? 0 : (size_t)ts.tail * ts.split * ts.bq * (HDB + 2) * sizeof(float);
+  const size_t need = ts.split == 1 ? 0 : (size_t)ts.tail * ts.split * ts.sh.bq * (HDB + 2) * sizeof(float);
   if (ws_bytes < need || (need && !ws))
     return fail(SC_EINVAL, "attention workspace of %zu bytes, need %zu", ws_bytes, need);
   if (reinterpret_cast<uintptr_t>(ws) & 15) return fail(SC_EINVAL, "workspace must be 16-byte aligned");
-  const int32_t bq = ts.bq;
+  const int32_t bq = ts.sh.bq;
   g.n_qtiles = (p->nq + bq - 1) / bq;
   g.whole_units = ts.whole;
   g.tail_units = ts.tail;
@@ -1093,7 +1117,8 @@ static int launch_attention_pieces(const sc_plan* p, const sc_cache* c, int32_t 
   const uint16_t* qb = static_cast<const uint16_t*>(q);
   uint16_t* ob = static_cast<uint16_t*>(o);
   timer_begin(TK_ATTENTION, stream);
-  if (bq == BQ_TINY && ts.ring == 4)
+  const int32_t ring = ts.sh.ring;
+  if (bq == BQ_TINY && ring == 4)
     hipLaunchKernelGGL((attn_bf16_kernel<2, 1, 4>), dim3(items), dim3(128), 0, stream, qb, ob, g, plan);
   else if (bq == BQ_TINY)
     hipLaunchKernelGGL((attn_bf16_kernel<2, 1, 3>), dim3(items), dim3(128), 0, stream, qb, ob, g, plan);
@@ -1106,11 +1131,11 @@ static int launch_attention_pieces(const sc_plan* p, const sc_cache* c, int32_t 
     timer_begin(TK_ATTN_COMBINE, stream);
     const dim3 grid((uint32_t)g.tail_units, (uint32_t)bq / 8);
     if (bq == BQ_TINY)
-      hipLaunchKernelGGL(attn_combine_kernel<BQ_TINY>, grid, dim3(256), 0, stream, ob, g, plan);
+      hipLaunchKernelGGL((attn_combine_kernel<BQ_TINY, 1>), grid, dim3(256), 0, stream, ob, g, plan);
     else if (bq == BQ_SMALL)
-      hipLaunchKernelGGL(attn_combine_kernel<BQ_SMALL>, grid, dim3(256), 0, stream, ob, g, plan);
+      hipLaunchKernelGGL((attn_combine_kernel<BQ_SMALL, 2>), grid, dim3(256), 0, stream, ob, g, plan);
     else
-      hipLaunchKernelGGL(attn_combine_kernel<BQ_MAX>, grid, dim3(256), 0, stream, ob, g, plan);
+      hipLaunchKernelGGL((attn_combine_kernel<BQ_MAX, 2>), grid, dim3(256), 0, stream, ob, g, plan);
     timer_end(TK_ATTN_COMBINE, stream);
   }
   SC_HIP(hipGetLastError());
@@ -1161,7 +1186,7 @@ extern "C" int sc_attention_noalloc(const sc_plan* p, const sc_cache* c, int32_t
   void* ptr = nullptr;
   if (c->d.dtype == SC_DTYPE_BF16 && (rc = scratch_address(&ptr)) != SC_OK) return rc;
   // as many key-range pieces as the scratch holds partials for
-  const int32_t bq = shape_queries(p->nq);
+  const int32_t bq = attn_shape(p, c).bq;
   const size_t piece_bytes = (size_t)bq * (HDB + 2) * sizeof(float);
   const int32_t max_pieces = (int32_t)std::min<size_t>(kAttnMaxPieces, kNoAllocScratchBytes / piece_bytes);
   const TailSplit ts = tail_split(p, c, max_pieces);

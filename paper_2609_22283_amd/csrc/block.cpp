@@ -261,7 +261,7 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
   // only now are the pack's K/V of this layer complete: a failed call leaves
   // them unwritten, so the caller can run the block again
   for (int32_t i = 0; i < n; ++i)
-    c->states.at(StateKey(p->nodes[i].chunk, p->nodes[i].level)).written[layer] = 1;
+    set_written(c, c->states.at(StateKey(p->nodes[i].chunk, p->nodes[i].level)), layer, 1);
   return SC_OK;
 }
 

@@ -36,13 +36,18 @@ int plan_check(const sc_plan* plan, const sc_cache* cache, int32_t layer) {
     if (!cache->used[s] || cache->gen[s] != plan->page_gen[p])
       return fail(SC_ESTALE, "slot %d was released after the plan was built", s);
   }
-  for (size_t p = 0; p < plan->page_state.size(); ++p) {
-    auto it = cache->states.find(plan->page_state[p]);
-    if (it == cache->states.end() || !it->second.written[layer])
+  // every slot is still the one planned (above), so its flag is its state's
+  const uint8_t* wr = cache->slot_written.data() + (size_t)layer * cache->d.n_slots;
+  for (size_t p = 0; p < plan->page_slot.size(); ++p)
+    if (!wr[plan->page_slot[p]])
       return fail(SC_EUNAVAILABLE, "state (%d,%d) has no K/V at layer %d",
                   plan->page_state[p].first, plan->page_state[p].second, layer);
-  }
   return SC_OK;
+}
+
+void set_written(sc_cache* cache, StateEntry& e, int32_t layer, uint8_t v) {
+  e.written[layer] = v;
+  for (int32_t s : e.slots) cache->slot_written[(size_t)layer * cache->d.n_slots + s] = v;
 }
 
 int policy_check(const sc_policy* p) {
@@ -230,6 +235,7 @@ int sc_cache_create(const sc_cache_desc* d, void* pool, sc_cache** out) {
   c->used.assign(d->n_slots, 0);
   c->gen.assign(d->n_slots, 0);
   c->owner.assign(d->n_slots, StateKey(-1, -1));
+  c->slot_written.assign((size_t)d->n_layers * d->n_slots, 0);
   *out = c;
   return SC_OK;
 }
@@ -268,6 +274,7 @@ static int allocate_state(sc_cache* c, StateKey key) {
   for (int32_t s : got) {
     c->used[s] = 1;
     c->owner[s] = key;
+    for (int32_t l = 0; l < c->d.n_layers; ++l) c->slot_written[(size_t)l * c->d.n_slots + s] = 0;
   }
   StateEntry e;
   e.slots = got;
@@ -284,6 +291,7 @@ int sc_cache_release(sc_cache* c, sc_node st) {
     c->used[s] = 0;
     c->gen[s] += 1;
     c->owner[s] = StateKey(-1, -1);
+    for (int32_t l = 0; l < c->d.n_layers; ++l) c->slot_written[(size_t)l * c->d.n_slots + s] = 0;
   }
   c->states.erase(it);
   return SC_OK;
@@ -319,7 +327,7 @@ int sc_cache_append(sc_cache* c, int32_t layer, sc_node st, const void* k, const
     if (fresh) sc_cache_release(c, st);
     return rc;
   }
-  it->second.written[layer] = 1;
+  set_written(c, it->second, layer, 1);
   return SC_OK;
 }
 

@@ -51,6 +51,10 @@ struct sc_cache {
   std::vector<uint32_t> gen;
   std::vector<sc::StateKey> owner;  // slot -> state (valid when used)
   std::map<sc::StateKey, sc::StateEntry> states;
+  // [layer * n_slots + slot]: the written flag of the slot's state at that
+  // layer (a flat copy of StateEntry::written, so that checking a plan's
+  // pages costs no map lookups); kept by set_written
+  std::vector<uint8_t> slot_written;
 };
 
 struct sc_plan {
@@ -60,6 +64,8 @@ struct sc_plan {
   std::vector<sc::StateKey> page_state;
   const sc_cache* cache;
   int32_t nq;  // query tokens per node
+  // page slots in the bf16 attention's traversal order (built on first use)
+  mutable std::vector<int32_t> attn_slot;
 };
 
 namespace sc {
@@ -67,6 +73,9 @@ namespace sc {
 // Validates a plan against the cache for reading `layer` (generations and
 // written flags).  Returns SC_OK or an error code with the message set.
 int plan_check(const sc_plan* plan, const sc_cache* cache, int32_t layer);
+
+// Sets a state's written flag at `layer` and its slots' copies of it.
+void set_written(sc_cache* cache, StateEntry& e, int32_t layer, uint8_t v);
 
 // Policy helpers shared by the selection builder and the release rule:
 // validation (SC_OK or SC_EINVAL with the message set), whether offset r is

@@ -80,7 +80,7 @@ extern "C" int sc_stack_forward(const sc_block_weights* layers, int32_t n_layers
       for (int32_t e = 0; e < l; ++e)
         for (const sc_node& nd : plan->nodes) {
           auto it = cache->states.find(StateKey(nd.chunk, nd.level));
-          if (it != cache->states.end()) it->second.written[e] = 0;
+          if (it != cache->states.end()) set_written(cache, it->second, e, 0);
         }
       return rc;
     }

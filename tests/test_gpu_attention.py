@@ -3,8 +3,8 @@
 Covers the tiny fp32 case (every node of 4 chunks x 5 levels under all three
 policies, several pack shapes), small bf16 packs on each work-group shape
 (256, 128 and 64 queries) whose pages (104, 96 and 40 tokens) leave ragged
-tails inside key tiles, the short-context streaming shape whole and cut into
-key-range pieces, the Wan-shaped clean / same-level /
+tails inside key tiles, the short-context streaming shape and long windows
+cut into key-range pieces, the Wan-shaped clean / same-level /
 progressive packs on sampled rows, the segment probe, negative controls
 (mistakes planted in the oracle must fail the gates), NaN poisoning of
 unused slots, packed vs sequential, run-to-run determinism and the workspace
@@ -117,6 +117,21 @@ def test_narrow_many_units(heads):
     assert case.workspace_bytes == 0
     for i in (0, 21, 42, 63):
         bf16_gates(out[i], case.oracle(i), f"narrow {heads} heads node {pack[i]}")
+
+
+def test_wide_long_windows_cut_into_pieces():
+    """128-query nodes over 41 pages of 128 keys (5248 keys): the 128-query
+    shape, its 36 units cut into key-range pieces; every row against the
+    oracle."""
+    geo = kv_stream(128, W=40)
+    W = geo.W
+    pack = [(41 * i + W, 4) for i in range(3)]
+    resident = [(41 * i + r, 0) for i in range(3) for r in range(W)]
+    case = AttnCase(geo, sc.SC_DTYPE_BF16, "clean", pack, resident, seed=15)
+    out = case.run()
+    assert case.workspace_bytes > 0
+    for i in range(len(pack)):
+        bf16_gates(out[i], case.oracle(i), f"wide pieces node {pack[i]}")
 
 
 @pytest.mark.parametrize("nq", [64, 128])
