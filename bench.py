@@ -382,7 +382,9 @@ def bench_kv_stream(args):
     the bf16 ridge, so the attention streams K/V at HBM speed.  Reports, per
     (Nq, P): the time per launch of back-to-back launches (and with events
     around each launch), algorithmic bytes (K/V of the visible pages, Q, O)
-    and GB/s against 8 TB/s."""
+    and GB/s against 8 TB/s; beside them, the plain streaming-read rate of
+    the same GPU (sc_probe_read) over 4 GiB (HBM) and 128 MiB (within the
+    256 MB last-level cache)."""
     import numpy as np
     import torch
 
@@ -394,6 +396,24 @@ def bench_kv_stream(args):
         return torch.from_numpy(bf16_bits(x).view(np.int16)).cuda().view(torch.bfloat16)
 
     rows = []
+    # the plain streaming-read ceiling of this GPU, beyond and within the
+    # last-level cache (256 MB)
+    ceiling = {}
+    big = torch.empty(4 << 30, dtype=torch.uint8, device="cuda")
+    word = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for mib in (4096, 128):
+        nbytes = mib << 20
+        for _ in range(3):
+            sc.sc_probe_read(big, nbytes, word)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            sc.sc_probe_read(big, nbytes, word)
+        e1.record()
+        torch.cuda.synchronize()
+        ceiling[f"read_{mib}_mib_gb_s"] = round(nbytes / (e0.elapsed_time(e1) / args.steps * 1e-3) / 1e9, 1)
+    del big
+    log(f"[bench] streaming-read probe: {ceiling}")
     for nq in (64, 128):
         g = kv_stream(nq)
         shape = (nq, g.heads, g.head_dim)
@@ -452,7 +472,7 @@ def bench_kv_stream(args):
                 f"back to back ({ms_each:.4f} with events around each), {gbs:.0f} GB/s, "
                 f"{rows[-1]['tflops']} TFLOP/s")
             del cache, pool
-    return rows
+    return rows, ceiling
 
 
 def bench_stack(args):
@@ -583,7 +603,7 @@ def main():
         print(json.dumps({"copy_probe_bytes": 256 << 20, "copies": 4}), flush=True)
         return
     if args.workload == "kvstream":
-        rows = bench_kv_stream(args)
+        rows, ceiling = bench_kv_stream(args)
         best = max(rows, key=lambda r: r["gb_s"])
         print(json.dumps({
             "metric": "short-context K/V streaming rate of the packed attention",
@@ -594,7 +614,7 @@ def main():
             "roofline": {"bound": "hbm", "achieved": best["gb_s"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": round(best["gb_s"] / PEAK_HBM_GBS, 4), "traffic": None,
                          "kernel": "attn_bf16_kernel"},
-            "sweep": rows}), flush=True)
+            "read_probe": ceiling, "sweep": rows}), flush=True)
         return
     if args.workload == "cfg5":
         from synth.configs import WAN as g

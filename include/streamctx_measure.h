@@ -43,6 +43,16 @@ size_t sc_probe_mfma_out_bytes(void);
 int sc_probe_mfma(int32_t random_operands, int32_t iters, void* out, size_t out_bytes,
                   double* flops, sc_stream stream);
 
+/* ---- Streaming-read probe (measurement support) -----------------------
+ * Launches one kernel on `stream` that reads the `bytes` bytes of device
+ * buffer `buf` once with 16-byte loads (8192 work-groups of 256 lanes,
+ * grid-stride, four loads in flight per lane) and stores nothing but, never
+ * in practice, one word at `out` (device, 4 bytes).  The caller times it:
+ * the plain-read bandwidth a kernel can reach on this GPU, for buffers
+ * beyond the last-level cache (HBM) or within it.  buf 16-byte aligned,
+ * bytes a positive multiple of 16.  Errors: SC_EINVAL, SC_EDEVICE. */
+int sc_probe_read(const void* buf, size_t bytes, void* out, sc_stream stream);
+
 #ifdef __cplusplus
 }
 #endif

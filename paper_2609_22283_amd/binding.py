@@ -20,7 +20,7 @@ __all__ = [
     "sc_abi_version", "sc_selection_build", "sc_cache_pool_bytes", "sc_cache_create",
     "sc_rope_table_bytes", "sc_rope_table_build", "sc_plan_build", "sc_attention",
     "sc_attention_workspace_bytes", "sc_block_workspace_bytes", "sc_block_forward", "sc_sampler_step",
-    "sc_timer_enable", "sc_timer_read", "sc_probe_mfma_out_bytes", "sc_probe_mfma",
+    "sc_timer_enable", "sc_timer_read", "sc_probe_mfma_out_bytes", "sc_probe_mfma", "sc_probe_read",
     "Selection", "Cache", "Plan", "Rope", "BlockWeights", "CrossAttn",
     "sc_plan_condition", "sc_condition_workspace_bytes", "sc_condition_append",
     "sc_pipeline_rounds", "sc_pipeline_round_nodes", "sc_cache_release_unread", "sc_stack_forward",
@@ -45,7 +45,7 @@ EXPORTED_SYMBOLS = [
     "sc_condition_workspace_bytes", "sc_condition_append",
     "sc_attention_workspace_bytes", "sc_attention",
     "sc_block_workspace_bytes", "sc_block_forward", "sc_sampler_step",
-    "sc_timer_enable", "sc_timer_read", "sc_probe_mfma_out_bytes", "sc_probe_mfma",
+    "sc_timer_enable", "sc_timer_read", "sc_probe_mfma_out_bytes", "sc_probe_mfma", "sc_probe_read",
     "sc_pipeline_rounds", "sc_pipeline_round_nodes", "sc_cache_release_unread", "sc_stack_forward",
     "sc_serial_steps", "sc_serial_step_node", "sc_block_workspace_views",
     "sc_attention_noalloc", "sc_attention_noalloc_scratch_bytes",
@@ -151,6 +151,7 @@ _SIG = {
     "sc_timer_read": (C.c_int, [C.c_char_p, _I32P, C.POINTER(C.c_double)]),
     "sc_probe_mfma_out_bytes": (C.c_size_t, []),
     "sc_probe_mfma": (C.c_int, [C.c_int32, C.c_int32, _P, C.c_size_t, C.POINTER(C.c_double), _P]),
+    "sc_probe_read": (C.c_int, [_P, C.c_size_t, _P, _P]),
     "sc_pipeline_rounds": (C.c_int, [C.c_int32, C.c_int32, C.c_int32]),
     "sc_pipeline_round_nodes": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                           C.POINTER(sc_node), _I32P]),
@@ -507,6 +508,11 @@ def sc_probe_mfma(random_operands: bool, iters: int, out, out_bytes: int, stream
     _check(lib.sc_probe_mfma(1 if random_operands else 0, iters, _ptr(out), out_bytes, C.byref(fl),
                              _stream(stream)))
     return fl.value
+
+
+def sc_probe_read(buf, nbytes: int, out, stream=None) -> None:
+    """Launch the streaming-read probe over the first nbytes of buf."""
+    _check(lib.sc_probe_read(_ptr(buf), nbytes, _ptr(out), _stream(stream)))
 
 
 # ------------------------------------------------------------------- schedule

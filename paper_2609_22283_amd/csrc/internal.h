@@ -99,7 +99,7 @@ int launch_attention(const sc_plan* plan, const sc_cache* cache, int32_t layer,
 // whose units fill whole rounds of the CUs), and its bound over all plans
 // (at most kAttnMaxPieces partial results).
 constexpr int32_t kAttnMaxPieces = 1024;
-constexpr int32_t kAttnMinSplitTiles = 32;  // mean key tiles per unit below which nothing is cut
+constexpr int32_t kAttnMinSplitTiles = 32;  // mean 64-key tiles per unit below which nothing is cut
 size_t attention_workspace_bytes(const sc_plan* plan, const sc_cache* cache);
 size_t attention_workspace_bound();
 int launch_append(const sc_cache* cache, int32_t layer, const int32_t* slots, int32_t chunk,

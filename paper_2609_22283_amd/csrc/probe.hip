@@ -1,4 +1,7 @@
-// Matrix-core ceiling probe (measurement support, not part of the method).
+// Ceiling probes (measurement support, not part of the method): the matrix
+// cores' sustained rate and the streaming-read bandwidth of HBM.
+//
+// Matrix-core ceiling probe.
 // A grid of 8-wave work-groups, two per CU, issues back-to-back
 // 16x16x32 bf16 MFMAs (the instruction of the attention and GEMM kernels) on
 // eight accumulator chains with operands held in registers: no memory
@@ -47,10 +50,35 @@ __global__ __launch_bounds__(kProbeThreads) void mfma_probe_kernel(float* out, i
   out[blockIdx.x * kProbeThreads + threadIdx.x] = s;
 }
 
+// Streaming-read ceiling: every lane reads 16-byte pieces of the buffer,
+// four loads in flight, grid-stride; nothing is stored but one word when an
+// impossible checksum appears (so the loads are not optimised away).
+__global__ __launch_bounds__(256) void read_probe_kernel(const u32x4* __restrict__ p, size_t n16,
+                                                         uint32_t* out) {
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  uint32_t acc = 0;
+  for (; i + 3 * stride < n16; i += 4 * stride) {
+    const u32x4 a = p[i], b = p[i + stride], c = p[i + 2 * stride], d = p[i + 3 * stride];
+    acc ^= a.x ^ b.y ^ c.z ^ d.w;
+  }
+  for (; i < n16; i += stride) acc ^= p[i].x;
+  if (acc == 0x9e3779b9u) out[0] = acc;
+}
+
 }  // namespace
 }  // namespace sc
 
 using namespace sc;
+
+extern "C" int sc_probe_read(const void* buf, size_t bytes, void* out, sc_stream stream) {
+  if (!buf || !out || bytes == 0 || bytes % 16 || (reinterpret_cast<uintptr_t>(buf) & 15))
+    return fail(SC_EINVAL, "need a 16-byte aligned buffer of a positive multiple of 16 bytes and an output word");
+  hipLaunchKernelGGL(read_probe_kernel, dim3(8192), dim3(256), 0, static_cast<hipStream_t>(stream),
+                     static_cast<const u32x4*>(buf), bytes / 16, static_cast<uint32_t*>(out));
+  SC_HIP(hipGetLastError());
+  return SC_OK;
+}
 
 extern "C" size_t sc_probe_mfma_out_bytes(void) {
   int dev = 0, cus = 0;
