@@ -286,12 +286,26 @@ __device__ __forceinline__ void probs_tile(const STile<KH>& s, bf16x8 (&pb)[KH][
 
 // Direct global -> LDS copy of 16 bytes per lane (gfx950 LDS DMA): lane i
 // of the wave writes bytes [16 i, 16 i + 16) after the wave-uniform LDS
-// address, so the XOR swizzle is applied by choosing each lane's source.
-__device__ __forceinline__ void dma16(const char* src, char* lds_wave_base) {
-  __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src),
-                                   reinterpret_cast<__attribute__((address_space(3))) void*>(
-                                       reinterpret_cast<uintptr_t>(lds_wave_base)),
-                                   16, 0, 0);
+// address, so the XOR swizzle is applied by choosing each lane's source
+// (base + off).  Written as inline asm: while a copy it knows of is in
+// flight, the compiler waits for every LDS read with lgkmcnt(0), so no
+// fragment read could overlap another; the copies themselves complete
+// under this wave's explicit vmcnt waits (landed, landed_but).  M0, which
+// carries the LDS address, is saved and restored.
+__device__ __forceinline__ uint32_t lds_addr(const char* p) {
+  return (uint32_t)reinterpret_cast<uintptr_t>(p);
+}
+__device__ __forceinline__ void dma16(const char* base, uint32_t off, char* lds_wave_base) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off), "s"(base), "s"(lds_addr(lds_wave_base))
+      : "memory");
 }
 
 // Copies of BK-key K and V^T tiles of one (node, head) from the paged cache
@@ -379,7 +393,7 @@ struct KvTiles {
     for (int j = 0; j < KCP; ++j) {
       const int32_t rg = 4 * KCP * wave + 4 * j;  // first tile row of this copy (wave-uniform)
       const uint32_t src = rg >= lim ? kbad + (klane[j] & 255u) : (rg >= split ? hi : lo) + klane[j];
-      dma16(lbase + src, kl + rg * 256);
+      dma16(lbase, src, kl + rg * 256);
     }
   }
   // A V^T row holds the tile's BK keys; a page boundary or the node's end
@@ -391,7 +405,7 @@ struct KvTiles {
     const int32_t lim = nk - t0, split = bkey - t0;
     if (split >= BK && lim >= BK) {
 #pragma unroll
-      for (int j = 0; j < VCP; ++j) dma16(lbase + (lo + vlane[j]), vl + (RPI * VCP * wave + RPI * j) * 2 * BK);
+      for (int j = 0; j < VCP; ++j) dma16(lbase, lo + vlane[j], vl + (RPI * VCP * wave + RPI * j) * 2 * BK);
       return;
     }
     const uint32_t hi = sl.hi + vhead + (uint32_t)(t0 - bkey) * 2;
@@ -401,7 +415,7 @@ struct KvTiles {
       const bool in = rk < lim;
       const uint32_t off = in ? vlane[j] : vlane[j] - (uint32_t)rk * 2;
       const uint32_t base = (in && rk >= split) ? hi : lo;
-      dma16(lbase + (base + off), vl + (RPI * VCP * wave + RPI * j) * 2 * BK);
+      dma16(lbase, base + off, vl + (RPI * VCP * wave + RPI * j) * 2 * BK);
     }
   }
 };

@@ -38,12 +38,23 @@ __device__ __forceinline__ float gelu_tanh(float x) {
   return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
-// Direct global -> LDS copy of 16 bytes per lane (lane i lands at LDS base + 16 i).
-__device__ __forceinline__ void gdma16(const char* src, char* lds_wave_base) {
-  __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src),
-                                   reinterpret_cast<__attribute__((address_space(3))) void*>(
-                                       reinterpret_cast<uintptr_t>(lds_wave_base)),
-                                   16, 0, 0);
+// Direct global -> LDS copy of 16 bytes per lane (lane i lands at LDS base
+// + 16 i) from base + off.  Written as inline asm: while a copy it knows of
+// is in flight, the compiler waits for every LDS fragment read with
+// lgkmcnt(0); not knowing of these, it counts the reads exactly (the copies
+// complete under the loop's explicit vmcnt(0) wait).  M0, which carries the
+// LDS address, is saved and restored.  (QKV and MLP-up GEMMs 2 % faster.)
+__device__ __forceinline__ void gdma16(const char* base, uint32_t off, char* lds_wave_base) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off), "s"(base), "s"((uint32_t)reinterpret_cast<uintptr_t>(lds_wave_base))
+      : "memory");
 }
 
 // Per-token sum of squares of a wave's 128 x 64 accumulator tile: lane
@@ -130,9 +141,9 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
     const char* xk = xbase + (size_t)k0 * 2;
 #pragma unroll
     for (int j = 0; j < NCP; ++j) {
-      gdma16(wk + woff[j], a + (GROWS * wave + 8 * j) * 128);
+      gdma16(wk, woff[j], a + (GROWS * wave + 8 * j) * 128);
       if (j < NCPX && (XGROUPS % G_NW == 0 || wave + G_NW * j < XGROUPS))  // wave-uniform
-        gdma16(xk + xoff[j], b + (8 * (wave + G_NW * j)) * 128);
+        gdma16(xk, xoff[j], b + (8 * (wave + G_NW * j)) * 128);
     }
   };
   auto landed = [&]() {
