@@ -90,7 +90,7 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   // stage s: W tile at s * 64 KB, X tile at s * 64 KB + 32 KB; rows of 64 k
   // (128 B) with 16-byte column c stored at c ^ ((row >> 1) & 7)
   __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * G_TILE_BYTES];
-  static_assert(WL == 0 || (EPI != EPI_QKV && EPI != EPI_STORE), "layout 1 is for the plain epilogues");
+  static_assert(WL == 0 || EPI != EPI_STORE, "layout 1 is not used for the store epilogue");
   constexpr int WM = WL ? 64 : GWM;    // features per wave tile
   constexpr int GWN = WL ? BN / 2 : BN / 4;  // tokens per wave tile
   static_assert(GWN % 16 == 0, "wave tiles hold whole 16-token blocks");
@@ -223,7 +223,9 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
     const int32_t hf0 = f0 - sec * ep.hidden + wf;       // wave's first feature in its section
     const int32_t head = hf0 / ep.head_dim;
     const int32_t dbase = hf0 - head * ep.head_dim + 4 * lg;
-    if (ep.ss_part && sec < 2) {
+    // (qk-norm sums take one 128-feature head per wave: layout 0 only; the
+    // launcher never gives layout 1 a QKV launch with ss_part)
+    if (WL == 0 && ep.ss_part && sec < 2) {
       // qk-norm: sums of squares of the raw q or k, then the gain (before
       // RoPE); the 1 / rms factor is applied by norm_scale_kernel
       store_sum_squares(acc, ep.ss_part, ep.n_part, (f0 + wf) / GWM, t0 + wt, T, lg, c16);
@@ -336,9 +338,11 @@ template <int BN, int WL>
 static void launch_gemm_bn(int epi, const uint16_t* W, const uint16_t* X, int32_t F, int32_t T, int32_t Kd,
                            const GemmEpilogue& ep, hipStream_t stream) {
   const dim3 grid((uint32_t)(F / GBM) * (uint32_t)((T + BN - 1) / BN));
-  if constexpr (WL == 1) {  // the plain epilogues only
+  if constexpr (WL == 1) {  // GELU, residual and QKV without qk-norm sums
     if (epi == EPI_GELU)
       hipLaunchKernelGGL((gemm_bf16_kernel<EPI_GELU, BN, 1>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
+    else if (epi == EPI_QKV)
+      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV, BN, 1>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
     else
       hipLaunchKernelGGL((gemm_bf16_kernel<EPI_RESIDUAL, BN, 1>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd,
                          ep);
@@ -365,14 +369,16 @@ static void launch_gemm_bn(int epi, const uint16_t* W, const uint16_t* X, int32_
 // BN / 256 of a 256-token tile's time times a per-shape efficiency loss
 // (more fragment reads and copies per MFMA), measured on the Wan block's
 // GEMMs.  The shape with the fewest tile-times wins, the wider one on ties.
-// Layout 1 (224-token tiles) serves the GELU and residual epilogues.
+// Layout 1 (224-token tiles, a wave holds 64 features: half a head) serves
+// the GELU and residual epilogues and QKV without qk-norm sums, which need
+// a whole 128-feature head per wave.
 struct GemmShape {
   int bn, wl;
 };
-static GemmShape gemm_tile_shape(int epi, int32_t F, int32_t T) {
+static GemmShape gemm_tile_shape(int epi, int32_t F, int32_t T, bool qk_sums) {
   GemmShape best{256, 0};
   double best_cost = 1e30;
-  const bool plain = epi == EPI_GELU || epi == EPI_RESIDUAL;
+  const bool plain = epi == EPI_GELU || epi == EPI_RESIDUAL || (epi == EPI_QKV && !qk_sums);
   const GemmShape cands[] = {{256, 0}, {224, 1}, {192, 0}, {128, 0}};
   for (const GemmShape c : cands) {
     if (c.wl == 1 && !plain) continue;
@@ -397,7 +403,7 @@ int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, i
   if (epi == EPI_QKV && (ep.hidden % GBM || ep.head_dim != GWM))
     return fail(SC_EUNSUPPORTED, "QKV epilogue needs hidden %% %d == 0 and head_dim %d", GBM, GWM);
   timer_begin(timer_kind, stream);
-  const GemmShape shape = gemm_tile_shape(epi, F, T);
+  const GemmShape shape = gemm_tile_shape(epi, F, T, ep.ss_part != nullptr);
   if (shape.wl == 1)
     launch_gemm_bn<224, 1>(epi, W, X, F, T, Kd, ep, stream);
   else if (shape.bn == 128)
