@@ -443,13 +443,15 @@ __device__ __forceinline__ void landed_but(int32_t n) {
 #undef SC_LANDED_BUT
 }
 
-// Schedule.  A unit is a (head, query tile, node) triple, numbered head-major
-// then query tile then node; a unit's key tiles are processed in order by one
-// work-group.  Units of one head are consecutive, and every node's page list
-// starts at the state most nodes of the pack read (see shared_order), so the
-// work-groups an XCD runs side by side -- a few query tiles of every node of
-// one head -- read the same K/V tiles at about the same time and share them
-// in its L2.  Equal units fill the resident work-groups in whole rounds but the
+// Schedule.  A unit is a (head, node, query tile) triple, numbered head-major
+// then node then query tile; a unit's key tiles are processed in order by one
+// work-group.  The work-groups an XCD runs side by side are then the query
+// tiles of one or two nodes of one head, which read the same K/V tiles at
+// about the same time and share them in its L2; every node's page list
+// starts at the state most nodes of the pack read (see shared_order), so
+// two nodes there read their shared states together too.  (With the node
+// fastest, four nodes' streams shared an XCD's L2 and it fetched 11 % more.)
+// Equal units fill the resident work-groups in whole rounds but the
 // last U mod R; those "tail" units are each cut into S pieces of their key
 // range, numbered piece-major (piece p of every tail unit before piece p+1),
 // so the last round is S times shorter.  Pieces leave unnormalised partials
@@ -480,8 +482,8 @@ __device__ __forceinline__ AttnItem decode_item(const AttnPlan& plan, const Attn
     unit = g.whole_units + j % g.tail_units;
     it.slot = j;
   }
-  it.node = unit % g.n_nodes;
-  it.qt = (unit / g.n_nodes) % g.n_qtiles;
+  it.qt = unit % g.n_qtiles;
+  it.node = (unit / g.n_qtiles) % g.n_nodes;
   it.head = unit / (g.n_qtiles * g.n_nodes);
   it.ntiles = node_tiles<KH>(plan, g, it.node);
   if (it.slot < 0) {
@@ -893,8 +895,8 @@ template <int BQ, int KH>
 __global__ __launch_bounds__(256) void attn_combine_kernel(uint16_t* __restrict__ o, AttnGeom g, AttnPlan plan) {
   const int32_t tu = blockIdx.x;
   const int32_t unit = g.whole_units + tu;
-  const int32_t node = unit % g.n_nodes;
-  const int32_t qt = (unit / g.n_nodes) % g.n_qtiles;
+  const int32_t qt = unit % g.n_qtiles;
+  const int32_t node = (unit / g.n_qtiles) % g.n_nodes;
   const int32_t head = unit / (g.n_qtiles * g.n_nodes);
   const int32_t lrow = blockIdx.y * 8 + (threadIdx.x >> 5);
   const int32_t dl = threadIdx.x & 31;
