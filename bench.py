@@ -42,8 +42,8 @@ METRIC = "steady-state latent frames/s per DiT block + attention TFLOP/s (% bf16
 # FETCH_SIZE and WRITE_SIZE per dispatch, scaled by what the same counters
 # read for a plain 256 MiB copy (x2.0 fetch, x1.0 write).  Valid only for the
 # kernel sources it was measured on (hash below); otherwise reported as null.
-ATTN_TRAFFIC = {"sources_sha1": "3bd116396f32f48eab7647934bf2bed3b642ba12",
-                "fetch_bytes": 1.3460e+09, "write_bytes": 2.0064e+08}
+ATTN_TRAFFIC = {"sources_sha1": "285733cc1466b1de936ead77546343c245c9a7b7",
+                "fetch_bytes": 1.3541e+09, "write_bytes": 2.0061e+08}
 
 
 def attn_traffic():

@@ -369,9 +369,9 @@ struct KvTiles {
     }
   }
   // Page slots of the tile starting at key t0 >= 0 (two scalar loads),
-  // fetched one step before the copy that uses them so their latency
-  // overlaps the step in between.  Clamped to the node's pages: a tile past
-  // the end is never read.
+  // fetched ahead of the copy that uses them so their latency overlaps other
+  // work (a step, or the barrier wait before the copy).  Clamped to the
+  // node's pages: a tile past the end is never read.
   __device__ __forceinline__ Slots slots(int32_t t0) const {
     Slots sl;
     sl.plo = min((int32_t)fast_div((uint32_t)t0, tpp_div), npages - 1);
@@ -586,6 +586,64 @@ __device__ __forceinline__ void attn_step(const char* smem, const AttnLane& L, c
                                           f32x4 (&lsum)[2], const bf16x8& ones, int32_t t0, int32_t nk,
                                           int32_t lg) {
   using T = Tile<KH>;
+  if constexpr (NEXT && !MASK && KH == 2) {
+    // One stream of 32 fragment reads (the 16 K fragments of S(t+1), then
+    // the 16 V^T fragments of tile t), each issued PF fragments ahead of the
+    // two MFMAs it feeds; the 32 exponentials of P(t) ride two to a K group.
+    // The fences keep that order: left to itself the compiler reads each
+    // fragment just before its MFMAs, which then wait out the LDS latency.
+    constexpr int PF = 4, NKF = 16, NF = 32;
+    const char* kl = smem + KN * T::KT_BYTES;
+    const char* vl = smem + 2 * T::KT_BYTES + VC * T::VT_BYTES;
+    auto frag = [&](int i) -> bf16x8 {
+      if (i < NKF) return *reinterpret_cast<const bf16x8*>(kl + L.koff[i & 1][i >> 2] + ((i >> 1) & 1) * 8192);
+      const int j = i - NKF;
+      return *reinterpret_cast<const bf16x8*>(vl + L.voff[j >> 3] + (j & 7) * (16 * 2 * T::BK));
+    };
+    STile<2> sn;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sn[h][b][qb][r] = -m[qb];
+    bf16x8 pb[2][2];
+    bf16x8 ring[PF];
+#pragma unroll
+    for (int i = 0; i < PF; ++i) ring[i] = frag(i);
+#pragma unroll
+    for (int i = 0; i < NF; ++i) {
+      const bf16x8 f = ring[i % PF];
+      if (i + PF < NF) ring[i % PF] = frag(i + PF);
+      if (i < NKF) {  // K fragment (ds, h, b) = (i / 4, i / 2 mod 2, i mod 2), as in qk_tile
+        const int ds = i >> 2, h = (i >> 1) & 1, b = i & 1;
+        sn[h][b][0] = mfma16(f, qreg[0][ds], sn[h][b][0]);
+        sn[h][b][1] = mfma16(f, qreg[1][ds], sn[h][b][1]);
+        const int ph = i >> 3, pq = (i >> 2) & 1, pe = 2 * (i & 3);  // pb[ph][pq] elements pe, pe + 1
+        pb[ph][pq][pe] = static_cast<__bf16>(__builtin_amdgcn_exp2f(s[ph][pe >> 2][pq][pe & 3]));
+        pb[ph][pq][pe + 1] = static_cast<__bf16>(__builtin_amdgcn_exp2f(s[ph][(pe + 1) >> 2][pq][(pe + 1) & 3]));
+      } else {  // V^T fragment (h, db) = (j / 8, j mod 8), as in pv_tile
+        const int j = i - NKF, h = j >> 3, db = j & 7;
+        oacc[0][db] = mfma16(f, pb[h][0], oacc[0][db]);
+        oacc[1][db] = mfma16(f, pb[h][1], oacc[1][db]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      lsum[0] = mfma16(ones, pb[h][0], lsum[0]);
+      lsum[1] = mfma16(ones, pb[h][1], lsum[1]);
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) s[h][b][qb] = sn[h][b][qb];
+    return;
+  }
   if constexpr (MASK) mask_tile<KH>(s, t0, nk, lg);
   bf16x8 pb[KH][2];
   probs<KH>(s, pb);
@@ -741,16 +799,21 @@ __global__ __launch_bounds__(64 * NW, NW == 8 || D == 4 ? 1 : 2) void attn_bf16_
     for (; t + 2 < ntiles; t += 2) {
       kv.copy_k((t + 2) * BK, smem, sk);
       kv.copy_v((t + 1) * BK, smem + 2 * KT_BYTES + VT_BYTES, sv);
+      if constexpr (ACT) attn_step<KH, 1, 0, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
+      // the next copies' page slots: their scalar loads share the LDS wait
+      // counter, so they are issued after the step's fragment reads (a wait
+      // for one fragment would otherwise wait for them too)
+      __builtin_amdgcn_sched_barrier(0);
       sk = kv.slots(min(t + 3, it.ntiles - 1) * BK);
       sv = kv.slots(min(t + 2, it.ntiles - 1) * BK);
-      if constexpr (ACT) attn_step<KH, 1, 0, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, t * BK, nk, lg);
       landed();
       if (t + 3 < ntiles) kv.copy_k((t + 3) * BK, smem + KT_BYTES, sk);
       kv.copy_v((t + 2) * BK, smem + 2 * KT_BYTES, sv);
-      sk = kv.slots(min(t + 4, it.ntiles - 1) * BK);
-      sv = kv.slots(min(t + 3, it.ntiles - 1) * BK);
       if constexpr (ACT)
         attn_step<KH, 0, 1, true, false>(smem, L, qreg, oacc, s, m, lsum, ones, (t + 1) * BK, nk, lg);
+      __builtin_amdgcn_sched_barrier(0);
+      sk = kv.slots(min(t + 4, it.ntiles - 1) * BK);
+      sv = kv.slots(min(t + 3, it.ntiles - 1) * BK);
       landed();
     }
     if (t + 1 < ntiles) {  // two tiles left, parity 0
