@@ -47,13 +47,6 @@ struct AttnGeom {
                           // (BQ: queries per work-group of the instantiation launched)
 };
 
-static DivMagic magic_div(uint32_t d) {
-  uint32_t l = 0;
-  while ((1ull << l) < d) ++l;
-  uint64_t m = ((1ull << 32) * ((1ull << l) - d)) / d + 1;
-  return DivMagic{(uint32_t)m, l, d};
-}
-
 // ------------------------------------------------------------- fp32 kernel
 // One thread per query row, keys streamed from the cache; used for the fp32
 // path (small parity shapes), not tuned.

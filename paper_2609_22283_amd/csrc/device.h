@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <cstdint>
 
+#include "divmagic.h"
+
 namespace sc {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -28,13 +30,7 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
 }
 
-// n / d for n < 2^31 with a host-computed magic pair (see host magic_div()).
-struct DivMagic {
-  uint32_t mul;
-  uint32_t shift;
-  uint32_t div;
-};
-
+// n / d for n < 2^31 with a host-computed magic pair (divmagic.h).
 __device__ __forceinline__ uint32_t fast_div(uint32_t n, DivMagic m) {
   return (__umulhi(n, m.mul) + n) >> m.shift;
 }

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <cstdint>
 
+#include "divmagic.h"
+
 namespace sc {
 
 enum { EPI_STORE = 0, EPI_QKV = 1, EPI_GELU = 2, EPI_RESIDUAL = 3 };
@@ -20,6 +22,7 @@ struct GemmEpilogue {
   char* layer_base;
   uint64_t slot_bytes, kv_half;
   int32_t hidden, head_dim, nq, tpp, ppc, grid_w;
+  DivMagic nq_div, tpp_div, gw_div;  // set by the launcher from nq, tpp, grid_w
   const float2* rope_table;  // NULL: no rotation
   int32_t pairs_t, pairs_h, pairs_w;
   int64_t rope_off_h, rope_off_w;

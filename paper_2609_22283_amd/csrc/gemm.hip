@@ -5,7 +5,7 @@
 // into the epilogue:
 //   QKV      RoPE on q and k; q to a token-major buffer; k and v scattered
 //            into the pack nodes' page slots (k as [head][token][d], v as
-//            [head][d][token])
+//            [head][d][token], transposed through LDS into 8-token runs)
 //   GELU     out[t][f] = GELU_tanh(D)
 //   RESIDUAL x[t][f] += D   (in place)
 //   STORE    out[t][f] = D
@@ -239,54 +239,110 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
           for (int e = 0; e < 4; ++e) acc[fb][tb][e] *= gv[e];
       }
     }
+    // v is stored transposed per page ([head][d][token]).  Each wave stages
+    // its v tile in its own LDS region (free after the main loop; rows
+    // padded by 16 bytes against bank conflicts; in two passes of half the
+    // rows where the whole tile does not fit), then each lane writes runs of
+    // 8 consecutive tokens of one feature row as 16-byte stores.  Pages hold
+    // a multiple of 8 tokens (so do nodes), so no run crosses a page.
+    if (sec == 2) {
+      constexpr int LDSW = GWN + 8;  // staged row length (elements)
+      constexpr int RP = WM * LDSW * 2 * G_NW <= (int)sizeof(smem) ? WM : WM / 2;  // rows per pass
+      constexpr int SEGS = GWN / 8;
+      static_assert(RP * LDSW * 2 * G_NW <= (int)sizeof(smem) && (RP * SEGS) % 64 == 0 && RP % 16 == 0,
+                    "v staging layout");
+      uint16_t* lt = reinterpret_cast<uint16_t*>(smem) + (size_t)wave * RP * LDSW;
+      const int32_t d0 = hf0 - head * ep.head_dim;  // wave's first feature within its head
+#pragma unroll
+      for (int pass = 0; pass < WM / RP; ++pass) {
+#pragma unroll
+        for (int fb = pass * RP / 16; fb < (pass + 1) * RP / 16; ++fb)
+#pragma unroll
+          for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              lt[(16 * fb - pass * RP + 4 * lg + e) * LDSW + 16 * tb + c16] = f32_to_bf16(acc[fb][tb][e]);
+#pragma unroll
+        for (int j = 0; j < RP * SEGS / 64; ++j) {
+          const int32_t r = lane + 64 * j, row = r / SEGS, seg = r - row * SEGS;
+          const int32_t t = t0 + wt + 8 * seg;
+          if (t >= T) continue;
+          const u32x4 val = *reinterpret_cast<const u32x4*>(lt + row * LDSW + 8 * seg);
+          const int32_t node = (int32_t)fast_div((uint32_t)t, ep.nq_div), tok = t - node * ep.nq;
+          const int32_t frame = (int32_t)fast_div((uint32_t)tok, ep.tpp_div), n = tok - frame * ep.tpp;
+          char* slot_base = ep.layer_base + (size_t)ep.node_slot[node * ep.ppc + frame] * ep.slot_bytes;
+          uint16_t* vrow = reinterpret_cast<uint16_t*>(slot_base + ep.kv_half) +
+                           ((size_t)head * ep.head_dim + d0 + pass * RP + row) * ep.tpp + n;
+          if (t + 8 <= T) {
+            *reinterpret_cast<u32x4*>(vrow) = val;
+          } else {  // a launch ending inside a run
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+              if (i < T - t) vrow[i] = (uint16_t)(val[i >> 1] >> (16 * (i & 1)));
+          }
+        }
+      }
+      return;
+    }
+    // RoPE pairs p = d / 2 + pp: the axis of each pair (time, height, width)
+    // and its table offset are fixed per lane, so they are resolved once;
+    // per token only the axis's position term is selected (no branches).
+    const bool rope = ep.rope_table != nullptr;  // q or k here
+    int32_t rbase[FB][2], rax[FB][2];
+#pragma unroll
+    for (int fb = 0; fb < FB; ++fb)
+#pragma unroll
+      for (int pp = 0; pp < 2; ++pp) {
+        const int32_t p = (dbase + 16 * fb) / 2 + pp;
+        if (p < ep.pairs_t) {
+          rax[fb][pp] = 0;
+          rbase[fb][pp] = p;
+        } else if (p < ep.pairs_t + ep.pairs_h) {
+          rax[fb][pp] = 1;
+          rbase[fb][pp] = (int32_t)ep.rope_off_h + (p - ep.pairs_t);
+        } else {
+          rax[fb][pp] = 2;
+          rbase[fb][pp] = (int32_t)ep.rope_off_w + (p - ep.pairs_t - ep.pairs_h);
+        }
+      }
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
       const int32_t t = t0 + wt + 16 * tb + c16;
       if (t >= T) continue;
-      const int32_t node = t / ep.nq, tok = t - node * ep.nq;
-      const int32_t frame = tok / ep.tpp, n = tok - frame * ep.tpp;
+      const int32_t node = (int32_t)fast_div((uint32_t)t, ep.nq_div), tok = t - node * ep.nq;
+      const int32_t frame = (int32_t)fast_div((uint32_t)tok, ep.tpp_div), n = tok - frame * ep.tpp;
       const int32_t pos_t = ep.node_chunk[node] * ep.ppc + frame;
-      const int32_t pos_h = n / ep.grid_w, pos_w = n - pos_h * ep.grid_w;
+      const int32_t pos_h = (int32_t)fast_div((uint32_t)n, ep.gw_div), pos_w = n - pos_h * ep.grid_w;
+      const int32_t term_t = pos_t * ep.pairs_t, term_h = pos_h * ep.pairs_h, term_w = pos_w * ep.pairs_w;
       char* slot_base = ep.layer_base + (size_t)ep.node_slot[node * ep.ppc + frame] * ep.slot_bytes;
       uint16_t* qrow = ep.q_out + (size_t)t * ep.hidden + hf0 + 4 * lg;
       uint16_t* krow = reinterpret_cast<uint16_t*>(slot_base) + ((size_t)head * ep.tpp + n) * ep.head_dim;
-      uint16_t* vcol = reinterpret_cast<uint16_t*>(slot_base + ep.kv_half) +
-                       (size_t)head * ep.head_dim * ep.tpp + n;
 #pragma unroll
       for (int fb = 0; fb < FB; ++fb) {
-          const int32_t d = dbase + 16 * fb;
-          float v0 = acc[fb][tb][0], v1 = acc[fb][tb][1];
-          float v2 = acc[fb][tb][2], v3 = acc[fb][tb][3];
-          if (sec < 2 && ep.rope_table) {
+        const int32_t d = dbase + 16 * fb;
+        float v0 = acc[fb][tb][0], v1 = acc[fb][tb][1];
+        float v2 = acc[fb][tb][2], v3 = acc[fb][tb][3];
+        if (rope) {
 #pragma unroll
-            for (int pp = 0; pp < 2; ++pp) {
-              int32_t p = d / 2 + pp;
-              float2 cs;
-              if (p < ep.pairs_t) cs = ep.rope_table[(int64_t)pos_t * ep.pairs_t + p];
-              else if ((p -= ep.pairs_t) < ep.pairs_h) cs = ep.rope_table[ep.rope_off_h + (int64_t)pos_h * ep.pairs_h + p];
-              else cs = ep.rope_table[ep.rope_off_w + (int64_t)pos_w * ep.pairs_w + (p - ep.pairs_h)];
-              float& x0 = pp ? v2 : v0;
-              float& x1 = pp ? v3 : v1;
-              const float r0 = x0 * cs.x - x1 * cs.y, r1 = x0 * cs.y + x1 * cs.x;
-              x0 = r0;
-              x1 = r1;
-            }
-          }
-          u32x2 pk;
-          pk.x = pack_bf16x2(v0, v1);
-          pk.y = pack_bf16x2(v2, v3);
-          if (sec == 0) {
-            *reinterpret_cast<u32x2*>(qrow + 16 * fb) = pk;
-          } else if (sec == 1) {
-            *reinterpret_cast<u32x2*>(krow + d) = pk;
-          } else {
-            uint16_t* vd = vcol + (size_t)d * ep.tpp;
-            vd[0] = (uint16_t)(pk.x & 0xffff);
-            vd[ep.tpp] = (uint16_t)(pk.x >> 16);
-            vd[2 * ep.tpp] = (uint16_t)(pk.y & 0xffff);
-            vd[3 * ep.tpp] = (uint16_t)(pk.y >> 16);
+          for (int pp = 0; pp < 2; ++pp) {
+            const int32_t ax = rax[fb][pp];
+            const int32_t idx = rbase[fb][pp] + (ax == 0 ? term_t : ax == 1 ? term_h : term_w);
+            const float2 cs = ep.rope_table[idx];
+            float& x0 = pp ? v2 : v0;
+            float& x1 = pp ? v3 : v1;
+            const float r0 = x0 * cs.x - x1 * cs.y, r1 = x0 * cs.y + x1 * cs.x;
+            x0 = r0;
+            x1 = r1;
           }
         }
+        u32x2 pk;
+        pk.x = pack_bf16x2(v0, v1);
+        pk.y = pack_bf16x2(v2, v3);
+        if (sec == 0)
+          *reinterpret_cast<u32x2*>(qrow + 16 * fb) = pk;
+        else
+          *reinterpret_cast<u32x2*>(krow + d) = pk;
+      }
     }
   } else {
     if (EPI == EPI_STORE && ep.ss_part)
@@ -402,16 +458,27 @@ int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, i
     return fail(SC_EUNSUPPORTED, "gemm operands beyond 4 GB");
   if (epi == EPI_QKV && (ep.hidden % GBM || ep.head_dim != GWM))
     return fail(SC_EUNSUPPORTED, "QKV epilogue needs hidden %% %d == 0 and head_dim %d", GBM, GWM);
+  GemmEpilogue e = ep;
+  if (epi == EPI_QKV) {
+    // v goes out in 16-byte runs of 8 tokens within one page
+    if (ep.nq <= 0 || ep.tpp <= 0 || ep.grid_w <= 0 || ep.tpp % 8 || ep.nq % 8 || ep.slot_bytes % 16 ||
+        ep.kv_half % 16 || reinterpret_cast<uintptr_t>(ep.layer_base) % 16)
+      return fail(SC_EUNSUPPORTED, "QKV epilogue needs tpp and nq multiples of 8 and 16-byte aligned slots "
+                  "(nq %d, tpp %d, grid_w %d)", ep.nq, ep.tpp, ep.grid_w);
+    e.nq_div = magic_div((uint32_t)ep.nq);
+    e.tpp_div = magic_div((uint32_t)ep.tpp);
+    e.gw_div = magic_div((uint32_t)ep.grid_w);
+  }
   timer_begin(timer_kind, stream);
   const GemmShape shape = gemm_tile_shape(epi, F, T, ep.ss_part != nullptr);
   if (shape.wl == 1)
-    launch_gemm_bn<224, 1>(epi, W, X, F, T, Kd, ep, stream);
+    launch_gemm_bn<224, 1>(epi, W, X, F, T, Kd, e, stream);
   else if (shape.bn == 128)
-    launch_gemm_bn<128, 0>(epi, W, X, F, T, Kd, ep, stream);
+    launch_gemm_bn<128, 0>(epi, W, X, F, T, Kd, e, stream);
   else if (shape.bn == 192)
-    launch_gemm_bn<192, 0>(epi, W, X, F, T, Kd, ep, stream);
+    launch_gemm_bn<192, 0>(epi, W, X, F, T, Kd, e, stream);
   else
-    launch_gemm_bn<256, 0>(epi, W, X, F, T, Kd, ep, stream);
+    launch_gemm_bn<256, 0>(epi, W, X, F, T, Kd, e, stream);
   timer_end(timer_kind, stream);
   SC_HIP(hipGetLastError());
   return SC_OK;

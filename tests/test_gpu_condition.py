@@ -139,3 +139,22 @@ def test_wan_block_qk_norm_and_cross_sampled_rows():
     want, _ = case.oracle(rows=rows)
     for i in range(len(wl.pack)):
         block_gate(got[i][rows], want[i], f"wan qk+cross node {wl.pack[i]}", ROUNDINGS["all"])
+
+
+def test_wan_width_qk_norm_256_token_tiles():
+    """Wan widths with qk-norm over one 3584-token chunk (one 28 x 128
+    frame): the QKV GEMM that also emits the sums of squares runs on
+    256-token tiles here (252 tiles, one round), whose v tile is staged
+    through LDS in two passes.  Sampled output rows, and the whole cached
+    K (normalised) and V pages, against the oracle."""
+    import dataclasses
+    geo = dataclasses.replace(WAN, grid_h=28, grid_w=128, frames_per_chunk=1)
+    qk = np.stack([gains(WAN.hidden, (44, TAG_GAIN, s)) for s in range(2)])
+    case = BlockCase(geo, "clean", [(1, 4)], [(0, 0)], seed=45, qk=qk)
+    got = case.run()
+    rows = sample_rows(geo.tokens_per_chunk, 24, seed=6)
+    want, new_kv = case.oracle(rows=rows)
+    block_gate(got[0][rows], want[0], "wan-width qk-norm 3584-token node (1, 4)", ROUNDINGS["qk"])
+    k_got, v_got = read_pages(case.pool, geo, case.n_slots, case.cache.slots((1, 4)))
+    block_gate(k_got, new_kv[0][0], "3584-token cached K (qk-norm)")
+    bf16_gates(v_got, new_kv[0][1], "3584-token cached V")
