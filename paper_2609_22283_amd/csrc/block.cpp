@@ -101,7 +101,7 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
   if (rope) {
     const sc_rope_desc& r = rope->desc;
     if (!rope->dev_table || r.grid_h * r.grid_w != d.tokens_per_page ||
-        r.dim_t + r.dim_h + r.dim_w != d.head_dim)
+        r.dim_t + r.dim_h + r.dim_w != d.head_dim || (r.dim_t | r.dim_h | r.dim_w) & 1)
       return fail(SC_EINVAL, "rope descriptor does not match the cache geometry");
   }
   // pages of states the pack does not produce must be written at this layer;
