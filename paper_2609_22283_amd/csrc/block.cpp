@@ -24,7 +24,7 @@ extern "C" size_t sc_block_workspace_bytes(const sc_block_weights* w, int32_t n_
   if (!w || n_tokens <= 0) return 0;
   const size_t T = (size_t)n_tokens;
   return align256(T * w->hidden * 2) * 3 + align256(T * w->mlp * 2) + attention_workspace_bound() +
-         align256(T * (2 * w->hidden / 128) * 4);
+         align256(T * (2 * w->hidden / kSsPartWidth) * 4);
 }
 
 extern "C" int sc_block_workspace_views(const sc_block_weights* w, int32_t n_tokens, size_t* q_offset,
@@ -168,7 +168,7 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
 
   if (w->qk_norm) {
     ep.ss_part = ssb;
-    ep.n_part = 2 * D / 128;
+    ep.n_part = 2 * D / kSsPartWidth;
     ep.qk_gain = w->qk_norm;
   }
 
@@ -179,7 +179,7 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
     NormScale ns;
     std::memset(&ns, 0, sizeof ns);
     ns.part = ssb;
-    ns.n_part = 2 * D / 128;
+    ns.n_part = 2 * D / kSsPartWidth;
     ns.D = D;
     ns.eps = kNormEps;
     ns.rows = qb;
@@ -217,7 +217,7 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
     ec.ld_out = D;
     if (cr->q_norm) {
       ec.ss_part = ssb;
-      ec.n_part = D / 128;
+      ec.n_part = D / kSsPartWidth;
     }
     if ((rc = launch_gemm(EPI_STORE, TK_GEMM_CROSS_Q, static_cast<const uint16_t*>(cr->w_q), hn, D, T, D, ec, stream)) != SC_OK)
       return rc;
@@ -225,7 +225,7 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
       NormScale ns;
       std::memset(&ns, 0, sizeof ns);
       ns.part = ssb;
-      ns.n_part = D / 128;
+      ns.n_part = D / kSsPartWidth;
       ns.D = D;
       ns.eps = kNormEps;
       ns.rows = qb;
@@ -269,7 +269,7 @@ extern "C" size_t sc_condition_workspace_bytes(const sc_cache* c) {
   if (!c) return 0;
   const size_t L = (size_t)c->d.tokens_per_page * c->d.pages_per_chunk;
   const size_t D = (size_t)c->d.n_heads * c->d.head_dim;
-  return 2 * align256(L * D * 2) + align256(L * (D / 128) * 4);
+  return 2 * align256(L * D * 2) + align256(L * (D / kSsPartWidth) * 4);
 }
 
 extern "C" int sc_condition_append(sc_cache* c, int32_t layer, sc_node st, const void* ctx,
@@ -305,7 +305,7 @@ extern "C" int sc_condition_append(sc_cache* c, int32_t layer, sc_node st, const
   e.ld_out = D;
   if (k_norm) {
     e.ss_part = ssb;
-    e.n_part = D / 128;
+    e.n_part = D / kSsPartWidth;
   }
   int rc;
   if ((rc = launch_gemm(EPI_STORE, TK_GEMM_CONDITION, static_cast<const uint16_t*>(w_k), xb, D, L, D, e, stream)) != SC_OK)
@@ -314,7 +314,7 @@ extern "C" int sc_condition_append(sc_cache* c, int32_t layer, sc_node st, const
     NormScale ns;
     std::memset(&ns, 0, sizeof ns);
     ns.part = ssb;
-    ns.n_part = D / 128;
+    ns.n_part = D / kSsPartWidth;
     ns.D = D;
     ns.eps = kNormEps;
     ns.rows = kb;

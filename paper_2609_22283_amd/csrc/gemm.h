@@ -12,6 +12,7 @@ enum { EPI_STORE = 0, EPI_QKV = 1, EPI_GELU = 2, EPI_RESIDUAL = 3 };
 
 constexpr int kGemmMaxNodes = 64;
 constexpr int kGemmMaxNodePages = 256;
+constexpr int kSsPartWidth = 64;  // features per sum-of-squares partial (qk-norm)
 
 struct GemmEpilogue {
   // STORE / GELU / RESIDUAL: out[t * ld_out + f]
@@ -34,8 +35,9 @@ struct GemmEpilogue {
   int32_t gate_row;
   int32_t node_level[kGemmMaxNodes];
   // Sums of squares for a later RMSNorm over features (qk-norm), STORE and
-  // QKV (q and k sections): ss_part[t * n_part + f / 128] = sum of D[f'][t]^2
-  // over the 128 features f' of f's wave tile, before any gain or RoPE.
+  // QKV (q and k sections): ss_part[t * n_part + f / kSsPartWidth] = sum of
+  // D[f'][t]^2 over the kSsPartWidth features f' of f's group, before any
+  // gain or RoPE.
   // NULL: none.  QKV with ss_part also multiplies q and k by qk_gain
   // ([2][hidden], the gains of q then k) before RoPE.
   float* ss_part;
@@ -45,7 +47,7 @@ struct GemmEpilogue {
 
 // Second half of an RMSNorm whose sums of squares came from a GEMM epilogue:
 // for each token t, inv = 1 / sqrt(sum_p part[t * n_part + p0 + p] / D + eps)
-// over the D / 128 partials of one tensor, then
+// over the D / kSsPartWidth partials of one tensor, then
 //   rows[t][:] *= inv (* gain[:] when gain != NULL)   (token-major, q)
 //   the token's k rows in its node's page slot *= inv  (k of the QKV pass)
 struct NormScale {
@@ -55,7 +57,7 @@ struct NormScale {
   uint16_t* rows;          // token-major [T][ld] rows (part offset 0), or NULL
   int32_t ld;
   const float* gain;       // [D] fp32 for rows, or NULL
-  char* layer_base;        // page-slot keys (part offset D / 128), or NULL
+  char* layer_base;        // page-slot keys (part offset D / kSsPartWidth), or NULL
   uint64_t slot_bytes;
   int32_t nq, tpp, ppc, head_dim;
   int32_t node_slot[kGemmMaxNodePages];

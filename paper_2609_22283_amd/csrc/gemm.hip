@@ -9,8 +9,8 @@
 //   GELU     out[t][f] = GELU_tanh(D)
 //   RESIDUAL x[t][f] += D   (in place)
 //   STORE    out[t][f] = D
-// QKV and STORE can also emit per-token sums of squares over each wave's 128
-// features, the first half of an RMSNorm over the feature axis (qk-norm);
+// QKV and STORE can also emit per-token sums of squares over each group of
+// 64 features, the first half of an RMSNorm over the feature axis (qk-norm);
 // norm_scale_kernel finishes it.
 // Work-group tile 256 (features) x BN (tokens: 256, 192 or 128) x 64 (k),
 // eight waves of 128 x BN/4, operands double-buffered in LDS with an XOR
@@ -57,25 +57,30 @@ __device__ __forceinline__ void gdma16(const char* base, uint32_t off, char* lds
       : "memory");
 }
 
-// Per-token sum of squares of a wave's 128 x 64 accumulator tile: lane
-// (lg, c16) holds 32 features of token c16 of each 16-token block; the four
-// lg lanes of a token are summed with two butterflies and lane lg = 0 stores.
+// Per-token sums of squares of a wave's accumulator tile, one partial per
+// kSsPartWidth (64) features: lane (lg, c16) holds 16 of a partial's features
+// for token c16 of each 16-token block; the four lg lanes of a token are
+// summed with two butterflies and lane lg = 0 stores partial part0 + g.
 template <int FB, int TB>
 __device__ __forceinline__ void store_sum_squares(const f32x4 (&acc)[FB][TB], float* ss,
-                                                  int32_t n_part, int32_t part, int32_t tw0,
+                                                  int32_t n_part, int32_t part0, int32_t tw0,
                                                   int32_t T, int32_t lg, int32_t c16) {
+  constexpr int FPG = kSsPartWidth / 16;  // 16-feature blocks per partial
+  static_assert(FB % FPG == 0, "whole partials per wave");
 #pragma unroll
-  for (int tb = 0; tb < TB; ++tb) {
-    float s = 0.f;
+  for (int g = 0; g < FB / FPG; ++g)
 #pragma unroll
-    for (int fb = 0; fb < FB; ++fb)
+    for (int tb = 0; tb < TB; ++tb) {
+      float s = 0.f;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) s = fmaf(acc[fb][tb][e], acc[fb][tb][e], s);
-    s += __shfl_xor(s, 16);
-    s += __shfl_xor(s, 32);
-    const int32_t t = tw0 + 16 * tb + c16;
-    if (lg == 0 && t < T) ss[(size_t)t * n_part + part] = s;
-  }
+      for (int fb = g * FPG; fb < (g + 1) * FPG; ++fb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s = fmaf(acc[fb][tb][e], acc[fb][tb][e], s);
+      s += __shfl_xor(s, 16);
+      s += __shfl_xor(s, 32);
+      const int32_t t = tw0 + 16 * tb + c16;
+      if (lg == 0 && t < T) ss[(size_t)t * n_part + part0 + g] = s;
+    }
 }
 
 // BN tokens per work-group tile.  Wave layout WL = 0: 2 (features) x 4
@@ -90,7 +95,6 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   // stage s: W tile at s * 64 KB, X tile at s * 64 KB + 32 KB; rows of 64 k
   // (128 B) with 16-byte column c stored at c ^ ((row >> 1) & 7)
   __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * G_TILE_BYTES];
-  static_assert(WL == 0 || EPI != EPI_STORE, "layout 1 is not used for the store epilogue");
   constexpr int WM = WL ? 64 : GWM;    // features per wave tile
   constexpr int GWN = WL ? BN / 2 : BN / 4;  // tokens per wave tile
   static_assert(GWN % 16 == 0, "wave tiles hold whole 16-token blocks");
@@ -218,17 +222,15 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   // f = f0 + wf + 16 fb + 4 lg + e (e = 0..3)
   if constexpr (EPI == EPI_QKV) {
     // a 256-feature tile lies in one of q, k, v (hidden is a multiple of 256)
-    // and each wave's 128 features in one head (head_dim 128)
+    // and each wave's 128 or 64 features in one head (head_dim 128)
     const int32_t sec = f0 / ep.hidden;
     const int32_t hf0 = f0 - sec * ep.hidden + wf;       // wave's first feature in its section
     const int32_t head = hf0 / ep.head_dim;
     const int32_t dbase = hf0 - head * ep.head_dim + 4 * lg;
-    // (qk-norm sums take one 128-feature head per wave: layout 0 only; the
-    // launcher never gives layout 1 a QKV launch with ss_part)
-    if (WL == 0 && ep.ss_part && sec < 2) {
+    if (ep.ss_part && sec < 2) {
       // qk-norm: sums of squares of the raw q or k, then the gain (before
       // RoPE); the 1 / rms factor is applied by norm_scale_kernel
-      store_sum_squares(acc, ep.ss_part, ep.n_part, (f0 + wf) / GWM, t0 + wt, T, lg, c16);
+      store_sum_squares(acc, ep.ss_part, ep.n_part, (f0 + wf) / kSsPartWidth, t0 + wt, T, lg, c16);
       const float* g = ep.qk_gain + f0 + wf + 4 * lg;
 #pragma unroll
       for (int fb = 0; fb < FB; ++fb) {
@@ -346,7 +348,7 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
     }
   } else {
     if (EPI == EPI_STORE && ep.ss_part)
-      store_sum_squares(acc, ep.ss_part, ep.n_part, (f0 + wf) / GWM, t0 + wt, T, lg, c16);
+      store_sum_squares(acc, ep.ss_part, ep.n_part, (f0 + wf) / kSsPartWidth, t0 + wt, T, lg, c16);
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
       const int32_t t = t0 + wt + 16 * tb + c16;
@@ -394,14 +396,21 @@ template <int BN, int WL>
 static void launch_gemm_bn(int epi, const uint16_t* W, const uint16_t* X, int32_t F, int32_t T, int32_t Kd,
                            const GemmEpilogue& ep, hipStream_t stream) {
   const dim3 grid((uint32_t)(F / GBM) * (uint32_t)((T + BN - 1) / BN));
-  if constexpr (WL == 1) {  // GELU, residual and QKV without qk-norm sums
-    if (epi == EPI_GELU)
-      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_GELU, BN, 1>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
-    else if (epi == EPI_QKV)
-      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV, BN, 1>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
-    else
-      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_RESIDUAL, BN, 1>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd,
-                         ep);
+  if constexpr (WL == 1) {
+    switch (epi) {
+      case EPI_QKV:
+        hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV, BN, 1>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
+        break;
+      case EPI_GELU:
+        hipLaunchKernelGGL((gemm_bf16_kernel<EPI_GELU, BN, 1>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
+        break;
+      case EPI_RESIDUAL:
+        hipLaunchKernelGGL((gemm_bf16_kernel<EPI_RESIDUAL, BN, 1>), grid, dim3(G_THREADS), 0, stream, W, X, F, T,
+                           Kd, ep);
+        break;
+      default:
+        hipLaunchKernelGGL((gemm_bf16_kernel<EPI_STORE, BN, 1>), grid, dim3(G_THREADS), 0, stream, W, X, F, T, Kd, ep);
+    }
   } else {
   switch (epi) {
     case EPI_QKV:
@@ -426,18 +435,15 @@ static void launch_gemm_bn(int epi, const uint16_t* W, const uint16_t* X, int32_
 // (more fragment reads and copies per MFMA), measured on the Wan block's
 // GEMMs.  The shape with the fewest tile-times wins, the wider one on ties.
 // Layout 1 (224-token tiles, a wave holds 64 features: half a head) serves
-// the GELU and residual epilogues and QKV without qk-norm sums, which need
-// a whole 128-feature head per wave.
+// every epilogue (sums of squares are kept per 64 features).
 struct GemmShape {
   int bn, wl;
 };
-static GemmShape gemm_tile_shape(int epi, int32_t F, int32_t T, bool qk_sums) {
+static GemmShape gemm_tile_shape(int32_t F, int32_t T) {
   GemmShape best{256, 0};
   double best_cost = 1e30;
-  const bool plain = epi == EPI_GELU || epi == EPI_RESIDUAL || (epi == EPI_QKV && !qk_sums);
   const GemmShape cands[] = {{256, 0}, {224, 1}, {192, 0}, {128, 0}};
   for (const GemmShape c : cands) {
-    if (c.wl == 1 && !plain) continue;
     const int64_t tiles = (int64_t)(F / GBM) * ((T + c.bn - 1) / c.bn);
     const double eff = c.bn == 256 ? 1.0 : c.bn == 224 ? 1.02 : c.bn == 192 ? 1.12 : 1.4;
     const double cost = (double)((tiles + kCUs - 1) / kCUs) * c.bn / 256.0 * eff;
@@ -470,7 +476,7 @@ int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, i
     e.gw_div = magic_div((uint32_t)ep.grid_w);
   }
   timer_begin(timer_kind, stream);
-  const GemmShape shape = gemm_tile_shape(epi, F, T, ep.ss_part != nullptr);
+  const GemmShape shape = gemm_tile_shape(F, T);
   if (shape.wl == 1)
     launch_gemm_bn<224, 1>(epi, W, X, F, T, Kd, e, stream);
   else if (shape.bn == 128)
@@ -547,7 +553,7 @@ __global__ __launch_bounds__(256) void norm_scale_kernel(int32_t T, NormScale ns
   const int32_t t = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int32_t lane = threadIdx.x & 63;
   if (t >= T) return;
-  const int32_t np = ns.D / 128, nv = ns.D / 8;
+  const int32_t np = ns.D / kSsPartWidth, nv = ns.D / 8;
   const float* pr = ns.part + (size_t)t * ns.n_part;
   auto scale8 = [&](u32x4* p, float inv, const float* gain) {
     const u32x4 a = *p;

@@ -289,7 +289,7 @@ def test_condition_append_and_cross_block_checks_without_device():
     cond = sc.sc_cache_create(0x100000, 1, 2, 128, 64, 1, 1)
     need = sc.sc_condition_workspace_bytes(cond)
     L, D = 64, 256
-    assert need == 2 * L * D * 2 + L * (D // 128) * 4
+    assert need == 2 * L * D * 2 + L * (D // 64) * 4
     args = dict(ctx=0x1000, w_k=0x2000, w_v=0x3000, k_norm=None, ws=0x4000)
     for layer, ws_bytes, extra, code in [(1, need, {}, sc.SC_EINVAL),         # layer out of range
                                          (0, need - 1, {}, sc.SC_EINVAL),     # workspace too small
