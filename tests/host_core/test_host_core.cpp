@@ -7,14 +7,18 @@
 // the schedule (Eq. 7 rounds, Eq. 2 serial order, the release rule), and the
 // block and stack orchestration's error paths: a launch failing at any point
 // of a block leaves the pack's states unwritten, and a stack failing in its
-// second layer leaves the first layer unwritten too.  Exit status 0 when
-// every check holds; the sanitizers abort on the first memory or UB error.
+// second layer leaves the first layer unwritten too.  Also the magic
+// dividers the kernels split token indices with: exact quotients for every
+// divisor up to 4096 and the workload's own.  Exit status 0 when every check
+// holds; the sanitizers abort on the first memory or UB error.
+#include <cstdint>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <vector>
 
 #include "../../include/streamctx.h"
+#include "../../paper_2609_22283_amd/csrc/divmagic.h"
 
 extern int g_launches;
 extern int g_fail_at;
@@ -289,8 +293,46 @@ static void test_block_error_paths() {
   }
 }
 
+// The quotient as the kernels form it: (high 32 bits of n * mul, + n) >> shift.
+static uint32_t magic_quotient(uint32_t n, const sc::DivMagic& m) {
+  const uint32_t hi = (uint32_t)(((uint64_t)n * m.mul) >> 32);
+  return (hi + n) >> m.shift;
+}
+
+static void test_magic_div() {
+  std::vector<uint32_t> divs;
+  for (uint32_t d = 1; d <= 4096; ++d) divs.push_back(d);
+  // node sizes, page sizes and grid widths of the workloads, and large ones
+  for (uint32_t d : {4680u, 9360u, 14040u, 18720u, 23400u, 1560u, 3120u, 6241u, 65535u, 65536u, 65537u,
+                     1000003u, (1u << 30) - 1, 1u << 30, (1u << 30) + 1, (1u << 31) - 1})
+    divs.push_back(d);
+  uint64_t state = 0x9e3779b97f4a7c15ull;  // xorshift64 numerators
+  int bad = 0;
+  for (uint32_t d : divs) {
+    const sc::DivMagic m = sc::magic_div(d);
+    if (m.div != d) ++bad;
+    // quotient boundaries k d - 1, k d for small k and near 2^31, then random n < 2^31
+    std::vector<uint32_t> ns = {0u, 1u, (1u << 31) - 1, (1u << 31) - 2};
+    for (uint32_t k = 1; k <= 64; ++k) {
+      const uint64_t kd = (uint64_t)k * d, top = (uint64_t)((((1ull << 31) - 1) / d) - (k - 1)) * d;
+      if (kd < (1ull << 31)) ns.insert(ns.end(), {(uint32_t)(kd - 1), (uint32_t)kd});
+      if (top > 0 && top < (1ull << 31)) ns.insert(ns.end(), {(uint32_t)(top - 1), (uint32_t)top});
+    }
+    for (int i = 0; i < 256; ++i) {
+      state ^= state << 13;
+      state ^= state >> 7;
+      state ^= state << 17;
+      ns.push_back((uint32_t)(state & 0x7fffffffu));
+    }
+    for (uint32_t n : ns)
+      if (magic_quotient(n, m) != n / d) ++bad;
+  }
+  CHECK(bad == 0);
+}
+
 int main() {
   CHECK(sc_abi_version() == SC_ABI_VERSION);
+  test_magic_div();
   test_selection();
   test_cache_and_plan();
   test_schedule();
