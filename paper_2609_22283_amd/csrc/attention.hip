@@ -398,7 +398,13 @@ struct KvTiles {
     const int32_t lim = nk - t0, split = bkey - t0;
     if (split >= BK && lim >= BK) {
 #pragma unroll
-      for (int j = 0; j < VCP; ++j) dma16(lbase, lo + vlane[j], vl + (RPI * VCP * wave + RPI * j) * 2 * BK);
+      for (int j = 0; j < VCP; ++j) {
+        // opaque, so the offset stays one add of the scalar base (the
+        // compiler otherwise re-derives it with a per-lane multiply)
+        uint32_t off = vlane[j];
+        asm volatile("" : "+v"(off));
+        dma16(lbase, lo + off, vl + (RPI * VCP * wave + RPI * j) * 2 * BK);
+      }
       return;
     }
     const uint32_t hi = sl.hi + vhead + (uint32_t)(t0 - bkey) * 2;
