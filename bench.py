@@ -202,7 +202,7 @@ def time_steps(setup, fn, steps, warmup, timer=False):
     kernels = {}
     if timer:
         for kind in ("attention", "attention_combine", "gemm_qkv", "gemm_out", "gemm_up",
-                     "gemm_down", "rmsnorm", "sampler", "qk_norm", "cross_attention",
+                     "gemm_down", "rmsnorm", "row_scale", "sampler", "qk_norm", "cross_attention",
                      "gemm_cross_q", "gemm_cross_out"):
             n, tot = sc.sc_timer_read(kind)
             if n:

@@ -25,7 +25,8 @@ extern "C" {
  * "attention" is the main kernel alone), "qk_norm" (the per-token scaling of
  * qk-norm and of the normalised condition queries and keys),
  * "cross_attention", "gemm_cross_q", "gemm_cross_out", "gemm_condition"
- * (the projections of sc_condition_append).  Enabling clears earlier records.  Events are created
+ * (the projections of sc_condition_append), "row_scale" (the 1 / rms per
+ * token of an RMSNorm folded into the MLP's first GEMM).  Enabling clears earlier records.  Events are created
  * lazily and reused; the cost is two event records per launch. */
 int sc_timer_enable(int on);
 int sc_timer_read(const char* kind, int32_t* launches, double* total_ms);

@@ -18,8 +18,8 @@ static size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
 
 constexpr float kNormEps = 1e-6f;
 
-// workspace: normalised input | q | attention output | MLP hidden |
-// attention partials | qk-norm partial sums of squares
+// workspace: normalised input (or the folded RMSNorm's per-token factors) | q |
+// attention output | MLP hidden | attention partials | partial sums of squares
 extern "C" size_t sc_block_workspace_bytes(const sc_block_weights* w, int32_t n_tokens) {
   if (!w || n_tokens <= 0) return 0;
   const size_t T = (size_t)n_tokens;
@@ -204,6 +204,13 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
   e2.mod = w->mod;
   e2.gate_row = 2;  // gate_a
   for (int32_t i = 0; i < n; ++i) e2.node_level[i] = p->nodes[i].level;
+  // Without modulation the MLP's RMSNorm folds into its first GEMM: the last
+  // residual GEMM before it stores per-64-feature sums of squares of the rows
+  // it writes (part-major in ssb), a per-token kernel turns them into 1 / rms
+  // (into hn's region, unused then), and the GELU epilogue scales each
+  // token's accumulators by it, reading the raw rows x.
+  const bool fold_mlp_norm = !w->mod;
+  if (fold_mlp_norm && !w->cross) e2.ss_part = ssb;
   if ((rc = launch_gemm(EPI_RESIDUAL, TK_GEMM_OUT, static_cast<const uint16_t*>(w->w_o), ob, D, T, D, e2, stream)) != SC_OK)
     return rc;
   if (const sc_cross_attn* cr = w->cross) {
@@ -244,17 +251,27 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
     eo.out = xb;
     eo.ld_out = D;
     eo.nq = p->nq;
+    if (fold_mlp_norm) eo.ss_part = ssb;
     if ((rc = launch_gemm(EPI_RESIDUAL, TK_GEMM_CROSS_OUT, static_cast<const uint16_t*>(cr->w_o), ob, D, T, D, eo, stream)) != SC_OK)
       return rc;
   }
-  if ((rc = launch_rmsnorm(xb, hn, T, D, nm_m, stream)) != SC_OK) return rc;
   GemmEpilogue e3;
   std::memset(&e3, 0, sizeof e3);
   e3.out = ub;
   e3.ld_out = w->mlp;
-  if ((rc = launch_gemm(EPI_GELU, TK_GEMM_UP, static_cast<const uint16_t*>(w->w_up), hn, w->mlp, T, D, e3, stream)) != SC_OK)
+  const uint16_t* mlp_in = hn;
+  if (fold_mlp_norm) {
+    float* rsb = reinterpret_cast<float*>(hn);
+    if ((rc = launch_row_scale(ssb, D / kSsPartWidth, T, D, kNormEps, rsb, stream)) != SC_OK) return rc;
+    e3.row_scale = rsb;
+    mlp_in = xb;
+  } else if ((rc = launch_rmsnorm(xb, hn, T, D, nm_m, stream)) != SC_OK) {
+    return rc;
+  }
+  if ((rc = launch_gemm(EPI_GELU, TK_GEMM_UP, static_cast<const uint16_t*>(w->w_up), mlp_in, w->mlp, T, D, e3, stream)) != SC_OK)
     return rc;
   GemmEpilogue e4 = e2;
+  e4.ss_part = nullptr;
   e4.gate_row = 5;  // gate_m
   if ((rc = launch_gemm(EPI_RESIDUAL, TK_GEMM_DOWN, static_cast<const uint16_t*>(w->w_down), ub, D, T, w->mlp, e4, stream)) != SC_OK)
     return rc;

@@ -34,10 +34,17 @@ struct GemmEpilogue {
   const float* mod;
   int32_t gate_row;
   int32_t node_level[kGemmMaxNodes];
+  // GELU with row_scale: an RMSNorm of the input rows folded into the GEMM.
+  // X holds the raw rows; each token's accumulators are multiplied by
+  // row_scale[t] (1 / rms of its row, launch_row_scale) before the GELU.
+  // NULL: none.
+  const float* row_scale;
   // Sums of squares for a later RMSNorm over features (qk-norm), STORE and
   // QKV (q and k sections): ss_part[t * n_part + f / kSsPartWidth] = sum of
   // D[f'][t]^2 over the kSsPartWidth features f' of f's group, before any
-  // gain or RoPE.
+  // gain or RoPE.  RESIDUAL: the same over the updated rows as stored (bf16)
+  // but part-major, ss_part[(f / kSsPartWidth) * T + t], for an RMSNorm of
+  // the result folded into the next GEMM (n_part unused).
   // NULL: none.  QKV with ss_part also multiplies q and k by qk_gain
   // ([2][hidden], the gains of q then k) before RoPE.
   float* ss_part;
@@ -77,5 +84,11 @@ int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, i
 int launch_norm_scale(int32_t T, const NormScale& ns, hipStream_t stream);
 int launch_rmsnorm(const uint16_t* x, uint16_t* y, int32_t rows, int32_t D, const NormMod& nm,
                    hipStream_t stream);
+// The second half of an RMSNorm without modulation or gain whose sums of
+// squares a RESIDUAL epilogue stored part-major: for t < T,
+//   scale[t] = 1 / sqrt(sum_{p < n_part} part[p * T + t] / D + eps),
+// summed in increasing p (deterministic).  Feeds GemmEpilogue::row_scale.
+int launch_row_scale(const float* part, int32_t n_part, int32_t T, int32_t D, float eps, float* scale,
+                     hipStream_t stream);
 
 }  // namespace sc

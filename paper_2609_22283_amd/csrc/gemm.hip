@@ -6,15 +6,17 @@
 //   QKV      RoPE on q and k; q to a token-major buffer; k and v scattered
 //            into the pack nodes' page slots (k as [head][token][d], v as
 //            [head][d][token], transposed through LDS into 8-token runs)
-//   GELU     out[t][f] = GELU_tanh(D)
+//   GELU     out[t][f] = GELU_tanh(D), or GELU_tanh(row_scale[t] D) with an
+//            RMSNorm of the input folded in (X then holds the raw rows)
 //   RESIDUAL x[t][f] += D   (in place)
 //   STORE    out[t][f] = D
 // QKV and STORE can also emit per-token sums of squares over each group of
 // 64 features, the first half of an RMSNorm over the feature axis (qk-norm);
-// norm_scale_kernel finishes it.
-// Work-group tile 256 (features) x BN (tokens: 256, 192 or 128) x 64 (k),
-// eight waves of 128 x BN/4, operands double-buffered in LDS with an XOR
-// swizzle.  Each lane holds four consecutive features of one token, so RoPE
+// norm_scale_kernel finishes it.  RESIDUAL can emit them for the rows it
+// writes, part-major; row_scale_kernel turns them into GELU's row_scale.
+// Work-group tile 256 (features) x BN (tokens: 256, 224, 192 or 128) x 64
+// (k), eight waves (2 x 4 of 128 x BN/4, or 4 x 2 of 64 x BN/2 at 224),
+// operands double-buffered in LDS with an XOR swizzle.  Each lane holds four consecutive features of one token, so RoPE
 // pairs stay in-lane.
 #include "device.h"
 #include "gemm.h"
@@ -195,6 +197,18 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
       for (int fb = 0; fb < FB; ++fb) res[tb][fb] = *reinterpret_cast<const u32x2*>(orow + 16 * fb);
     }
   }
+  // The folded RMSNorm's per-token factors (GELU epilogue): lane j loads
+  // those of the wave's tokens j and j + 64 (two coalesced loads at most),
+  // also before the main loop; the epilogue takes each token's from its lane.
+  constexpr bool ROWPRE = EPI == EPI_GELU;
+  constexpr int RT = ROWPRE ? (GWN + 63) / 64 : 1;
+  float rtok[RT];
+  if constexpr (ROWPRE) {
+    if (ep.row_scale) {
+#pragma unroll
+      for (int r = 0; r < RT; ++r) rtok[r] = ep.row_scale[min(t0 + wt + 64 * r + lane, T - 1)];
+    }
+  }
 
   const int32_t nk = Kd / GBK;
   issue(0, 0);
@@ -349,11 +363,23 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   } else {
     if (EPI == EPI_STORE && ep.ss_part)
       store_sum_squares(acc, ep.ss_part, ep.n_part, (f0 + wf) / kSsPartWidth, t0 + wt, T, lg, c16);
+    constexpr int FPG = kSsPartWidth / 16;  // 16-feature blocks per sum-of-squares partial
+    static_assert(FB % FPG == 0, "whole partials per wave");
+    const bool row_sums = EPI == EPI_RESIDUAL && ep.ss_part;
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
       const int32_t t = t0 + wt + 16 * tb + c16;
-      if (t >= T) continue;
+      // the folded RMSNorm's factor of token 16 tb + c16 of the wave, from
+      // the lane that loaded it (while every lane is active)
+      float rscale = 1.f;
+      if constexpr (ROWPRE) {
+        if (ep.row_scale) rscale = __shfl(rtok[tb >> 2], 16 * (tb & 3) + c16);
+      }
+      if (t >= T) continue;  // uniform over the 4 lanes of a token, so the butterflies below stay inside it
       uint16_t* orow = ep.out + (size_t)t * ep.ld_out + f0 + wf + 4 * lg;
+      float ssq[FB / FPG];
+#pragma unroll
+      for (int g = 0; g < FB / FPG; ++g) ssq[g] = 0.f;
       // noise-level gate of this token's node (residual epilogue only)
       const float* gate = nullptr;
       if (EPI == EPI_RESIDUAL && ep.mod)
@@ -381,13 +407,27 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
             v[3] += __uint_as_float(r.y & 0xffff0000u);
           } else if constexpr (EPI == EPI_GELU) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
+            for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e] * rscale);
           }
           u32x2 pk;
           pk.x = pack_bf16x2(v[0], v[1]);
           pk.y = pack_bf16x2(v[2], v[3]);
           *reinterpret_cast<u32x2*>(dst) = pk;
+          if (row_sums) {  // of the values as stored
+            const float a = __uint_as_float(pk.x << 16), b = __uint_as_float(pk.x & 0xffff0000u);
+            const float c = __uint_as_float(pk.y << 16), d = __uint_as_float(pk.y & 0xffff0000u);
+            ssq[fb / FPG] = fmaf(a, a, fmaf(b, b, fmaf(c, c, fmaf(d, d, ssq[fb / FPG]))));
+          }
         }
+      if (row_sums) {
+#pragma unroll
+        for (int g = 0; g < FB / FPG; ++g) {
+          float sq = ssq[g];
+          sq += __shfl_xor(sq, 16);
+          sq += __shfl_xor(sq, 32);
+          if (lg == 0) ep.ss_part[(size_t)((f0 + wf) / kSsPartWidth + g) * T + t] = sq;
+        }
+      }
     }
   }
 }
@@ -464,6 +504,7 @@ int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, i
     return fail(SC_EUNSUPPORTED, "gemm operands beyond 4 GB");
   if (epi == EPI_QKV && (ep.hidden % GBM || ep.head_dim != GWM))
     return fail(SC_EUNSUPPORTED, "QKV epilogue needs hidden %% %d == 0 and head_dim %d", GBM, GWM);
+  if (ep.row_scale && epi != EPI_GELU) return fail(SC_EINVAL, "row_scale is a GELU epilogue input");
   GemmEpilogue e = ep;
   if (epi == EPI_QKV) {
     // v goes out in 16-byte runs of 8 tokens within one page
@@ -619,6 +660,28 @@ int launch_rmsnorm(const uint16_t* x, uint16_t* y, int32_t rows, int32_t D, cons
   hipLaunchKernelGGL(rmsnorm_kernel, dim3((rows + 3) / 4), dim3(256), 0, stream, x, y, rows, D, 1e-6f,
                      nm);
   timer_end(TK_RMSNORM, stream);
+  SC_HIP(hipGetLastError());
+  return SC_OK;
+}
+
+// One thread per token; partial p of all tokens is contiguous, so each of
+// the n_part loads of a wave reads 256 consecutive bytes.
+__global__ __launch_bounds__(256) void row_scale_kernel(const float* __restrict__ part, int32_t n_part, int32_t T,
+                                                        float inv_d, float eps, float* __restrict__ scale) {
+  const int32_t t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= T) return;
+  float s = 0.f;
+  for (int32_t p = 0; p < n_part; ++p) s += part[(size_t)p * T + t];
+  scale[t] = rsqrtf(s * inv_d + eps);
+}
+
+int launch_row_scale(const float* part, int32_t n_part, int32_t T, int32_t D, float eps, float* scale,
+                     hipStream_t stream) {
+  if (T <= 0 || n_part <= 0 || D <= 0) return fail(SC_EINVAL, "row_scale needs T, n_part, D > 0");
+  timer_begin(TK_ROW_SCALE, stream);
+  hipLaunchKernelGGL(row_scale_kernel, dim3((T + 255) / 256), dim3(256), 0, stream, part, n_part, T,
+                     1.0f / (float)D, eps, scale);
+  timer_end(TK_ROW_SCALE, stream);
   SC_HIP(hipGetLastError());
   return SC_OK;
 }

@@ -110,7 +110,7 @@ int launch_rope_table(const sc_rope_desc* d, void* table, hipStream_t stream);
 enum TimerKind {
   TK_ATTENTION = 0, TK_GEMM_QKV, TK_GEMM_OUT, TK_GEMM_UP, TK_GEMM_DOWN, TK_RMSNORM, TK_APPEND,
   TK_SAMPLER, TK_ATTN_COMBINE, TK_QK_NORM, TK_CROSS_ATTENTION, TK_GEMM_CROSS_Q,
-  TK_GEMM_CROSS_OUT, TK_GEMM_CONDITION, TK_COUNT
+  TK_GEMM_CROSS_OUT, TK_GEMM_CONDITION, TK_ROW_SCALE, TK_COUNT
 };
 void timer_begin(int kind, hipStream_t stream);
 void timer_end(int kind, hipStream_t stream);

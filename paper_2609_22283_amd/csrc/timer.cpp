@@ -10,7 +10,8 @@ namespace {
 const char* const kNames[TK_COUNT] = {"attention", "gemm_qkv", "gemm_out", "gemm_up",
                                       "gemm_down", "rmsnorm", "append", "sampler",
                                       "attention_combine", "qk_norm", "cross_attention",
-                                      "gemm_cross_q", "gemm_cross_out", "gemm_condition"};
+                                      "gemm_cross_q", "gemm_cross_out", "gemm_condition",
+                                      "row_scale"};
 
 struct Record {
   int kind;

@@ -38,6 +38,9 @@ int launch_norm_scale(int32_t, const NormScale&, hipStream_t) { return launched(
 int launch_rmsnorm(const uint16_t*, uint16_t*, int32_t, int32_t, const NormMod&, hipStream_t) {
   return launched("rmsnorm");
 }
+int launch_row_scale(const float*, int32_t, int32_t, int32_t, float, float*, hipStream_t) {
+  return launched("row_scale");
+}
 TimerAlias::TimerAlias(int from_, int to) : from(from_), prev(to) {}
 TimerAlias::~TimerAlias() {}
 
