@@ -18,7 +18,7 @@ static size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
 
 constexpr float kNormEps = 1e-6f;
 
-// workspace: normalised input (or the folded RMSNorm's per-token factors) | q |
+// workspace: normalised input (or the folded RMSNorms' per-token factors) | q |
 // attention output | MLP hidden | attention partials | partial sums of squares
 extern "C" size_t sc_block_workspace_bytes(const sc_block_weights* w, int32_t n_tokens) {
   if (!w || n_tokens <= 0) return 0;
@@ -172,8 +172,19 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
     ep.qk_gain = w->qk_norm;
   }
 
-  if ((rc = launch_rmsnorm(xb, hn, T, D, nm_a, stream)) != SC_OK) return rc;
-  if ((rc = launch_gemm(EPI_QKV, TK_GEMM_QKV, static_cast<const uint16_t*>(w->w_qkv), hn, 3 * D, T, D, ep, stream)) != SC_OK)
+  // Without modulation the pre-attention RMSNorm folds into the QKV GEMM:
+  // one pass over x writes each token's 1 / rms (into hn's region), and the
+  // QKV epilogue scales the token's accumulators by it, reading the raw rows.
+  const uint16_t* qkv_in = hn;
+  if (!w->mod) {
+    float* rsa = reinterpret_cast<float*>(hn);
+    if ((rc = launch_row_rms(xb, T, D, rsa, stream)) != SC_OK) return rc;
+    ep.row_scale = rsa;
+    qkv_in = xb;
+  } else if ((rc = launch_rmsnorm(xb, hn, T, D, nm_a, stream)) != SC_OK) {
+    return rc;
+  }
+  if ((rc = launch_gemm(EPI_QKV, TK_GEMM_QKV, static_cast<const uint16_t*>(w->w_qkv), qkv_in, 3 * D, T, D, ep, stream)) != SC_OK)
     return rc;
   if (w->qk_norm) {  // 1 / rms of q (token-major) and of k (in the page slots)
     NormScale ns;

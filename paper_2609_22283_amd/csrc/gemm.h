@@ -34,9 +34,10 @@ struct GemmEpilogue {
   const float* mod;
   int32_t gate_row;
   int32_t node_level[kGemmMaxNodes];
-  // GELU with row_scale: an RMSNorm of the input rows folded into the GEMM.
-  // X holds the raw rows; each token's accumulators are multiplied by
-  // row_scale[t] (1 / rms of its row, launch_row_scale) before the GELU.
+  // GELU or QKV with row_scale: an RMSNorm of the input rows folded into the
+  // GEMM.  X holds the raw rows; each token's accumulators are multiplied by
+  // row_scale[t] (1 / rms of its row: launch_row_scale or launch_row_rms)
+  // before the GELU, or before anything else of the QKV epilogue.
   // NULL: none.
   const float* row_scale;
   // Sums of squares for a later RMSNorm over features (qk-norm), STORE and
@@ -84,6 +85,10 @@ int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, i
 int launch_norm_scale(int32_t T, const NormScale& ns, hipStream_t stream);
 int launch_rmsnorm(const uint16_t* x, uint16_t* y, int32_t rows, int32_t D, const NormMod& nm,
                    hipStream_t stream);
+// The factor alone of an RMSNorm without modulation or gain, from the rows
+// themselves: scale[r] = 1 / sqrt(mean_f x[r][f]^2 + 1e-6) (a read of x,
+// no write of the normalised rows).  Feeds GemmEpilogue::row_scale.
+int launch_row_rms(const uint16_t* x, int32_t rows, int32_t D, float* scale, hipStream_t stream);
 // The second half of an RMSNorm without modulation or gain whose sums of
 // squares a RESIDUAL epilogue stored part-major: for t < T,
 //   scale[t] = 1 / sqrt(sum_{p < n_part} part[p * T + t] / D + eps),

@@ -18,6 +18,8 @@
 // (k), eight waves (2 x 4 of 128 x BN/4, or 4 x 2 of 64 x BN/2 at 224),
 // operands double-buffered in LDS with an XOR swizzle.  Each lane holds four consecutive features of one token, so RoPE
 // pairs stay in-lane.
+#include <cstring>
+
 #include "device.h"
 #include "gemm.h"
 #include "internal.h"
@@ -197,10 +199,11 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
       for (int fb = 0; fb < FB; ++fb) res[tb][fb] = *reinterpret_cast<const u32x2*>(orow + 16 * fb);
     }
   }
-  // The folded RMSNorm's per-token factors (GELU epilogue): lane j loads
-  // those of the wave's tokens j and j + 64 (two coalesced loads at most),
-  // also before the main loop; the epilogue takes each token's from its lane.
-  constexpr bool ROWPRE = EPI == EPI_GELU;
+  // The folded RMSNorm's per-token factors (GELU and QKV epilogues): lane j
+  // loads those of the wave's tokens j and j + 64 (two coalesced loads at
+  // most), also before the main loop; the epilogue takes each token's from
+  // its lane.
+  constexpr bool ROWPRE = EPI == EPI_GELU || EPI == EPI_QKV;
   constexpr int RT = ROWPRE ? (GWN + 63) / 64 : 1;
   float rtok[RT];
   if constexpr (ROWPRE) {
@@ -235,6 +238,18 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
   // epilogue: lane holds D[f][t] for t = t0 + wt + 16 tb + c16 and
   // f = f0 + wf + 16 fb + 4 lg + e (e = 0..3)
   if constexpr (EPI == EPI_QKV) {
+    // the folded RMSNorm of the input rows: q, k and v are linear in the
+    // row, so its 1 / rms scales the accumulators before anything else
+    if (ep.row_scale) {
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb) {
+        const float r = __shfl(rtok[tb >> 2], 16 * (tb & 3) + c16);
+#pragma unroll
+        for (int fb = 0; fb < FB; ++fb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[fb][tb][e] *= r;
+      }
+    }
     // a 256-feature tile lies in one of q, k, v (hidden is a multiple of 256)
     // and each wave's 128 or 64 features in one head (head_dim 128)
     const int32_t sec = f0 / ep.hidden;
@@ -504,7 +519,8 @@ int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, i
     return fail(SC_EUNSUPPORTED, "gemm operands beyond 4 GB");
   if (epi == EPI_QKV && (ep.hidden % GBM || ep.head_dim != GWM))
     return fail(SC_EUNSUPPORTED, "QKV epilogue needs hidden %% %d == 0 and head_dim %d", GBM, GWM);
-  if (ep.row_scale && epi != EPI_GELU) return fail(SC_EINVAL, "row_scale is a GELU epilogue input");
+  if (ep.row_scale && epi != EPI_GELU && epi != EPI_QKV)
+    return fail(SC_EINVAL, "row_scale is a GELU or QKV epilogue input");
   GemmEpilogue e = ep;
   if (epi == EPI_QKV) {
     // v goes out in 16-byte runs of 8 tokens within one page
@@ -535,8 +551,8 @@ int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, i
 // y = x / sqrt(mean(x^2) + eps), one wave per row, fp32 math, bf16 in/out;
 // with a modulation table, y * (1 + scale) + shift of the row's node level.
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict__ x,
-                                                      uint16_t* __restrict__ y, int32_t rows,
-                                                      int32_t D, float eps, NormMod nm) {
+                                                      uint16_t* __restrict__ y, float* __restrict__ inv_out,
+                                                      int32_t rows, int32_t D, float eps, NormMod nm) {
   const int32_t row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int32_t lane = threadIdx.x & 63;
   if (row >= rows) return;
@@ -555,6 +571,10 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
   const float inv = rsqrtf(ss / (float)D + eps);
+  if (inv_out) {  // the factor alone, for a GEMM that folds the norm in
+    if (lane == 0) inv_out[row] = inv;
+    return;
+  }
   const float *shift = nullptr, *scale = nullptr;
   if (nm.mod) {
     const int32_t lev = nm.node_level[row / nm.nq];
@@ -657,8 +677,20 @@ int launch_rmsnorm(const uint16_t* x, uint16_t* y, int32_t rows, int32_t D, cons
                    hipStream_t stream) {
   if (D % 8) return fail(SC_EUNSUPPORTED, "rmsnorm needs D %% 8 == 0");
   timer_begin(TK_RMSNORM, stream);
-  hipLaunchKernelGGL(rmsnorm_kernel, dim3((rows + 3) / 4), dim3(256), 0, stream, x, y, rows, D, 1e-6f,
-                     nm);
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3((rows + 3) / 4), dim3(256), 0, stream, x, y, nullptr, rows, D,
+                     1e-6f, nm);
+  timer_end(TK_RMSNORM, stream);
+  SC_HIP(hipGetLastError());
+  return SC_OK;
+}
+
+int launch_row_rms(const uint16_t* x, int32_t rows, int32_t D, float* scale, hipStream_t stream) {
+  if (D % 8) return fail(SC_EUNSUPPORTED, "rmsnorm needs D %% 8 == 0");
+  NormMod plain;
+  std::memset(&plain, 0, sizeof plain);
+  timer_begin(TK_RMSNORM, stream);
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3((rows + 3) / 4), dim3(256), 0, stream, x, nullptr, scale, rows, D,
+                     1e-6f, plain);
   timer_end(TK_RMSNORM, stream);
   SC_HIP(hipGetLastError());
   return SC_OK;

@@ -41,6 +41,7 @@ int launch_rmsnorm(const uint16_t*, uint16_t*, int32_t, int32_t, const NormMod&,
 int launch_row_scale(const float*, int32_t, int32_t, int32_t, float, float*, hipStream_t) {
   return launched("row_scale");
 }
+int launch_row_rms(const uint16_t*, int32_t, int32_t, float*, hipStream_t) { return launched("row_rms"); }
 TimerAlias::TimerAlias(int from_, int to) : from(from_), prev(to) {}
 TimerAlias::~TimerAlias() {}
 

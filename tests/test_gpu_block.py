@@ -9,9 +9,9 @@ are averaged over >= 256-term dot products.  Gates: elementwise
 |gpu - oracle| <= 2e-2 * max(1, |oracle|), and
 mean |gpu - oracle| <= 4e-3 * max(1, mean |oracle|) (two residual roundings
 of ~2^-9 each, with margin).  The K/V the block writes into the cache use the
-attention gates.  Without level modulation the second norm is folded into the
-MLP's first GEMM and its output is never rounded, so that block has six
-roundings; the gates keep the count of seven.
+attention gates.  Without level modulation both norms are folded into the
+GEMMs that follow them and their outputs are never rounded, so that block has
+five roundings; the gates keep the count of seven.
 """
 import math
 
