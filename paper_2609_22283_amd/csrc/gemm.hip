@@ -697,12 +697,14 @@ int launch_row_rms(const uint16_t* x, int32_t rows, int32_t D, float* scale, hip
 }
 
 // One thread per token; partial p of all tokens is contiguous, so each of
-// the n_part loads of a wave reads 256 consecutive bytes.
+// the n_part loads of a wave reads 256 consecutive bytes.  Unrolled so that
+// eight loads are in flight at once; the adds keep increasing p.
 __global__ __launch_bounds__(256) void row_scale_kernel(const float* __restrict__ part, int32_t n_part, int32_t T,
                                                         float inv_d, float eps, float* __restrict__ scale) {
   const int32_t t = blockIdx.x * 256 + threadIdx.x;
   if (t >= T) return;
   float s = 0.f;
+#pragma unroll 8
   for (int32_t p = 0; p < n_part; ++p) s += part[(size_t)p * T + t];
   scale[t] = rsqrtf(s * inv_d + eps);
 }
