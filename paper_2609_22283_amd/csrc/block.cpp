@@ -225,19 +225,20 @@ extern "C" int sc_block_forward(const sc_block_weights* w, sc_cache* c, int32_t 
   if ((rc = launch_gemm(EPI_RESIDUAL, TK_GEMM_OUT, static_cast<const uint16_t*>(w->w_o), ob, D, T, D, e2, stream)) != SC_OK)
     return rc;
   if (const sc_cross_attn* cr = w->cross) {
-    NormMod plain;
-    std::memset(&plain, 0, sizeof plain);
-    plain.nq = p->nq;
-    if ((rc = launch_rmsnorm(xb, hn, T, D, plain, stream)) != SC_OK) return rc;
+    // the query's RMSNorm (no modulation) folded into its GEMM, the factors
+    // in hn's region (free once the QKV GEMM has read it)
+    float* rsq = reinterpret_cast<float*>(hn);
+    if ((rc = launch_row_rms(xb, T, D, rsq, stream)) != SC_OK) return rc;
     GemmEpilogue ec;
     std::memset(&ec, 0, sizeof ec);
     ec.out = qb;
     ec.ld_out = D;
+    ec.row_scale = rsq;
     if (cr->q_norm) {
       ec.ss_part = ssb;
       ec.n_part = D / kSsPartWidth;
     }
-    if ((rc = launch_gemm(EPI_STORE, TK_GEMM_CROSS_Q, static_cast<const uint16_t*>(cr->w_q), hn, D, T, D, ec, stream)) != SC_OK)
+    if ((rc = launch_gemm(EPI_STORE, TK_GEMM_CROSS_Q, static_cast<const uint16_t*>(cr->w_q), xb, D, T, D, ec, stream)) != SC_OK)
       return rc;
     if (cr->q_norm) {
       NormScale ns;

@@ -34,11 +34,10 @@ struct GemmEpilogue {
   const float* mod;
   int32_t gate_row;
   int32_t node_level[kGemmMaxNodes];
-  // GELU or QKV with row_scale: an RMSNorm of the input rows folded into the
-  // GEMM.  X holds the raw rows; each token's accumulators are multiplied by
-  // row_scale[t] (1 / rms of its row: launch_row_scale or launch_row_rms)
-  // before the GELU, or before anything else of the QKV epilogue.
-  // NULL: none.
+  // QKV, GELU and STORE with row_scale: an RMSNorm of the input rows folded
+  // into the GEMM.  X holds the raw rows; each token's accumulators are
+  // multiplied by row_scale[t] (1 / rms of its row: launch_row_scale or
+  // launch_row_rms) before anything else of the epilogue.  NULL: none.
   const float* row_scale;
   // Sums of squares for a later RMSNorm over features (qk-norm), STORE and
   // QKV (q and k sections): ss_part[t * n_part + f / kSsPartWidth] = sum of

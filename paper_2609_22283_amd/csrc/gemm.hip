@@ -6,14 +6,15 @@
 //   QKV      RoPE on q and k; q to a token-major buffer; k and v scattered
 //            into the pack nodes' page slots (k as [head][token][d], v as
 //            [head][d][token], transposed through LDS into 8-token runs)
-//   GELU     out[t][f] = GELU_tanh(D), or GELU_tanh(row_scale[t] D) with an
-//            RMSNorm of the input folded in (X then holds the raw rows)
+//   GELU     out[t][f] = GELU_tanh(D)
 //   RESIDUAL x[t][f] += D   (in place)
 //   STORE    out[t][f] = D
+// QKV, GELU and STORE can take an RMSNorm of the input rows folded in: X
+// then holds the raw rows and D[f][t] is first multiplied by row_scale[t].
 // QKV and STORE can also emit per-token sums of squares over each group of
 // 64 features, the first half of an RMSNorm over the feature axis (qk-norm);
 // norm_scale_kernel finishes it.  RESIDUAL can emit them for the rows it
-// writes, part-major; row_scale_kernel turns them into GELU's row_scale.
+// writes, part-major; row_scale_kernel turns them into a row_scale.
 // Work-group tile 256 (features) x BN (tokens: 256, 224, 192 or 128) x 64
 // (k), eight waves (2 x 4 of 128 x BN/4, or 4 x 2 of 64 x BN/2 at 224),
 // operands double-buffered in LDS with an XOR swizzle.  Each lane holds four consecutive features of one token, so RoPE
@@ -199,11 +200,11 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
       for (int fb = 0; fb < FB; ++fb) res[tb][fb] = *reinterpret_cast<const u32x2*>(orow + 16 * fb);
     }
   }
-  // The folded RMSNorm's per-token factors (GELU and QKV epilogues): lane j
-  // loads those of the wave's tokens j and j + 64 (two coalesced loads at
-  // most), also before the main loop; the epilogue takes each token's from
-  // its lane.
-  constexpr bool ROWPRE = EPI == EPI_GELU || EPI == EPI_QKV;
+  // The folded RMSNorm's per-token factors (every epilogue but RESIDUAL):
+  // lane j loads those of the wave's tokens j and j + 64 (two coalesced
+  // loads at most), also before the main loop; the epilogue takes each
+  // token's from its lane.
+  constexpr bool ROWPRE = EPI != EPI_RESIDUAL;
   constexpr int RT = ROWPRE ? (GWN + 63) / 64 : 1;
   float rtok[RT];
   if constexpr (ROWPRE) {
@@ -237,9 +238,10 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
 
   // epilogue: lane holds D[f][t] for t = t0 + wt + 16 tb + c16 and
   // f = f0 + wf + 16 fb + 4 lg + e (e = 0..3)
-  if constexpr (EPI == EPI_QKV) {
-    // the folded RMSNorm of the input rows: q, k and v are linear in the
-    // row, so its 1 / rms scales the accumulators before anything else
+  // The folded RMSNorm of the input rows: D is linear in the row, so the
+  // token's 1 / rms scales its accumulators before anything else (taken
+  // from the lane that loaded it while every lane is active).
+  if constexpr (ROWPRE) {
     if (ep.row_scale) {
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
@@ -250,6 +252,8 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
           for (int e = 0; e < 4; ++e) acc[fb][tb][e] *= r;
       }
     }
+  }
+  if constexpr (EPI == EPI_QKV) {
     // a 256-feature tile lies in one of q, k, v (hidden is a multiple of 256)
     // and each wave's 128 or 64 features in one head (head_dim 128)
     const int32_t sec = f0 / ep.hidden;
@@ -384,12 +388,6 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
       const int32_t t = t0 + wt + 16 * tb + c16;
-      // the folded RMSNorm's factor of token 16 tb + c16 of the wave, from
-      // the lane that loaded it (while every lane is active)
-      float rscale = 1.f;
-      if constexpr (ROWPRE) {
-        if (ep.row_scale) rscale = __shfl(rtok[tb >> 2], 16 * (tb & 3) + c16);
-      }
       if (t >= T) continue;  // uniform over the 4 lanes of a token, so the butterflies below stay inside it
       uint16_t* orow = ep.out + (size_t)t * ep.ld_out + f0 + wf + 4 * lg;
       float ssq[FB / FPG];
@@ -422,7 +420,7 @@ __global__ __launch_bounds__(G_THREADS, 1) void gemm_bf16_kernel(const uint16_t*
             v[3] += __uint_as_float(r.y & 0xffff0000u);
           } else if constexpr (EPI == EPI_GELU) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e] * rscale);
+            for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
           }
           u32x2 pk;
           pk.x = pack_bf16x2(v[0], v[1]);
@@ -519,8 +517,7 @@ int launch_gemm(int epi, int timer_kind, const uint16_t* W, const uint16_t* X, i
     return fail(SC_EUNSUPPORTED, "gemm operands beyond 4 GB");
   if (epi == EPI_QKV && (ep.hidden % GBM || ep.head_dim != GWM))
     return fail(SC_EUNSUPPORTED, "QKV epilogue needs hidden %% %d == 0 and head_dim %d", GBM, GWM);
-  if (ep.row_scale && epi != EPI_GELU && epi != EPI_QKV)
-    return fail(SC_EINVAL, "row_scale is a GELU or QKV epilogue input");
+  if (ep.row_scale && epi == EPI_RESIDUAL) return fail(SC_EINVAL, "row_scale is not a RESIDUAL epilogue input");
   GemmEpilogue e = ep;
   if (epi == EPI_QKV) {
     // v goes out in 16-byte runs of 8 tokens within one page

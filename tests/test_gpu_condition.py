@@ -86,7 +86,9 @@ RESIDENT = [(c, 0) for c in range(6)]
 # plain block's seven, plus q and k rounded again after the qk-norm (1); for
 # cross-attention its RMSNorm output, query, cached condition K/V, attention
 # output and residual (5); with its norms the query and the condition keys
-# rounded again after them (2).
+# rounded again after them (2).  Folded RMSNorms (the query's always, the
+# block's without modulation) never round their outputs, so these counts are
+# upper bounds.
 ROUNDINGS = {"qk": 8, "cross": 12, "cross_norm": 14, "all": 15}
 
 
