@@ -43,7 +43,7 @@ METRIC = "steady-state latent frames/s per DiT block + attention TFLOP/s (% bf16
 # read for a plain 256 MiB copy (x2.0 fetch, x1.0 write).  Valid only for the
 # kernel sources it was measured on (hash below); otherwise reported as null.
 ATTN_TRAFFIC = {"sources_sha1": "c261a262610c20a9c596a956e8688d36f375a5bb",
-                "fetch_bytes": 1.3526e+09, "write_bytes": 2.0062e+08}
+                "fetch_bytes": 1.3516e+09, "write_bytes": 2.0062e+08}
 
 
 def attn_traffic():
