@@ -21,10 +21,10 @@ import pytest
 import paper_2609_22283_amd as sc
 from oracle.pipeline import sampler_step
 from oracle.rope import chunk_positions, rope
-from synth import TAG_K, TAG_NOISE, TAG_V, TAG_X, normal
+from synth import TAG_K, TAG_NOISE, TAG_V, TAG_X, bf16_bits, normal
 from synth.configs import SHORT, SMALL, WAN, cfg3_same, cfg4_prog
 
-from block_inputs import X_SMALL, BlockInputs, branch_gate, oracle_traces, planted_must_fail
+from block_inputs import X_SMALL, BlockInputs, branch_gate, exact, oracle_traces, planted_must_fail
 from gpu_cases import bf16_gates, bits_to_device, from_device, sample_rows, to_device, torch_mod
 
 pytestmark = pytest.mark.gpu
@@ -231,6 +231,35 @@ def test_short_block_prog():
     want, _ = case.oracle()
     for i in range(len(pack)):
         block_gate(got[i], want[i], f"short node {pack[i]}")
+
+
+def test_small_block_extreme_rows():
+    """Rows at the ends of the RMSNorms' range, which the plain block folds
+    into its GEMMs as per-token factors: an all-zero input row (its factor
+    is 1 / sqrt(eps) = 1000 and every projection of it is zero) and a row
+    2^12 times larger than the others (exact in bf16; its normalised rows
+    equal the unscaled row's), through the block and its cached K/V,
+    against the oracle on the same values."""
+    kind, pack, resident = SMALL_BLOCK_PACKS[0]
+    case = BlockCase(SMALL, kind, pack, resident, seed=19)
+    n = SMALL.tokens_per_chunk
+    bits = case.inp.x_bits.copy()
+    bits[3] = 0                                                # node 0, row 3
+    bits[n + 5] = bf16_bits(exact(bits[n + 5]) * 4096.0)       # node 1, row 5
+    xv = exact(bits)
+    case.inp.x_bits = bits
+    case.inp.x = case.x = [xv[i * n:(i + 1) * n] for i in range(len(pack))]
+    case.x_dev = bits_to_device(bits)
+    got = case.run()
+    want, new_kv = case.oracle()
+    assert np.abs(want[1][5]).max() > 1000.0                   # the large row stays large
+    for i in range(len(pack)):
+        block_gate(got[i], want[i], f"extreme rows, node {pack[i]}")
+        k_got, v_got = read_pages(case.pool, SMALL, case.n_slots, case.cache.slots(pack[i]))
+        bf16_gates(k_got, new_kv[i][0], "cached K (extreme rows)")
+        bf16_gates(v_got, new_kv[i][1], "cached V (extreme rows)")
+    k0, v0 = read_pages(case.pool, SMALL, case.n_slots, case.cache.slots(pack[0]))
+    assert not np.any(k0[3]) and not np.any(v0[3])            # the zero row's K and V are zero
 
 
 def test_block_rejects_level_beyond_modulation_table():
