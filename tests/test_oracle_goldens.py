@@ -11,6 +11,9 @@
   at given (t, h, w) positions for the Wan split 44 / 42 / 42, theta 10000,
   pairs 0, 1, 2 and the last of each axis -- the frequency table
   pos * theta^(-2 i / d_a) and the pair-to-axis assignment.
+* ``golden/input_times_k4.txt``: the four denoising input times as the
+  paper's training configuration table prints them, per level, for the
+  sampler's schedule in the oracle and in bench.py's workloads.
 """
 import math
 import os
@@ -111,3 +114,24 @@ def test_rope_pair_angles_match_the_hand_table():
         assert min(diff, 2 * math.pi - diff) < 1e-9, (pos, a, i, got, ang)
         others = np.delete(y, [2 * p, 2 * p + 1])
         assert np.all(others == 0.0)                       # a rotation stays in its pair
+
+
+def test_input_times_match_paper_table():
+    """t_j of levels 0..4: the oracle's schedule and bench.py's, exactly."""
+    from fractions import Fraction
+
+    import bench
+    from oracle.pipeline import T_SCHEDULE_K4
+
+    want = {}
+    with open(os.path.join(GOLDEN, "input_times_k4.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            level, num, den = (int(v) for v in line.split())
+            want[level] = Fraction(num, den)
+    assert sorted(want) == [0, 1, 2, 3, 4]
+    for sched in (T_SCHEDULE_K4, bench.T_SCHEDULE_K4):
+        assert len(sched) == 5
+        for level, t in want.items():
+            assert sched[level] == float(t), (level, sched[level], t)
